@@ -1,0 +1,198 @@
+/*
+ * efsparse — error-feedback gradient sparsification on one AMD MI355X (gfx950).
+ *
+ * C ABI of the hot path of sparsified SGD with error feedback
+ * (Foroutan Eghlidi & Jaggi, "Sparse Communication for Training Deep
+ * Networks", Algorithm 1 and Section 3).  One worker step is
+ *
+ *     acc = g + e                      (Algorithm 1, accumulate step)
+ *     q   = C(acc)                     (Algorithm 1, compress step; Section 3:
+ *                                       top-k, random-k or block-random-k,
+ *                                       layer-wise or global scope)
+ *     e'  = acc with q's support set to +0.0
+ *                                      (Section 3 worker steps / Algorithm 1:
+ *                                       keep what was not sent)
+ *
+ * and the partner call sums W workers' messages into a dense vector in a fixed
+ * worker order (Algorithm 1, aggregate step), averaged over W by default.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Sizes: d is the gradient length, 1 <= d < 2^31.  A layout splits [0, d)
+ *    into n_seg contiguous segments (one per layer for layer-wise scope, one
+ *    in total for global scope; Section 3, sparsification scope).
+ *  - k per segment: k_l = clamp(floor(density * d_l + 0.5), 1, d_l), computed
+ *    in IEEE double; K = sum of k_l.  Segment l's message entries occupy
+ *    positions [P_l, P_l + k_l), P_l = k_0 + ... + k_{l-1}.
+ *  - Sparse message (top-k, random-k): idx uint32[K] (global element indices,
+ *    strictly ascending) and val float32[K] (acc at those indices, exact bits).
+ *  - Block message (block-random-k): start uint32[n_seg] (segment-local start
+ *    of the run) and val float32[K], val[P_l + t] = acc[o_l + (start_l + t)
+ *    mod d_l], t = 0..k_l-1.
+ *  - Memory: every pointer named g, e, acc, idx, val, start, out, ws is a
+ *    device pointer owned by the caller; the library never allocates device
+ *    memory and never synchronises the stream (ef_layout_bind excepted).
+ *    g, e, acc and out must be 16-byte aligned (8-byte for a bf16 g); idx,
+ *    val and start 4-byte aligned; ws 256-byte aligned.
+ *  - Streams: `stream` is a hipStream_t (NULL = the null stream).  All work
+ *    is enqueued on it, in order; results are ready when the stream is.
+ *  - Aliasing: only where stated (acc may equal e in ef_accumulate; e may
+ *    equal acc in ef_update).  Messages must not alias inputs.
+ *  - Errors: argument errors are detected on the host before anything is
+ *    enqueued and return a status below; launch failures return EF_EHIP.
+ *    No call throws, exits or prints.
+ *  - Threading: a bound layout is read-only and may be shared; concurrent
+ *    calls need distinct workspaces (or the same stream).
+ *  - Determinism: every output is bitwise reproducible for the same inputs,
+ *    independent of launch timing (integer atomics only; no float atomics).
+ */
+#ifndef EFSPARSE_H
+#define EFSPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define EF_OK 0
+#define EF_EINVAL 1     /* null / misaligned pointer, bad dtype or kind, density outside (0,1],
+                           block < 1, segment table not a strictly increasing partition of [0,d),
+                           layout not bound */
+#define EF_ERANGE 2     /* d == 0, d >= 2^31, n_seg < 1 or n_seg >= 2^24, W < 1 or W > 65536 */
+#define EF_EWORKSPACE 3 /* ws_bytes smaller than ef_workspace_bytes() */
+#define EF_EHIP 4       /* a HIP runtime or launch error */
+
+/* gradient dtypes */
+#define EF_F32 0
+#define EF_BF16 1
+
+/* workspace kinds for ef_workspace_bytes */
+#define EF_OP_TOPK 0
+#define EF_OP_RANDK 1
+#define EF_OP_RANDBLOCK 2
+#define EF_OP_AGG_SPARSE 3
+#define EF_OP_AGG_BLOCK 4
+
+/* message kinds */
+#define EF_MSG_SPARSE 0
+#define EF_MSG_BLOCK 1
+
+/* tuning knobs for ef_layout_tune: they size candidate lists and change speed only, never
+   results (a segment whose list cannot hold the answer takes the exact slow path) */
+#define EF_TUNE_RANDK_SIGMA 0  /* random-k candidate margin in standard deviations (default 10) */
+#define EF_TUNE_RANDK_EXTRA 1  /* random-k candidate margin, constant part (default 64) */
+#define EF_TUNE_TOPK_CAP_MULT 2  /* top-k candidate capacity: mult * k_l + extra (default 2) */
+#define EF_TUNE_TOPK_CAP_EXTRA 3 /* (default 65536) */
+#define EF_TUNE_RANDK_CAP_MULT 4 /* random-k candidate list capacity multiplier (default 1) */
+
+typedef struct ef_layout ef_layout;
+
+/* Human-readable name of a status code (static storage). */
+const char* ef_status_string(int status);
+
+/* Create a host-side layout (Section 3, sparsification scope).
+ *   d            gradient length, 1 <= d < 2^31
+ *   seg_offsets  host array of n_seg + 1 int64: 0 = o_0 < o_1 < ... < o_n_seg = d;
+ *                segment l is [o_l, o_{l+1}).  Copied; the caller keeps ownership.
+ *   density      k/d fraction in (0, 1] (Section 4.1 uses 1 %)
+ *   block        random-block start alignment b >= 1; a segment with d_l <= b uses 1
+ *   out          receives the new layout (unchanged on error)
+ * Returns EF_OK, EF_EINVAL or EF_ERANGE.  Pure host code. */
+int ef_layout_create(int64_t d, const int64_t* seg_offsets, int32_t n_seg, double density,
+                     int64_t block, ef_layout** out);
+int ef_layout_destroy(ef_layout* layout);
+
+/* K = sum of k_l; -1 for a null layout. */
+int64_t ef_layout_total_k(const ef_layout* layout);
+int32_t ef_layout_num_segments(const ef_layout* layout);
+/* Copies k_l for every segment into the host array k_out[n_seg]. */
+int ef_layout_segment_k(const ef_layout* layout, int64_t* k_out);
+
+/* Change a performance knob (EF_TUNE_*).  Must be called before ef_layout_bind. */
+int ef_layout_tune(ef_layout* layout, int knob, double value);
+
+/* Bytes of device memory the layout's tables need. */
+size_t ef_layout_device_bytes(const ef_layout* layout);
+/* Upload the layout's tables into caller-owned device memory `dev_tables`
+ * (>= ef_layout_device_bytes, 256-byte aligned), which must stay allocated
+ * while the layout is used.  Synchronises `stream` once (setup call). */
+int ef_layout_bind(ef_layout* layout, void* dev_tables, size_t bytes, void* stream);
+
+/* Workspace bytes an entry point needs: EF_OP_TOPK for compress_topk /
+ * ef_step_topk, EF_OP_RANDK for compress_randk / ef_step_randk,
+ * EF_OP_AGG_SPARSE / EF_OP_AGG_BLOCK for decompress_aggregate with W workers
+ * (W is ignored otherwise).  Random-block needs none (returns 0).
+ * Returns 0 for a null layout or unknown op. */
+size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W);
+
+/* Algorithm 1, accumulate step: acc_i = fl32(g_i + e_i) for all i < d.
+ *   g    f32[d] or bf16[d] (g_dtype EF_F32 / EF_BF16; bf16 widens exactly)
+ *   e    f32[d];  acc  f32[d], may equal e (in place). */
+int ef_accumulate(const ef_layout* layout, const void* g, int g_dtype, const float* e,
+                  float* acc, void* stream);
+
+/* Section 3, top-k: per segment, the k_l entries of acc with the largest
+ * magnitude (key = float bits with the sign cleared; equal keys go to the
+ * lower index), written as a sparse message (idx ascending, val = acc). */
+int compress_topk(const ef_layout* layout, const float* acc, uint32_t* idx, float* val,
+                  void* ws, size_t ws_bytes, void* stream);
+
+/* Section 3, random-k: per segment, the k_l positions j with the smallest
+ * Philox4x32-10 keys u_j (word j mod 4 of counter (j div 4, 0, step,
+ * 0x01000000 | l) under key (seed lo, seed hi); equal keys: lower j), as a
+ * sparse message.  Workers with equal seeds pick equal coordinates (the
+ * allReduce mode of Section 3), distinct seeds the allGather mode. */
+int compress_randk(const ef_layout* layout, const float* acc, uint64_t seed, uint32_t step,
+                   uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream);
+
+/* Section 3, block-random-k: per segment one random start s_l (aligned to
+ * b_l = b if d_l > b else 1; s_l = b_l * floor(r * n_l / 2^64), n_l =
+ * ceil(d_l / b_l), r = x0 + 2^32 x1 of Philox counter (0, 0, step,
+ * 0x02000000 | l)) and the k_l values that follow it, wrapping at the end of
+ * the segment, as a block message.  Needs no workspace. */
+int compress_randblock(const ef_layout* layout, const float* acc, uint64_t seed, uint32_t step,
+                       uint32_t* start, float* val, void* stream);
+
+/* Residual update (Section 3 worker steps; Algorithm 1): e_i = +0.0 where the
+ * message (msg_kind EF_MSG_SPARSE: idx[K]; EF_MSG_BLOCK: start[n_seg]) sent
+ * element i, else acc_i (bits unchanged).  e may equal acc. */
+int ef_update(const ef_layout* layout, const float* acc, int msg_kind, const uint32_t* idx_or_start,
+              float* e, void* stream);
+
+/* Algorithm 1, aggregate step: out_i = fl32(sum over w = 0..W-1 in order of
+ * the entries of message w at i, starting from +0.0), divided by W in IEEE
+ * float32 when average != 0 (the plain sum of Algorithm 1 when 0).
+ *   idx_or_start  uint32[W][K] (sparse) or uint32[W][n_seg] (block)
+ *   val           float32[W][K]
+ *   out           float32[d], written in full
+ * Sparse messages must hold valid ascending indices as produced by the
+ * compressors; entries that violate this are ignored, never written out of
+ * bounds. */
+int decompress_aggregate(const ef_layout* layout, int msg_kind, int32_t W,
+                         const uint32_t* idx_or_start, const float* val, int average, float* out,
+                         void* ws, size_t ws_bytes, void* stream);
+
+/* Fused worker steps: accumulate + compress + residual update in one call,
+ * bitwise identical to ef_accumulate(g, e -> e), compress_*(e), ef_update(e, e).
+ * e holds e_t on entry and e_{t+1} on return. */
+int ef_step_topk(const ef_layout* layout, const void* g, int g_dtype, float* e, uint32_t* idx,
+                 float* val, void* ws, size_t ws_bytes, void* stream);
+int ef_step_randk(const ef_layout* layout, const void* g, int g_dtype, float* e, uint64_t seed,
+                  uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream);
+int ef_step_randblock(const ef_layout* layout, const void* g, int g_dtype, float* e, uint64_t seed,
+                      uint32_t step, uint32_t* start, float* val, void* stream);
+
+/* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
+ * word that is 0 after a healthy call (bit 0: a bounded wait in a kernel
+ * timed out; bit 1: the slow exact path ran for at least one segment).
+ * Returns (size_t)-1 for other ops. */
+size_t ef_workspace_diag_offset(const ef_layout* layout, int op);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EFSPARSE_H */

@@ -1,0 +1,215 @@
+"""Python binding of libefsparse (error-feedback gradient sparsification on MI355X).
+
+Argument marshalling only: every step of the hot path runs in the HIP kernels of
+``libefsparse.so``; this module passes device pointers (``tensor.data_ptr()``),
+sizes and the current HIP stream across the C ABI declared in
+``include/efsparse.h``.  Function names match the C entry points.
+
+If the shared library has not been built, importing this package raises
+ImportError: there is no fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libefsparse.so")
+
+EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP = range(5)
+EF_F32, EF_BF16 = 0, 1
+EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK = range(5)
+EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
+EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_CAP_MULT, EF_TUNE_TOPK_CAP_EXTRA, EF_TUNE_RANDK_CAP_MULT = range(5)
+DIAG_SPIN_TIMEOUT, DIAG_SLOW_PATH = 1, 2
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2009_09271_amd.build` "
+                      "(or __graft_entry__.build()) first")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_c = ctypes
+_P = _c.c_void_p
+_SIGS = {
+    "ef_status_string": (_c.c_char_p, [_c.c_int]),
+    "ef_layout_create": (_c.c_int, [_c.c_int64, _P, _c.c_int32, _c.c_double, _c.c_int64, _c.POINTER(_P)]),
+    "ef_layout_destroy": (_c.c_int, [_P]),
+    "ef_layout_total_k": (_c.c_int64, [_P]),
+    "ef_layout_num_segments": (_c.c_int32, [_P]),
+    "ef_layout_segment_k": (_c.c_int, [_P, _P]),
+    "ef_layout_tune": (_c.c_int, [_P, _c.c_int, _c.c_double]),
+    "ef_layout_device_bytes": (_c.c_size_t, [_P]),
+    "ef_layout_bind": (_c.c_int, [_P, _P, _c.c_size_t, _P]),
+    "ef_workspace_bytes": (_c.c_size_t, [_P, _c.c_int, _c.c_int32]),
+    "ef_workspace_diag_offset": (_c.c_size_t, [_P, _c.c_int]),
+    "ef_accumulate": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P]),
+    "compress_topk": (_c.c_int, [_P, _P, _P, _P, _P, _c.c_size_t, _P]),
+    "compress_randk": (_c.c_int, [_P, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
+    "compress_randblock": (_c.c_int, [_P, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
+    "ef_update": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P]),
+    "decompress_aggregate": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_size_t, _P]),
+    "ef_step_topk": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randk": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randblock": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
+}
+for _name, (_res, _args) in _SIGS.items():
+    _f = getattr(_lib, _name)
+    _f.restype, _f.argtypes = _res, _args
+
+EXPORTED = tuple(_SIGS)
+
+
+class EfError(RuntimeError):
+    def __init__(self, code, where):
+        self.code = code
+        super().__init__(f"{where}: {_lib.ef_status_string(code).decode()}")
+
+
+def _check(code, where):
+    if code != EF_OK:
+        raise EfError(code, where)
+
+
+def _stream(t):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _gdt(g):
+    import torch
+    if g.dtype == torch.float32:
+        return EF_F32
+    if g.dtype == torch.bfloat16:
+        return EF_BF16
+    raise TypeError(f"gradient dtype {g.dtype} not supported (float32 or bfloat16)")
+
+
+class Layout:
+    """Segment table, density and block size of one gradient layout (host object).
+
+    ``seg_offsets``: [0, o_1, ..., d] (one segment per layer, or [0, d] for global scope).
+    ``bind(device)`` uploads its tables to device memory; compute calls need a bound layout.
+    """
+
+    def __init__(self, d, seg_offsets=None, density=0.01, block=1, tune=None):
+        offs = np.asarray([0, d] if seg_offsets is None else seg_offsets, dtype=np.int64)
+        self._offs = np.ascontiguousarray(offs)
+        h = ctypes.c_void_p()
+        _check(_lib.ef_layout_create(int(d), self._offs.ctypes.data, len(offs) - 1, float(density),
+                                     int(block), ctypes.byref(h)), "ef_layout_create")
+        self._h = h
+        self.d = int(d)
+        self.density = float(density)
+        self.block = int(block)
+        self.tables = None
+        for knob, value in (tune or {}).items():
+            _check(_lib.ef_layout_tune(self._h, int(knob), float(value)), "ef_layout_tune")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _lib.ef_layout_destroy(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def K(self) -> int:
+        return int(_lib.ef_layout_total_k(self._h))
+
+    @property
+    def n_seg(self) -> int:
+        return int(_lib.ef_layout_num_segments(self._h))
+
+    @property
+    def seg_offsets(self):
+        return self._offs.copy()
+
+    def segment_k(self):
+        out = np.zeros(self.n_seg, dtype=np.int64)
+        _check(_lib.ef_layout_segment_k(self._h, out.ctypes.data), "ef_layout_segment_k")
+        return out
+
+    def device_bytes(self) -> int:
+        return int(_lib.ef_layout_device_bytes(self._h))
+
+    def workspace_bytes(self, op, W=1) -> int:
+        return int(_lib.ef_workspace_bytes(self._h, int(op), int(W)))
+
+    def bind(self, device="cuda"):
+        import torch
+        n = max(self.device_bytes(), 256)
+        self.tables = torch.empty(n, dtype=torch.uint8, device=device)
+        _check(_lib.ef_layout_bind(self._h, _ptr(self.tables), n, _stream(self.tables)), "ef_layout_bind")
+        return self
+
+    def workspace(self, op, W=1, device="cuda"):
+        import torch
+        n = max(self.workspace_bytes(op, W), 256)
+        return torch.empty(n, dtype=torch.uint8, device=device)
+
+    def diag(self, ws, op) -> int:
+        """Diagnostics word of a top-k / random-k workspace (synchronises)."""
+        off = int(_lib.ef_workspace_diag_offset(self._h, int(op)))
+        return int(ws[off:off + 4].cpu().numpy().view(np.uint32)[0])
+
+
+def ef_accumulate(layout, g, e, acc):
+    _check(_lib.ef_accumulate(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(acc), _stream(e)), "ef_accumulate")
+
+
+def compress_topk(layout, acc, idx, val, ws):
+    _check(_lib.compress_topk(layout.handle, _ptr(acc), _ptr(idx), _ptr(val), _ptr(ws), ws.numel(), _stream(acc)),
+           "compress_topk")
+
+
+def compress_randk(layout, acc, seed, step, idx, val, ws):
+    _check(_lib.compress_randk(layout.handle, _ptr(acc), int(seed), int(step), _ptr(idx), _ptr(val), _ptr(ws),
+                               ws.numel(), _stream(acc)), "compress_randk")
+
+
+def compress_randblock(layout, acc, seed, step, start, val):
+    _check(_lib.compress_randblock(layout.handle, _ptr(acc), int(seed), int(step), _ptr(start), _ptr(val),
+                                   _stream(acc)), "compress_randblock")
+
+
+def ef_update(layout, acc, msg_kind, idx_or_start, e):
+    _check(_lib.ef_update(layout.handle, _ptr(acc), int(msg_kind), _ptr(idx_or_start), _ptr(e), _stream(e)),
+           "ef_update")
+
+
+def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, average=True):
+    n = ws.numel() if ws is not None else 0
+    _check(_lib.decompress_aggregate(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
+                                     1 if average else 0, _ptr(out), _ptr(ws), n, _stream(out)),
+           "decompress_aggregate")
+
+
+def ef_step_topk(layout, g, e, idx, val, ws):
+    _check(_lib.ef_step_topk(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val), _ptr(ws), ws.numel(),
+                             _stream(e)), "ef_step_topk")
+
+
+def ef_step_randk(layout, g, e, seed, step, idx, val, ws):
+    _check(_lib.ef_step_randk(layout.handle, _ptr(g), _gdt(g), _ptr(e), int(seed), int(step), _ptr(idx), _ptr(val),
+                              _ptr(ws), ws.numel(), _stream(e)), "ef_step_randk")
+
+
+def ef_step_randblock(layout, g, e, seed, step, start, val):
+    _check(_lib.ef_step_randblock(layout.handle, _ptr(g), _gdt(g), _ptr(e), int(seed), int(step), _ptr(start),
+                                  _ptr(val), _stream(e)), "ef_step_randblock")
+
+
+def lib():
+    """The loaded ctypes library (for contract tests)."""
+    return _lib

@@ -1,0 +1,124 @@
+"""GPU parity: accumulate, random-block and the aggregate against the CPU oracle
+(bit-exact), through the C ABI via the Python binding."""
+
+import numpy as np
+import pytest
+
+from efs_gpu import Case, announce, assert_f32_equal, assert_msg_equal, bits, dev, host
+from oracle import efsparse_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+LAYOUTS = [
+    [0, 1],
+    [0, 5],
+    [0, 1001],
+    [0, 8192],
+    [0, 8193],
+    [0, 100000],
+    [0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000],
+    [0, 3, 8190, 8195, 16384, 16385, 16386, 30000],
+]
+
+
+def _inputs(d, seed):
+    rng = np.random.default_rng(seed)
+    g = (rng.standard_normal(d) * 0.01).astype(np.float32)
+    e = (rng.standard_normal(d) * 0.003).astype(np.float32)
+    g[::97] = 0.0
+    e[::89] = -0.0
+    return g, e
+
+
+@pytest.mark.parametrize("offs", LAYOUTS, ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+def test_accumulate(offs):
+    import paper_2009_09271_amd as E
+    import torch
+    announce("accumulate", offs[-1], len(offs) - 1)
+    c = Case(offs, 0.1)
+    g, e = _inputs(c.d, 1)
+    acc = torch.empty(c.d, dtype=torch.float32, device="cuda")
+    E.ef_accumulate(c.L, dev(g), dev(e), acc)
+    assert_f32_equal(acc, O.ef_accumulate(g, e), "acc")
+    # bf16 gradient, in place
+    from workloads import to_bf16_bits
+    gb = to_bf16_bits(g)
+    ed = dev(e)
+    E.ef_accumulate(c.L, dev(gb).view(torch.bfloat16), ed, ed)
+    assert_f32_equal(ed, O.ef_accumulate(gb, e), "acc bf16 in place")
+
+
+@pytest.mark.parametrize("offs", LAYOUTS, ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+@pytest.mark.parametrize("block", [1, 2, 256, 1024])
+@pytest.mark.parametrize("rho", [0.01, 0.3, 1.0])
+def test_randblock_fused_and_composed(offs, block, rho):
+    announce("randblock", offs[-1], len(offs) - 1, block, rho)
+    c = Case(offs, rho, block)
+    g, e = _inputs(c.d, 2)
+    seed = (7 << 32) | 3
+    for step in range(3):
+        ed = dev(e)
+        st, val, _ = c.step("randblock", g, ed, seed, step)
+        (wst, wval), we = c.oracle_step("randblock", g, e, seed, step)
+        assert_msg_equal("randblock", (st, val), (wst, wval), f"step {step}")
+        assert_f32_equal(ed, we, f"e' step {step}")
+        ed2 = dev(e)
+        m2, val2 = c.step_composed("randblock", g, ed2, seed, step)
+        assert_msg_equal("randblock", (m2, val2), (wst, wval), f"composed step {step}")
+        assert_f32_equal(ed2, we, f"composed e' step {step}")
+        e = we
+
+
+def _agg_check(c, kind, msgs, W, average):
+    import paper_2009_09271_amd as E
+    import torch
+    out = torch.empty(c.d, dtype=torch.float32, device="cuda")
+    if kind == "sparse":
+        idx = np.stack([m[0] for m in msgs]).astype(np.uint32)
+        val = np.stack([m[1] for m in msgs]).astype(np.float32)
+        ws = c.L.workspace(E.EF_OP_AGG_SPARSE, W)
+        E.decompress_aggregate(c.L, E.EF_MSG_SPARSE, W, dev(idx.view(np.int32)), dev(val), out, ws, average)
+        want = O.decompress_aggregate_sparse(c.d, idx, val, average)
+    else:
+        st = np.stack([m[0] for m in msgs]).astype(np.uint32)
+        val = np.stack([m[1] for m in msgs]).astype(np.float32)
+        E.decompress_aggregate(c.L, E.EF_MSG_BLOCK, W, dev(st.view(np.int32)), dev(val), out, None, average)
+        want = O.decompress_aggregate_block(c.d, c.offs, c.ks, st, val, average)
+    assert_f32_equal(out, want, f"aggregate {kind} W={W} avg={average}")
+
+
+@pytest.mark.parametrize("offs", LAYOUTS[2:], ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+@pytest.mark.parametrize("W", [1, 3, 16])
+def test_aggregate_sparse_and_block(offs, W):
+    announce("aggregate", offs[-1], len(offs) - 1, W)
+    c = Case(offs, 0.05, 64)
+    rng = np.random.default_rng(W)
+    sparse, block = [], []
+    for w in range(W):
+        acc = (rng.standard_normal(c.d) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+        sparse.append(O.compress_randk(acc, c.offs, c.ks, 100 + w, 0))
+        block.append(O.compress_randblock(acc, c.offs, c.ks, 64, 100 + w, 0))
+    for average in (True, False):
+        _agg_check(c, "sparse", sparse, W, average)
+        _agg_check(c, "block", block, W, average)
+
+
+def test_aggregate_order_and_signed_zero():
+    """Worker order matters in float32 ((1 + 1e8) - 1e8 = 0); the sum starts at +0."""
+    announce("aggregate order")
+    c = Case([0, 8], 1.0)  # k = d = 8
+    msgs = []
+    vals = [[1.0] * 8, [1e8] * 8, [-1e8] * 8, [-0.0] * 8]
+    for v in vals:
+        msgs.append((np.arange(8, dtype=np.uint32), np.array(v, np.float32)))
+    _agg_check(c, "sparse", msgs, 4, False)
+    _agg_check(c, "sparse", msgs[3:], 1, True)
+
+
+def test_randblock_deterministic_and_shared_seed():
+    announce("randblock determinism")
+    c = Case([0, 50000, 123457], 0.01, 256)
+    g, e = _inputs(c.d, 5)
+    a = c.step("randblock", g, dev(e), 11, 4)
+    b = c.step("randblock", g, dev(e), 11, 4)
+    assert np.array_equal(host(a[0]), host(b[0])) and np.array_equal(bits(host(a[1])), bits(host(b[1])))

@@ -1,0 +1,124 @@
+"""GPU parity: fused and composed top-k / random-k worker steps against the CPU
+oracle, bit-exact (indices, values, residual), on ragged layouts, ties, signed
+zeros, bf16 gradients and the forced exact slow paths."""
+
+import numpy as np
+import pytest
+
+from efs_gpu import Case, announce, assert_f32_equal, assert_msg_equal, bits, dev, host
+
+pytestmark = pytest.mark.gpu
+
+LAYOUTS = [
+    [0, 1],
+    [0, 7],
+    [0, 1001],
+    [0, 8192],
+    [0, 8193],
+    [0, 100000],
+    [0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000],
+    [0, 3, 8190, 8195, 16384, 16385, 16386, 30000],
+    [0, 2, 6, 10, 14, 8200, 8204, 8300, 70000],
+]
+
+
+def _inputs(d, seed, ties=False):
+    rng = np.random.default_rng(seed)
+    if ties:  # few distinct magnitudes: many equal keys, both zeros
+        g = rng.choice(np.array([0.0, -0.0, 0.5, -0.5, 0.25, 1.0, -1.0, 2.0 ** -130], np.float32), size=d)
+        e = np.zeros(d, np.float32)
+        e[::3] = -0.0
+    else:
+        g = (rng.standard_normal(d) * 0.01).astype(np.float32)
+        e = (rng.standard_normal(d) * 0.003).astype(np.float32)
+        g[::97] = 0.0
+    return g, e
+
+
+def _run_steps(c, kind, g_list, e, seed=0, composed=True):
+    for step, g in enumerate(g_list):
+        ed = dev(e)
+        m, val, ws = c.step(kind, g, ed, seed, step)
+        (wm, wval), we = c.oracle_step(kind, g, e, seed, step)
+        assert_msg_equal(kind, (m, val), (wm, wval), f"{kind} step {step}")
+        assert_f32_equal(ed, we, f"{kind} e' step {step}")
+        diag = c.L.diag(ws, c.E.EF_OP_TOPK if kind == "topk" else c.E.EF_OP_RANDK)
+        assert diag & 1 == 0, "a bounded wait timed out"
+        if composed:
+            ed2 = dev(e)
+            m2, val2 = c.step_composed(kind, g, ed2, seed, step)
+            assert_msg_equal(kind, (m2, val2), (wm, wval), f"{kind} composed step {step}")
+            assert_f32_equal(ed2, we, f"{kind} composed e' step {step}")
+        e = we
+    return diag
+
+
+@pytest.mark.parametrize("offs", LAYOUTS, ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+@pytest.mark.parametrize("rho", [0.001, 0.01, 0.3, 1.0])
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_select_parity(kind, rho, offs):
+    announce(kind, offs[-1], len(offs) - 1, rho)
+    c = Case(offs, rho)
+    g0, e = _inputs(c.d, 3)
+    g1, _ = _inputs(c.d, 4)
+    _run_steps(c, kind, [g0, g1], e, seed=(5 << 32) | 9)
+
+
+@pytest.mark.parametrize("offs", LAYOUTS[2:], ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+@pytest.mark.parametrize("rho", [0.01, 0.5])
+def test_topk_ties_and_signed_zeros(rho, offs):
+    announce("topk ties", offs[-1], rho)
+    c = Case(offs, rho)
+    g, e = _inputs(c.d, 6, ties=True)
+    _run_steps(c, "topk", [g, g], e)
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_bf16_gradient(kind):
+    from workloads import to_bf16_bits
+    announce(kind, "bf16")
+    c = Case([0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000], 0.02)
+    g, e = _inputs(c.d, 7)
+    _run_steps(c, kind, [to_bf16_bits(g), to_bf16_bits(g * 3)], e, seed=42, composed=False)
+
+
+@pytest.mark.parametrize("offs", [[0, 100000], [0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000]],
+                         ids=["flat", "ragged"])
+def test_topk_forced_slow_path(offs):
+    import paper_2009_09271_amd as E
+    announce("topk slow", offs[-1])
+    c = Case(offs, 0.01, tune={E.EF_TUNE_TOPK_CAP_MULT: 0.0, E.EF_TUNE_TOPK_CAP_EXTRA: 0.0})
+    g, e = _inputs(c.d, 8)
+    diag = _run_steps(c, "topk", [g, g], e)
+    assert diag & 2, "the slow path did not run"
+
+
+@pytest.mark.parametrize("knob,value", [(0, -1e9), (4, 0.3)], ids=["underfill", "overflow"])
+def test_randk_forced_slow_path(knob, value):
+    announce("randk slow", knob, value)
+    c = Case([0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000, 100000], 0.01, tune={knob: value})
+    g, e = _inputs(c.d, 9)
+    diag = _run_steps(c, "randk", [g, g], e, seed=77)
+    assert diag & 2, "the slow path did not run"
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_deterministic_repeat(kind):
+    announce(kind, "repeat")
+    c = Case([0, 300000], 0.01)
+    g, e = _inputs(c.d, 10)
+    a = c.step(kind, g, dev(e), 3, 1)
+    b = c.step(kind, g, dev(e), 3, 1)
+    assert np.array_equal(host(a[0]), host(b[0])) and np.array_equal(bits(host(a[1])), bits(host(b[1])))
+
+
+def test_randk_shared_seed_same_coordinates():
+    announce("randk shared seed")
+    c = Case([0, 50000], 0.01)
+    g1, e = _inputs(c.d, 11)
+    g2, _ = _inputs(c.d, 12)
+    a = c.step("randk", g1, dev(e), 1 << 32, 5)
+    b = c.step("randk", g2, dev(e), 1 << 32, 5)
+    d_ = c.step("randk", g2, dev(e), (1 << 32) | 1, 5)
+    assert np.array_equal(host(a[0]), host(b[0]))
+    assert not np.array_equal(host(a[0]), host(d_[0]))
