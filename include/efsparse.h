@@ -93,6 +93,11 @@ typedef struct ef_layout ef_layout;
 /* Human-readable name of a status code (static storage). */
 const char* ef_status_string(int status);
 
+/* The hipError_t behind the calling thread's most recent EF_EHIP (0 if none),
+ * and its HIP description. */
+int ef_last_hip_error(void);
+const char* ef_last_hip_error_string(void);
+
 /* Create a host-side layout (Section 3, sparsification scope).
  *   d            gradient length, 1 <= d < 2^31
  *   seg_offsets  host array of n_seg + 1 int64: 0 = o_0 < o_1 < ... < o_n_seg = d;

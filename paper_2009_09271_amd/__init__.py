@@ -30,12 +30,21 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2009_09271_amd.build` "
                       "(or __graft_entry__.build()) first")
 
+# Load PyTorch first so that the library binds to the same HIP runtime that
+# allocates the tensors and owns the streams passed across the ABI.
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:  # host-only use (layout queries) works without it
+    _torch = None
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 _c = ctypes
 _P = _c.c_void_p
 _SIGS = {
     "ef_status_string": (_c.c_char_p, [_c.c_int]),
+    "ef_last_hip_error": (_c.c_int, []),
+    "ef_last_hip_error_string": (_c.c_char_p, []),
     "ef_layout_create": (_c.c_int, [_c.c_int64, _P, _c.c_int32, _c.c_double, _c.c_int64, _c.POINTER(_P)]),
     "ef_layout_destroy": (_c.c_int, [_P]),
     "ef_layout_total_k": (_c.c_int64, [_P]),
@@ -66,7 +75,10 @@ EXPORTED = tuple(_SIGS)
 class EfError(RuntimeError):
     def __init__(self, code, where):
         self.code = code
-        super().__init__(f"{where}: {_lib.ef_status_string(code).decode()}")
+        msg = f"{where}: {_lib.ef_status_string(code).decode()}"
+        if code == EF_EHIP:
+            msg += f" ({_lib.ef_last_hip_error()}: {_lib.ef_last_hip_error_string().decode()})"
+        super().__init__(msg)
 
 
 def _check(code, where):
@@ -115,7 +127,7 @@ class Layout:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and _lib is not None:
             _lib.ef_layout_destroy(h)
             self._h = None
 

@@ -221,7 +221,15 @@ WS make_ws(const WsLayout& l, void* base) {
 
 hipStream_t S(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
-int launched() { return hipGetLastError() == hipSuccess ? EF_OK : EF_EHIP; }
+thread_local int g_last_hip_error = 0;
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return EF_OK;
+  g_last_hip_error = (int)e;
+  return EF_EHIP;
+}
+
+int launched() { return hip_status(hipGetLastError()); }
 
 #define EF_TRY(x)              \
   do {                         \
@@ -335,6 +343,12 @@ const char* ef_status_string(int status) {
   }
 }
 
+int ef_last_hip_error(void) { return g_last_hip_error; }
+
+const char* ef_last_hip_error_string(void) {
+  return g_last_hip_error ? hipGetErrorString((hipError_t)g_last_hip_error) : "no HIP error";
+}
+
 int ef_layout_create(int64_t d, const int64_t* seg_offsets, int32_t n_seg, double density, int64_t block,
                      ef_layout** out) {
   if (!out || !seg_offsets) return EF_EINVAL;
@@ -391,9 +405,8 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   if (!L || !dev || !aligned(dev, kAlign)) return EF_EINVAL;
   if (bytes < L->blob.bytes.size()) return EF_EWORKSPACE;
   hipStream_t st = S(stream);
-  if (hipMemcpyAsync(dev, L->blob.bytes.data(), L->blob.bytes.size(), hipMemcpyHostToDevice, st) != hipSuccess)
-    return EF_EHIP;
-  if (hipStreamSynchronize(st) != hipSuccess) return EF_EHIP;
+  EF_TRY(hip_status(hipMemcpyAsync(dev, L->blob.bytes.data(), L->blob.bytes.size(), hipMemcpyHostToDevice, st)));
+  EF_TRY(hip_status(hipStreamSynchronize(st)));
   uint8_t* b = reinterpret_cast<uint8_t*>(dev);
   Tables& T = L->T;
   T.seg_off = reinterpret_cast<const int32_t*>(b + L->o_off);
