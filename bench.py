@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of the error-feedback sparsification hot path on one MI355X.
+
+One step = every simulated worker (W of them) runs one fused worker step
+(accumulate, compress, residual update) with each compressor variant, and the
+W messages of each variant are aggregated into a dense averaged gradient.
+Default workload: ResNet-50-shaped fp32 gradients (161 tensors, d = 25,557,032,
+Laplace values with per-tensor scales), density 0.1 %, W = 16, compressors
+top-k, random-k and block-random-k with start alignments 256 / 4096 / 65536,
+global (flat) scope.  Inputs are resident in HBM before the timed region.
+
+Prints ONE JSON line (see the design doc for every field).  `value` is compressed
+gradient elements per second over the whole step: n_variants * W * d elements
+per step.  `roofline` is for the kernel with the largest total time, timed
+per launch with HIP events the library records on the launch's stream.
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
+METRIC = "compressed gradient elements/s per compressor at 1 GPU; % of MI355X HBM BW"
+
+
+def _gen(args):
+    name, w, t = args
+    from workloads import WORKLOADS, gradient
+    return gradient(WORKLOADS[name], w, t)
+
+
+def gen_gradients(wl, W, t=0):
+    import multiprocessing as mp
+    n = max(1, min(8, os.cpu_count() or 1, W))
+    if n == 1:
+        return [_gen((wl.name, w, t)) for w in range(W)]
+    with mp.get_context("fork").Pool(n) as pool:
+        return pool.map(_gen, [(wl.name, w, t) for w in range(W)])
+
+
+def variant_list(spec, blocks):
+    out = []
+    for v in spec.split(","):
+        v = v.strip()
+        if v == "randblock":
+            out += [("randblock", b) for b in blocks]
+        elif v.startswith("randblock"):
+            out.append(("randblock", int(v[len("randblock"):])))
+        else:
+            out.append((v, 1))
+    return out
+
+
+def vname(v):
+    return v[0] if v[0] != "randblock" else f"randblock{v[1]}"
+
+
+def alg_bytes_op(kind, d, K, L, W):
+    """Algorithmic HBM bytes of one fused worker step (fp32 g) and of one aggregate."""
+    if kind in ("topk", "randk"):
+        step = 12 * d + 8 * K
+        agg = 4 * d + W * 8 * K
+    else:
+        step = 12 * d + 4 * K + 4 * L
+        agg = 4 * d + W * (4 * K + 4 * L)
+    return step, agg
+
+
+def kernel_alg_bytes(name, d, K, L, W):
+    """Algorithmic bytes per launch of the streaming kernels (None for small helpers)."""
+    if name.startswith("k_randblock_step"):
+        return 12 * d + 4 * K + 4 * L
+    if "k_topk_hist" in name or "k_randk_stream" in name:
+        return 12 * d
+    if name.startswith("k_topk_emit"):
+        return 4 * d
+    if name.startswith("k_agg_sparse"):
+        return 4 * d + W * 8 * K
+    if name.startswith("k_agg_block"):
+        return 4 * d + W * (4 * K + 4 * L)
+    return None
+
+
+def cpu_baseline(wl, offs, ks, variants, W, g0, budget_note):
+    """Time the CPU oracle on one worker's step per variant plus one aggregate per
+    variant, and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
+    from oracle import efsparse_oracle as O
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1):
+        return _cpu_baseline(O, wl, offs, ks, variants, W, g0, budget_note)
+
+
+def _cpu_baseline(O, wl, offs, ks, variants, W, g0, budget_note):
+    d = offs[-1]
+    e0 = np.zeros(d, np.float32)
+    t_steps, t_aggs, parts = 0.0, 0.0, []
+    from workloads import worker_seed
+    for kind, b in variants:
+        t0 = time.perf_counter()
+        (m, val), _ = O.ef_step(kind, g0, e0, offs, ks, seed=worker_seed(wl, 0), step=0, block=b)
+        t1 = time.perf_counter()
+        if kind == "randblock":
+            O.decompress_aggregate_block(d, offs, ks, [m] * W, [val] * W)
+        else:
+            O.decompress_aggregate_sparse(d, [m] * W, [val] * W)
+        t2 = time.perf_counter()
+        t_steps += t1 - t0
+        t_aggs += t2 - t1
+        parts.append(f"{vname((kind, b))} step {t1 - t0:.2f}s + aggregate {t2 - t1:.2f}s")
+    est_step_s = W * t_steps + t_aggs
+    value = len(variants) * W * d / est_step_s
+    return {
+        "value": value,
+        "unit": "elements/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"worker 0, step 0 of the same workload: one fused step per variant and one "
+                   f"aggregate of W={W} messages per variant ({'; '.join(parts)}); the step time is "
+                   f"scaled as W x steps + aggregates; NumPy, 1 thread{budget_note}"),
+        "measured_s": t_steps + t_aggs,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="resnet50")
+    ap.add_argument("--scope", default="flat", choices=["flat", "layer"])
+    ap.add_argument("--density", type=float, default=None)
+    ap.add_argument("--workers", type=int, default=None)
+    ap.add_argument("--variants", default="topk,randk,randblock")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(this build has no multi-GPU path; see DESIGN.md for how it would shard).", file=sys.stderr)
+        sys.exit(2)
+
+    from workloads import WORKLOADS, worker_seed
+    wl = WORKLOADS[args.workload]
+    W = args.workers or wl.W
+    density = args.density or wl.densities[0]
+    variants = variant_list(args.variants, wl.blocks)
+    offs = wl.seg_offsets(args.scope)
+    d = offs[-1]
+
+    t_gen = time.perf_counter()
+    grads = gen_gradients(wl, W)
+    t_gen = time.perf_counter() - t_gen
+
+    import torch
+    import paper_2009_09271_amd as E
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    layouts = {}
+    for kind, b in variants:
+        key = b if kind == "randblock" else 1
+        if key not in layouts:
+            layouts[key] = E.Layout(d, offs, density, key).bind(dev)
+    lay0 = next(iter(layouts.values()))
+    K, L = lay0.K, lay0.n_seg
+
+    g = [torch.from_numpy(x).to(dev) for x in grads]
+    e = {vname(v): [torch.zeros(d, dtype=torch.float32, device=dev) for _ in range(W)] for v in variants}
+    msg = {}
+    for v in variants:
+        n_m = L if v[0] == "randblock" else K
+        msg[vname(v)] = (torch.empty((W, n_m), dtype=torch.int32, device=dev),
+                         torch.empty((W, K), dtype=torch.float32, device=dev))
+    out = {vname(v): torch.empty(d, dtype=torch.float32, device=dev) for v in variants}
+    ws_topk = lay0.workspace(E.EF_OP_TOPK, 1, dev)
+    ws_randk = lay0.workspace(E.EF_OP_RANDK, 1, dev)
+    ws_agg = lay0.workspace(E.EF_OP_AGG_SPARSE, W, dev)
+
+    def run_variant(v, t):
+        kind, b = v
+        lay = layouts[b if kind == "randblock" else 1]
+        mi, mv = msg[vname(v)]
+        ev = e[vname(v)]
+        for w in range(W):
+            if kind == "topk":
+                E.ef_step_topk(lay, g[w], ev[w], mi[w], mv[w], ws_topk)
+            elif kind == "randk":
+                E.ef_step_randk(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], ws_randk)
+            else:
+                E.ef_step_randblock(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w])
+        kindm = E.EF_MSG_BLOCK if kind == "randblock" else E.EF_MSG_SPARSE
+        E.decompress_aggregate(lay, kindm, W, mi, mv, out[vname(v)], ws_agg if kindm == E.EF_MSG_SPARSE else None)
+
+    def run_step(t):
+        for v in variants:
+            run_variant(v, t)
+
+    step_no = 0
+    for _ in range(args.warmup):
+        run_step(step_no)
+        step_no += 1
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly `steps` steps --------------------------------------------------
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run_step(step_no)
+        step_no += 1
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    elems_per_step = len(variants) * W * d
+    value = elems_per_step / (ms_per_step / 1e3)
+
+    # ---- per-variant breakdown (events on the stream the library launches on) -----------------
+    per = {}
+    stream = torch.cuda.current_stream(dev)
+    for v in variants:
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            run_variant(v, step_no)
+            step_no += 1
+        b_.record(stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b_) / args.steps
+        step_b, agg_b = alg_bytes_op(v[0], d, K, L, W)
+        per[vname(v)] = {
+            "ms_per_step": round(ms, 4),
+            "elements_per_s": W * d / (ms / 1e3),
+            "alg_GB_per_step": round((W * step_b + agg_b) / 1e9, 4),
+            "alg_GBps": round((W * step_b + agg_b) / (ms / 1e3) / 1e9, 1),
+            "frac_of_hbm_peak": round((W * step_b + agg_b) / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+        }
+
+    # ---- per-kernel durations from library-recorded HIP events ---------------------------------
+    kernels, roofline = {}, None
+    if not args.no_kernel_timing:
+        E.timing_collect(reset=True)
+        E.timing_enable(True)
+        for _ in range(args.steps):
+            run_step(step_no)
+            step_no += 1
+        torch.cuda.synchronize()
+        E.timing_enable(False)
+        tm = E.timing_collect(reset=True)
+        for name, (tot_ms, n) in sorted(tm.items(), key=lambda kv: -kv[1][0]):
+            avg_us = tot_ms * 1e3 / n
+            ab = kernel_alg_bytes(name, d, K, L, W)
+            kernels[name] = {"avg_us": round(avg_us, 3), "launches": n, "total_ms": round(tot_ms, 3)}
+            if ab is not None:
+                kernels[name]["alg_bytes"] = ab
+                kernels[name]["alg_GBps"] = round(ab / (avg_us * 1e-6) / 1e9, 1)
+                kernels[name]["frac"] = round(ab / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        dom = next(iter(kernels))
+        ab = kernel_alg_bytes(dom, d, K, L, W)
+        if ab is not None:
+            achieved = ab / (kernels[dom]["avg_us"] * 1e-6) / 1e9
+            roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                        "alg_bytes_per_launch": ab, "avg_launch_us": kernels[dom]["avg_us"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        ks = [int(k) for k in lay0.segment_k()]
+        cpu = cpu_baseline(wl, offs, ks, variants, W, grads[0], "")
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "elements/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{wl.name}-shaped fp32 gradients ({len(wl.seg_offsets('layer')) - 1} tensors), "
+                         f"{args.scope} scope, d={d}, density {density}, W={W}, variants "
+                         f"{'/'.join(vname(v) for v in variants)}, one fused step per worker per variant "
+                         f"+ one aggregate per variant per step"),
+            "d": d, "segments": L, "K": K, "W": W, "density": density,
+            "variants": [vname(v) for v in variants], "scope": args.scope,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "per_compressor": per,
+        "kernels": kernels,
+        "input_generation_s": round(t_gen, 2),
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

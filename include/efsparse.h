@@ -61,7 +61,7 @@ extern "C" {
 #define EF_EINVAL 1     /* null / misaligned pointer, bad dtype or kind, density outside (0,1],
                            block < 1, segment table not a strictly increasing partition of [0,d),
                            layout not bound */
-#define EF_ERANGE 2     /* d == 0, d >= 2^31, n_seg < 1 or n_seg >= 2^24, W < 1 or W > 65536 */
+#define EF_ERANGE 2     /* d == 0, d >= 2^31, n_seg < 1 or n_seg >= 2^24, W < 1 or W > 65535 */
 #define EF_EWORKSPACE 3 /* ws_bytes smaller than ef_workspace_bytes() */
 #define EF_EHIP 4       /* a HIP runtime or launch error */
 
@@ -80,13 +80,13 @@ extern "C" {
 #define EF_MSG_SPARSE 0
 #define EF_MSG_BLOCK 1
 
-/* tuning knobs for ef_layout_tune: they size candidate lists and change speed only, never
-   results (a segment whose list cannot hold the answer takes the exact slow path) */
-#define EF_TUNE_RANDK_SIGMA 0  /* random-k candidate margin in standard deviations (default 10) */
-#define EF_TUNE_RANDK_EXTRA 1  /* random-k candidate margin, constant part (default 64) */
-#define EF_TUNE_TOPK_CAP_MULT 2  /* top-k candidate capacity: mult * k_l + extra (default 2) */
-#define EF_TUNE_TOPK_CAP_EXTRA 3 /* (default 65536) */
-#define EF_TUNE_RANDK_CAP_MULT 4 /* random-k candidate list capacity multiplier (default 1) */
+/* tuning knobs for ef_layout_tune: they size the candidate sets and change speed only, never
+   results (a segment whose candidates cannot contain the answer takes an exact whole-segment
+   path) */
+#define EF_TUNE_RANDK_SIGMA 0  /* random-k: candidate bound, standard deviations above k (default 10) */
+#define EF_TUNE_RANDK_EXTRA 1  /* random-k: candidate bound, constant margin (default 64) */
+#define EF_TUNE_TOPK_SIGMA 2   /* top-k: sampled threshold margin in standard deviations (default 6) */
+#define EF_TUNE_TOPK_EXTRA 3   /* top-k: sampled threshold margin, constant part (default 8) */
 
 typedef struct ef_layout ef_layout;
 
@@ -191,10 +191,23 @@ int ef_step_randblock(const ef_layout* layout, const void* g, int g_dtype, float
                       uint32_t step, uint32_t* start, float* val, void* stream);
 
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
- * word that is 0 after a healthy call (bit 0: a bounded wait in a kernel
- * timed out; bit 1: the slow exact path ran for at least one segment).
- * Returns (size_t)-1 for other ops. */
+ * word whose bit 1 is set when, for at least one segment, the candidates could
+ * not contain the answer and the exact whole-segment path ran instead (a
+ * slower path with the same result).  The word is only ever OR-ed: clear it to
+ * watch a given call.  Returns (size_t)-1 for other ops. */
 size_t ef_workspace_diag_offset(const ef_layout* layout, int op);
+
+/* Per-kernel timing (diagnostics).  While enabled, every kernel the library
+ * launches is bracketed by two HIP events recorded on the launch's stream.
+ * ef_timing_collect waits for the recorded events and adds each launch's
+ * duration to a per-kernel total; ef_timing_get reads total i (kernel name in
+ * static storage owned by the library, total milliseconds, launch count).
+ * Process-wide; intended for benchmarks, not for hot loops. */
+int ef_timing_enable(int enable);
+int ef_timing_collect(void);
+int ef_timing_count(void);
+int ef_timing_get(int i, const char** name, double* total_ms, int64_t* launches);
+int ef_timing_reset(void);
 
 #ifdef __cplusplus
 }

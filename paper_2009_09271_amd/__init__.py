@@ -17,14 +17,14 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libefsparse.so")
+LIB_PATH = os.environ.get("EFSPARSE_LIB") or os.path.join(_HERE, "libefsparse.so")
 
 EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP = range(5)
 EF_F32, EF_BF16 = 0, 1
 EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK = range(5)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
-EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_CAP_MULT, EF_TUNE_TOPK_CAP_EXTRA, EF_TUNE_RANDK_CAP_MULT = range(5)
-DIAG_SPIN_TIMEOUT, DIAG_SLOW_PATH = 1, 2
+EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA = range(4)
+DIAG_SLOW_PATH = 2
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2009_09271_amd.build` "
@@ -64,6 +64,12 @@ _SIGS = {
     "ef_step_topk": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randblock": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
+    "ef_timing_enable": (_c.c_int, [_c.c_int]),
+    "ef_timing_collect": (_c.c_int, []),
+    "ef_timing_count": (_c.c_int, []),
+    "ef_timing_get": (_c.c_int, [_c.c_int, _c.POINTER(_c.c_char_p), _c.POINTER(_c.c_double),
+                                 _c.POINTER(_c.c_int64)]),
+    "ef_timing_reset": (_c.c_int, []),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(_lib, _name)
@@ -166,9 +172,10 @@ class Layout:
         return self
 
     def workspace(self, op, W=1, device="cuda"):
+        """A zero-filled workspace (zeroed so that the diagnostics word starts clear)."""
         import torch
         n = max(self.workspace_bytes(op, W), 256)
-        return torch.empty(n, dtype=torch.uint8, device=device)
+        return torch.zeros(n, dtype=torch.uint8, device=device)
 
     def diag(self, ws, op) -> int:
         """Diagnostics word of a top-k / random-k workspace (synchronises)."""
@@ -225,3 +232,21 @@ def ef_step_randblock(layout, g, e, seed, step, start, val):
 def lib():
     """The loaded ctypes library (for contract tests)."""
     return _lib
+
+
+def timing_enable(on=True):
+    """Record HIP events around every library kernel launch (see ef_timing_enable)."""
+    _check(_lib.ef_timing_enable(1 if on else 0), "ef_timing_enable")
+
+
+def timing_collect(reset=True):
+    """Wait for recorded launches; return {kernel: (total_ms, launches)} and optionally reset."""
+    _check(_lib.ef_timing_collect(), "ef_timing_collect")
+    out = {}
+    for i in range(_lib.ef_timing_count()):
+        name, ms, n = ctypes.c_char_p(), ctypes.c_double(), ctypes.c_int64()
+        _check(_lib.ef_timing_get(i, ctypes.byref(name), ctypes.byref(ms), ctypes.byref(n)), "ef_timing_get")
+        out[name.value.decode()] = (ms.value, n.value)
+    if reset:
+        _lib.ef_timing_reset()
+    return out

@@ -1,20 +1,24 @@
 // HIP kernels of the efsparse hot path (gfx950).
 //
 // Streaming kernels walk the gradient in chunks of kTile elements (one workgroup per chunk,
-// kRounds float4 groups per thread, coalesced).  A chunk lies in one or more segments; the
-// common single-segment case takes uniform fast paths.
+// kRounds coalesced float4 groups per thread).  A chunk lies in one or more segments; the common
+// single-segment case takes uniform fast paths.
 //
-// Top-k (Section 3) is an exact radix selection on the 31-bit magnitude key:
-//   level 0  (bits 30:20) histogram fused into the accumulate pass      k_topk_hist
-//   level 1  (bits 19:10) over the candidate list, emitted in index
-//            order with a decoupled look-back                            k_topk_emit
-//   level 2  (bits 9:0)   over the list                                 k_list_level
-//   emission of the k_l winners in index order                           k_list_emit
-// Random-k (Section 3) draws Philox keys in the accumulate pass, keeps keys below a per-segment
-// bound as candidates (k_randk_stream), then resolves the exact k_l smallest keys on the list
-// (k_list_level) and emits them (k_list_emit).  A segment whose list cannot hold the answer is
-// resolved by an exact single-workgroup path over the whole segment.
-// Block-random-k (Section 3) is one fused streaming pass (k_randblock_step).
+// Top-k and random-k (Section 3) share one pipeline without any cross-workgroup synchronisation
+// inside a kernel:
+//   k_topk_sample   top-k only: per segment, a candidate threshold: exact (k-th largest key) for
+//                   segments of up to kSampleMax elements, otherwise from a sample of contiguous
+//                   runs spread over the segment, set so that the candidates very likely number
+//                   at least k_l.
+//   k_stream_sel    fused accumulate (acc = g + e, written to e) and candidate test (top-k: key >=
+//                   threshold; random-k: Philox key < tau_l, a binomial bound on k_l); every chunk
+//                   writes its candidates, in index order, to its own slot plus a count.
+//   k_select_emit   one workgroup per segment: gathers the segment's candidates, selects the k_l
+//                   winners exactly by radix levels (top-k: largest magnitude key; random-k:
+//                   smallest Philox key; ties to the lower index), writes them in index order to
+//                   the message and zeroes e there.  A segment with fewer than k_l candidates is
+//                   resolved exactly over all of its elements.
+// Block-random-k is one fused streaming pass (k_randblock_step).
 // The aggregate (Algorithm 1) accumulates each output tile in LDS in worker order.
 #pragma once
 
@@ -22,50 +26,43 @@
 
 namespace efs {
 
-struct WS {
-  uint32_t* diag;      // [1] diagnostics bits
-  uint32_t* tickets;   // [3] chunk tickets (stream / emit)
-  uint32_t* arrive;    // [3][L] per-level arrival counters
-  uint32_t* res;       // [L][kResWords]
-  uint32_t* cnt;       // [L] random-k candidate counts
-  uint32_t* hist;      // [3][L][kHBins]
-  uint64_t* st_stream; // [nchunks] look-back words of the streaming pass
-  uint64_t* st_emit;   // [n list chunks] look-back words of the emission
-  uint32_t* list_idx;  // [cap]
-  float* list_val;     // [cap]
-  uint32_t* list_key;  // [cap] random-k keys
+struct WSel {
+  uint32_t* diag;       // [4]   diagnostics bits
+  uint32_t* res;        // [L][kResWords]
+  uint32_t* counts;     // [nchunks] candidates per chunk
+  uint32_t* cofs;       // [2 * ncrows] per segment: compacted non-empty chunk rows (ids, flat offsets)
+  uint32_t* cand_idx;   // [nchunks * kTile] per-chunk candidate slots
+  float* cand_val;      // [nchunks * kTile]
+  uint32_t* cand_key;   // [nchunks * kTile] selection key' of each candidate
+  uint32_t* dense_idx;  // [d] candidates of segment l, gathered to [o_l, o_l + N_l)
+  float* dense_val;     // [d]
+  uint32_t* dense_key;  // [d]
 };
 
-__device__ __forceinline__ uint32_t* hist_row(const WS& w, int slot, int L, int l) {
-  return w.hist + ((size_t)slot * L + l) * kHBins;
-}
-__device__ __forceinline__ uint32_t* res_of(const WS& w, int l) { return w.res + (size_t)l * kResWords; }
+__device__ __forceinline__ uint32_t* res_of(const WSel& w, int l) { return w.res + (size_t)l * kResWords; }
 
 // ---------------------------------------------------------------------------------------------
 // Utility kernels
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_fill_zero(uint32_t* p, size_t nwords) {
-  const size_t n4 = nwords >> 2;
-  const size_t stride = (size_t)gridDim.x * kNT;
-  for (size_t i = (size_t)blockIdx.x * kNT + threadIdx.x; i < n4; i += stride)
-    reinterpret_cast<uint4*>(p)[i] = make_uint4(0, 0, 0, 0);
-  for (size_t i = (n4 << 2) + (size_t)blockIdx.x * kNT + threadIdx.x; i < nwords; i += stride) p[i] = 0;
-}
-
 // Algorithm 1 accumulate step: acc = g + e.
 template <int GDT>
 __global__ __launch_bounds__(kNT) void k_accumulate(int32_t d, const void* g, const float* e, float* acc) {
   const uint32_t lo = blockIdx.x * kTile, hi = min((uint32_t)d, lo + kTile);
+  float gv[kRounds][4], ev[kRounds][4];
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
-    float gv[4], ev[4], a[4];
-    load4g<GDT>(g, i0, nv, gv);
-    load4(e, i0, nv, ev);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    load4g<GDT>(g, i0, nv, gv[r]);
+    load4(e, i0, nv, ev[r]);
+  }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) a[q] = gv[q] + ev[q];
+  for (int r = 0; r < kRounds; ++r) {
+    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    float a[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[q] = gv[r][q] + ev[r][q];
     store4(acc, i0, nv, a);
   }
 }
@@ -75,8 +72,7 @@ __global__ __launch_bounds__(kNT) void k_copy(int32_t d, const float* src, float
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
     float v[4];
     load4(src, i0, nv, v);
     store4(dst, i0, nv, v);
@@ -126,17 +122,22 @@ __global__ __launch_bounds__(kNT) void k_randblock_step(Tables T, const void* g,
   const bool uni = sf == sl;
   RunSeg rs = run_seg(T, sf, step, s0, s1);
   int cur = sf;
+  float gv[kRounds][4], ev[kRounds][4];
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
-    float gv[4], ev[4], out[4];
-    load4g<GDT>(g, i0, nv, gv);
-    load4(e, i0, nv, ev);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    load4g<GDT>(g, i0, nv, gv[r]);
+    load4(e, i0, nv, ev[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    float out[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float a = gv[q] + ev[q];
+      const float a = gv[r][q] + ev[r][q];
       out[q] = a;
       if (q < nv) {
         const uint32_t i = i0 + q;
@@ -201,8 +202,7 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
     float v[4];
     load4(acc, i0, nv, v);
 #pragma unroll
@@ -225,18 +225,19 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 // output tile of kTile elements accumulates in LDS; a barrier separates consecutive workers.
 // ---------------------------------------------------------------------------------------------
 // tile_start[w][tau] = first entry of message w whose index lies in tile >= tau (tau = 0..nt).
-__global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t W, int32_t K, int32_t nt,
-                                                    const uint32_t* idx, uint32_t* tile_start) {
-  const size_t gid = (size_t)blockIdx.x * kNT + threadIdx.x;
-  if (gid >= (size_t)W * K) return;
-  const int w = (int)(gid / (uint32_t)K), j = (int)(gid % (uint32_t)K);
+// Grid: (ceil(K / kNT), W).
+__global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
+                                                    uint32_t* tile_start) {
+  const uint32_t j = blockIdx.x * kNT + threadIdx.x;
+  const int w = blockIdx.y;
+  if (j >= (uint32_t)K) return;
   const uint32_t* m = idx + (size_t)w * K;
   uint32_t* ts = tile_start + (size_t)w * (nt + 1);
   auto tile = [&](uint32_t i) -> int { return i < (uint32_t)d ? (int)(i / kTile) : nt; };
   const int tj = tile(m[j]);
   const int tp = j == 0 ? -1 : tile(m[j - 1]);
-  for (int tau = tp + 1; tau <= tj; ++tau) ts[tau] = (uint32_t)j;
-  if (j == K - 1)
+  for (int tau = tp + 1; tau <= tj; ++tau) ts[tau] = j;
+  if (j == (uint32_t)K - 1)
     for (int tau = tj + 1; tau <= nt; ++tau) ts[tau] = (uint32_t)K;
 }
 
@@ -246,8 +247,7 @@ __device__ __forceinline__ void agg_write(float* out, uint32_t lo, uint32_t hi, 
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t x = (uint32_t)(r * kNT + threadIdx.x) * 4u;
     const uint32_t i0 = lo + x;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
     float v[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(acc[x + q], fW) : acc[x + q];
@@ -306,470 +306,332 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
 }
 
 // ---------------------------------------------------------------------------------------------
-// Shared pieces of the selection kernels
+// Selection pipeline (top-k, random-k)
+// KIND 0 = top-k: key' = magnitude bits of the value, the k largest are sent.
+// KIND 1 = random-k: key' = ~Philox key, so the k smallest random keys have the largest key'.
+// Among equal key', lower indices are sent first.
 // ---------------------------------------------------------------------------------------------
-// Arrival at the end of a pass: every chunk counts itself in for each segment it touched; the
-// chunk that completes a segment's count runs `fn(l)` (block-wide) for it.
-template <typename F>
-__device__ void arrive_and_resolve(uint32_t* arrive, const int32_t* total, int sf, int sl, F fn) {
-  __shared__ uint32_t last[kNT];
-  __threadfence();
-  __syncthreads();
-  for (int base = sf; base <= sl; base += kNT) {
-    const int l = base + (int)threadIdx.x;
-    uint32_t is_last = 0;
-    if (l <= sl) is_last = atomicAdd(arrive + l, 1u) == (uint32_t)total[l] - 1u;
-    last[threadIdx.x] = is_last;
-    __syncthreads();
-    const int n = min(kNT, sl - base + 1);
-    for (int t = 0; t < n; ++t) {
-      if (last[t]) {
-        __threadfence();
-        fn(base + t);
-      }
-    }
-    __syncthreads();
-  }
+template <int KIND>
+__device__ __forceinline__ uint32_t sel_key(uint32_t idx, float val, uint32_t o, int l, uint32_t step,
+                                            uint32_t s0, uint32_t s1) {
+  if constexpr (KIND == 0) return mag_key(val);
+  else return ~randk_key(idx - o, (uint32_t)l, step, s0, s1);
 }
 
-// Exclusive prefix (within the chunk) of flags at element position x, from the per-group table
-// gp[g] = (prefix of the group << 4) | (flag bits of its 4 elements).
-__device__ __forceinline__ uint32_t chunk_prefix(const uint32_t* gp, uint32_t x, uint32_t ngroups, uint32_t total) {
-  const uint32_t g = x >> 2;
-  if (g >= ngroups) return total;
-  const uint32_t v = gp[g];
-  return (v >> 4) + __popc(v & ((1u << (x & 3)) - 1u));
-}
+constexpr int kBatch = 8;             // independent loads in flight per thread in the selection passes
+constexpr uint32_t kKeysLds = 28672;   // candidate keys held in LDS (larger sets stay in global memory)
+constexpr uint32_t kCofsLds = 4096;    // chunk rows whose flat offsets stay in LDS
 
-// Shared tail of the candidate-emitting streaming passes (top-k level-1 list, random-k
-// candidates): given per-element flags for the thread's kRounds groups, computes index-ordered
-// list positions per segment (prefix within the chunk + look-back across chunks).
-struct EmitCtx {
-  uint32_t c, lo, hi;
-  int sf, sl;
-  uint32_t excl_sf;   // count of the segment sf's flagged elements in earlier chunks
-};
-
-__device__ void ordered_positions(const Tables& T, uint64_t* status, uint32_t* diag, EmitCtx& E,
-                                  const uint32_t (&mask)[kRounds], uint32_t (&gpre)[kRounds],
-                                  uint32_t* gp, uint32_t* lds, uint32_t& total_out) {
-  __shared__ uint32_t s_excl;
-  uint32_t base = 0;
+// Workgroup-wide AND and OR of per-thread values; `lds` holds 2 * kSelNT / 64 words.
+__device__ __forceinline__ void block_and_or(uint32_t& a, uint32_t& o, uint32_t* lds) {
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan((uint32_t)__popc(mask[r]), lds, tot);
-    gpre[r] = base + ex;
-    gp[r * kNT + threadIdx.x] = ((base + ex) << 4) | mask[r];
-    base += tot;
+  for (int s = 32; s > 0; s >>= 1) {
+    a &= __shfl_xor(a, s, 64);
+    o |= __shfl_xor(o, s, 64);
+  }
+  constexpr int nw = kSelNT / 64;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  if (lane == 0) {
+    lds[wid] = a;
+    lds[nw + wid] = o;
   }
   __syncthreads();
-  const uint32_t total = base;
-  total_out = total;
-  const uint32_t ngroups = kTile / 4;
-  const uint32_t o_sl = (uint32_t)T.seg_off[E.sl];
-  const uint32_t start_sl = max(o_sl, E.lo);
-  const uint32_t cnt_sl = total - chunk_prefix(gp, start_sl - E.lo, ngroups, total);
-  const bool sl_cont = o_sl < E.lo;             // segment sl began in an earlier chunk (so sf == sl)
-  const uint32_t o_sf = (uint32_t)T.seg_off[E.sf];
-  const bool need_lb = o_sf < E.lo;
-  if (threadIdx.x == 0) {
-    lb_publish(status + E.c, sl_cont ? 1u : 2u, cnt_sl, 0u);
-    s_excl = 0;
+  a = 0xFFFFFFFFu;
+  o = 0u;
+#pragma unroll
+  for (int w = 0; w < nw; ++w) {
+    a &= lds[w];
+    o |= lds[nw + w];
   }
-  if (need_lb && threadIdx.x < 64) {
-    uint32_t ea, eb;
-    lb_lookback(status, (int)E.c, (int)(o_sf / kTile), ea, eb, diag);
-    if (threadIdx.x == 0) {
-      s_excl = ea;
-      if (sl_cont) lb_publish(status + E.c, 2u, ea + cnt_sl, 0u);
+  __syncthreads();
+}
+
+// Calls fn(key) for every keys[f], f < n, in a strided order with kBatch loads in flight.
+template <typename F>
+__device__ __forceinline__ void for_keys(const uint32_t* keys, uint32_t n, F fn) {
+  for (uint32_t base = 0; base < n; base += (uint32_t)kSelNT * kBatch) {
+    uint32_t k[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t f = base + (uint32_t)u * kSelNT + threadIdx.x;
+      k[u] = f < n ? keys[f] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t f = base + (uint32_t)u * kSelNT + threadIdx.x;
+      if (f < n) fn(k[u]);
     }
   }
-  __syncthreads();
-  E.excl_sf = s_excl;
 }
 
-// Position inside segment l's list of the flagged element at chunk offset x.
-__device__ __forceinline__ uint32_t list_pos(const Tables& T, const EmitCtx& E, const uint32_t* gp, int l,
-                                             uint32_t x_prefix, uint32_t total) {
-  if (E.sf == E.sl) return E.excl_sf + x_prefix;
-  const uint32_t o = (uint32_t)T.seg_off[l];
-  const uint32_t start = max(o, E.lo);
-  const uint32_t sp = chunk_prefix(gp, start - E.lo, kTile / 4, total);
-  return (l == E.sf ? E.excl_sf : 0u) + x_prefix - sp;
+// Radix selection of the need-th largest of n keys: returns T and r such that the winners are
+// the keys > T plus the first r keys == T.  kand / kor are the AND and OR of all keys; the levels
+// (11 bits each) start at the highest bit in which the keys differ, so concentrated keys still
+// spread over the histogram.
+__device__ void block_select(const uint32_t* keys, uint32_t n, uint32_t need, uint32_t kand, uint32_t kor,
+                             uint32_t* hist, uint32_t* lds, uint32_t& T_out, uint32_t& r_out) {
+  const uint32_t diff = kand ^ kor;
+  if (diff == 0) {  // all keys equal
+    T_out = kand;
+    r_out = need;
+    return;
+  }
+  const int h = 31 - __clz(diff);
+  uint32_t prefix = h == 31 ? 0u : (kand & (0xFFFFFFFFu << (h + 1)));
+  int known = 31 - h;
+  while (known < 32) {
+    const int w = min(11, 32 - known);
+    const int shift = 32 - known - w;
+    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
+    __syncthreads();
+    const uint32_t pmask = known == 0 ? 0u : (0xFFFFFFFFu << (32 - known));
+    const uint32_t want = prefix & pmask;
+    for_keys(keys, n, [&](uint32_t k) {
+      if ((k & pmask) == want) atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u);
+    });
+    __syncthreads();
+    uint32_t above;
+    const int bin = block_resolve<kSelNT>(hist, 1 << w, need, lds, above);
+    prefix |= (uint32_t)max(bin, 0) << shift;
+    need -= above;
+    known += w;
+  }
+  T_out = prefix;
+  r_out = need;
 }
 
-// Count of flagged elements of segment l inside the chunk.
-__device__ __forceinline__ uint32_t chunk_count(const Tables& T, const EmitCtx& E, const uint32_t* gp, int l,
-                                                uint32_t total) {
-  const uint32_t o = (uint32_t)T.seg_off[l], e = (uint32_t)T.seg_off[l + 1];
-  const uint32_t a = max(o, E.lo), b = min(e, E.hi);
-  return chunk_prefix(gp, b - E.lo, kTile / 4, total) - chunk_prefix(gp, a - E.lo, kTile / 4, total);
-}
-
-// ---------------------------------------------------------------------------------------------
-// Top-k level 0: fused accumulate + histogram of bits 30:20 of the magnitude key.
-// ---------------------------------------------------------------------------------------------
+// Top-k candidate threshold per segment (one workgroup per segment): the lower edge of the
+// 11-bit histogram bin (starting at the highest bit in which the sampled keys differ) that holds
+// the rank-th largest sampled key.  Exact k-th largest key when the whole segment fits the sample.
 template <int GDT, bool FUSED>
-__global__ __launch_bounds__(kNT) void k_topk_hist(Tables T, const void* g, const float* src, float* acc_out,
-                                                   WS ws) {
+__global__ __launch_bounds__(kSelNT) void k_topk_sample(Tables T, const void* g, const float* src, WSel ws) {
+  constexpr uint32_t runs = kSampleMax / kSampleRun;
+  __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[kHBins];
-  __shared__ uint32_t lds[kWaves];
+  __shared__ uint32_t lds[2 * kSelNT / 64];
+  __shared__ uint32_t run_start[runs];
+  const int l = blockIdx.x;
+  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
+  EFS_PHASE(8);
+  constexpr int per = kSampleMax / kSelNT;
+  const bool exact = n <= (uint32_t)kSampleMax;
+  const uint32_t m = exact ? n : (uint32_t)kSampleMax;
+  const uint32_t rank = exact ? (uint32_t)T.seg_k[l] : (uint32_t)T.seg_srank[l];
+  // runs of kSampleRun contiguous elements, evenly spaced over the segment
+  if (!exact && threadIdx.x < runs)
+    run_start[threadIdx.x] = o + (uint32_t)(((uint64_t)threadIdx.x * (n - kSampleRun)) / (runs - 1));
+  __syncthreads();
+  float a[per];
+#pragma unroll
+  for (int u = 0; u < per; ++u) {
+    const uint32_t j = (uint32_t)(u * kSelNT) + threadIdx.x;
+    const uint32_t i = exact ? o + j : run_start[j / kSampleRun] + j % kSampleRun;
+    a[u] = 0.0f;
+    if (j < m) {
+      if constexpr (FUSED) a[u] = load1g<GDT>(g, i) + src[i];
+      else a[u] = src[i];
+    }
+  }
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+#pragma unroll
+  for (int u = 0; u < per; ++u) {
+    const uint32_t j = (uint32_t)(u * kSelNT) + threadIdx.x;
+    if (j < m) {
+      const uint32_t k = mag_key(a[u]);
+      keys[j] = k;
+      kand &= k;
+      kor |= k;
+    }
+  }
+  block_and_or(kand, kor, lds);
+  EFS_PHASE(9);
+  uint32_t thr;
+  if (exact) {
+    uint32_t r_unused;
+    block_select(keys, m, rank, kand, kor, hist, lds, thr, r_unused);
+  } else if (kand == kor) {
+    thr = kand;
+  } else {
+    const int h = 31 - __clz(kand ^ kor);
+    const int w = min(11, h + 1), shift = h + 1 - w;
+    const uint32_t prefix = h == 31 ? 0u : (kand & (0xFFFFFFFFu << (h + 1)));
+    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
+    __syncthreads();
+    for_keys(keys, m, [&](uint32_t k) { atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u); });
+    __syncthreads();
+    uint32_t above;
+    const int bin = block_resolve<kSelNT>(hist, 1 << w, rank, lds, above);
+    thr = prefix | ((uint32_t)max(bin, 0) << shift);
+  }
+  EFS_PHASE(11);
+  if (threadIdx.x == 0) res_of(ws, l)[R_THR] = thr;
+}
+
+// Fused accumulate + candidate test + per-chunk ordered compaction into the chunk's slot.
+template <int KIND, int GDT, bool FUSED>
+__global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
+                                                    uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
+  __shared__ uint32_t wt[kRounds][kNT / 64];
   const uint32_t c = blockIdx.x;
   const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
   const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
   const bool uni = sf == sl;
-  for (int b = threadIdx.x; b < kHBins; b += kNT) hist[b] = 0;
-  __syncthreads();
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const uint32_t o_u = (uint32_t)T.seg_off[sf];
+  uint32_t thr_u = 0;
+  uint64_t tau_u = 0;
+  if constexpr (KIND == 0) thr_u = res_of(ws, sf)[R_THR];
+  else tau_u = T.seg_tau[sf];
+  const bool aligned = uni && (o_u & 3u) == 0;
+
+  float v[kRounds][4];
+  if constexpr (FUSED) {
+    float gv[kRounds][4];
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+      load4g<GDT>(g, i0, nv, gv[r]);
+      load4(src, i0, nv, v[r]);
+    }
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
+      store4(acc_out, i0, nv, v[r]);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+      load4(src, i0, nv, v[r]);
+    }
+  }
+  // candidate flags; wave-level prefixes through ballots, one barrier for the whole chunk
+  uint32_t mask[kRounds], lpre[kRounds];
+  uint32_t kk[kRounds][4];  // key' of each element (random-k: ~Philox key)
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    if (i0 >= hi) break;
-    const int nv = (int)min(4u, hi - i0);
-    float a[4];
-    if constexpr (FUSED) {
-      float gv[4], ev[4];
-      load4g<GDT>(g, i0, nv, gv);
-      load4(src, i0, nv, ev);
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    uint32_t mk = 0;
+    if constexpr (KIND == 0) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) a[q] = gv[q] + ev[q];
-      store4(acc_out, i0, nv, a);
+      for (int q = 0; q < 4; ++q) {
+        kk[r][q] = mag_key(v[r][q]);
+        if (q < nv) {
+          uint32_t thr = thr_u;
+          if (!uni) thr = res_of(ws, seg_of(i0 + q, sf, sl, T.seg_off))[R_THR];
+          if (kk[r][q] >= thr) mk |= 1u << q;
+        }
+      }
     } else {
-      load4(src, i0, nv, a);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < nv) {
-        const uint32_t bin = mag_key(a[q]) >> 20;
-        if (uni) {
-          atomicAdd(&hist[bin], 1u);
-        } else {
-          const int l = seg_of(i0 + q, sf, sl, T.seg_off);
-          atomicAdd(hist_row(ws, 0, T.L, l) + bin, 1u);
-        }
-      }
-    }
-  }
-  __syncthreads();
-  if (uni) {
-    uint32_t* row = hist_row(ws, 0, T.L, sf);
-    for (int b = threadIdx.x; b < kHBins; b += kNT) {
-      const uint32_t v = hist[b];
-      if (v) atomicAdd(row + b, v);
-    }
-  }
-  arrive_and_resolve(ws.arrive, T.seg_nchunks, sf, sl, [&](int l) {
-    const uint32_t need = (uint32_t)T.seg_k[l];
-    const uint32_t* row = hist_row(ws, 0, T.L, l);
-    uint32_t above;
-    int bin = block_resolve<true>(row, kHBins, need, lds, above);
-    if (threadIdx.x == 0) {
-      uint32_t* R = res_of(ws, l);
-      if (bin < 0) {  // cannot happen: the row holds all d_l >= k_l elements
-        atomicOr(ws.diag, kDiagSpinTimeout);
-        bin = 0;
-      }
-      const uint32_t nb = ld_acq(row + bin);
-      const uint32_t cnt = above + nb;
-      const uint32_t cap = (uint32_t)(T.tk_base[l + 1] - T.tk_base[l]);
-      R[R_PREFIX] = (uint32_t)bin << 20;
-      R[R_KNOWN] = 12;
-      R[R_NEED] = need - above;
-      R[R_ABOVE0] = above;
-      R[R_CNT] = cnt;
-      R[R_SLOW] = cnt > cap ? 1u : 0u;
-      if (cnt > cap) atomicOr(ws.diag, kDiagSlowPath);
-    }
-  });
-}
-
-// ---------------------------------------------------------------------------------------------
-// Top-k level 1: emit every element whose key is at or above the level-0 bin into the
-// segment's list (index order) and histogram bits 19:10 of those inside the bin.
-// ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kNT) void k_topk_emit(Tables T, const float* acc, WS ws) {
-  __shared__ uint32_t gp[kTile / 4];
-  __shared__ uint32_t lds[kWaves];
-  __shared__ uint32_t s_c;
-  if (threadIdx.x == 0) s_c = atomicAdd(ws.tickets + 0, 1u);
-  __syncthreads();
-  EmitCtx E;
-  E.c = s_c;
-  E.lo = E.c * kTile;
-  E.hi = min((uint32_t)T.d, E.lo + kTile);
-  E.sf = T.chunk_sf[E.c];
-  E.sl = T.chunk_sl[E.c];
-  const bool uni = E.sf == E.sl;
-  uint32_t thr_u = 0, slow_u = 1;
-  if (uni) {
-    const uint32_t* R = res_of(ws, E.sf);
-    thr_u = R[R_PREFIX];
-    slow_u = R[R_SLOW];
-  }
-  float v[kRounds][4];
-  uint32_t mask[kRounds], gpre[kRounds];
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = E.lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < E.hi ? (int)min(4u, E.hi - i0) : 0;
-    mask[r] = 0;
-    if (nv > 0) load4(acc, i0, nv, v[r]);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < nv) {
-        uint32_t thr = thr_u, slow = slow_u;
-        if (!uni) {
-          const uint32_t* R = res_of(ws, seg_of(i0 + q, E.sf, E.sl, T.seg_off));
-          thr = R[R_PREFIX];
-          slow = R[R_SLOW];
-        }
-        if (!slow && mag_key(v[r][q]) >= thr) mask[r] |= 1u << q;
-      }
-    }
-  }
-  uint32_t total;
-  ordered_positions(T, ws.st_stream, ws.diag, E, mask, gpre, gp, lds, total);
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    if (!mask[r]) continue;
-    const uint32_t i0 = E.lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    uint32_t pre = gpre[r];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (mask[r] & (1u << q)) {
-        const uint32_t i = i0 + q;
-        const int l = uni ? E.sf : seg_of(i, E.sf, E.sl, T.seg_off);
-        const uint32_t pos = list_pos(T, E, gp, l, pre, total);
-        const uint32_t at = (uint32_t)T.tk_base[l] + pos;
-        if (at < (uint32_t)T.tk_base[l + 1]) {
-          ws.list_idx[at] = i;
-          ws.list_val[at] = v[r][q];
-        }
-        const uint32_t key = mag_key(v[r][q]);
-        const uint32_t* R = res_of(ws, l);
-        if ((key >> 20) == (R[R_PREFIX] >> 20)) atomicAdd(hist_row(ws, 1, T.L, l) + ((key >> 10) & 1023u), 1u);
-        ++pre;
-      }
-    }
-  }
-  arrive_and_resolve(ws.arrive + T.L, T.seg_nchunks, E.sf, E.sl, [&](int l) {
-    uint32_t* R = res_of(ws, l);
-    if (R[R_SLOW]) return;
-    uint32_t above;
-    const int bin = block_resolve<true>(hist_row(ws, 1, T.L, l), 1024, R[R_NEED], lds, above);
-    if (threadIdx.x == 0) {
-      R[R_PREFIX] |= (uint32_t)max(bin, 0) << 10;
-      R[R_KNOWN] = 22;
-      R[R_NEED] -= above;
-    }
-  });
-}
-
-// ---------------------------------------------------------------------------------------------
-// Random-k candidate pass: acc = g + e (written to e when fused), Philox key per element; keys
-// below the segment's bound tau are emitted to the list in index order, and the first level of
-// the key histogram is built.  The chunk completing a segment checks the candidate count and
-// resolves that level.
-// ---------------------------------------------------------------------------------------------
-template <int GDT, bool FUSED>
-__global__ __launch_bounds__(kNT) void k_randk_stream(Tables T, const void* g, const float* src, float* acc_out,
-                                                      uint32_t s0, uint32_t s1, uint32_t step, WS ws) {
-  __shared__ uint32_t gp[kTile / 4];
-  __shared__ uint32_t lds[kWaves];
-  __shared__ uint32_t s_c;
-  if (threadIdx.x == 0) s_c = atomicAdd(ws.tickets + 0, 1u);
-  __syncthreads();
-  EmitCtx E;
-  E.c = s_c;
-  E.lo = E.c * kTile;
-  E.hi = min((uint32_t)T.d, E.lo + kTile);
-  E.sf = T.chunk_sf[E.c];
-  E.sl = T.chunk_sl[E.c];
-  const bool uni = E.sf == E.sl;
-  const uint32_t o_u = (uint32_t)T.seg_off[E.sf];
-  const uint64_t tau_u = T.seg_tau[E.sf];
-  const bool aligned = uni && (o_u & 3u) == 0;
-  float v[kRounds][4];
-  uint32_t key[kRounds][4];
-  uint32_t mask[kRounds], gpre[kRounds];
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = E.lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < E.hi ? (int)min(4u, E.hi - i0) : 0;
-    mask[r] = 0;
-    if (nv > 0) {
-      if constexpr (FUSED) {
-        float gv[4], ev[4];
-        load4g<GDT>(g, i0, nv, gv);
-        load4(src, i0, nv, ev);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[r][q] = gv[q] + ev[q];
-        store4(acc_out, i0, nv, v[r]);
-      } else {
-        load4(src, i0, nv, v[r]);
-      }
       if (aligned) {
-        const uint4 x = philox(make_uint4((i0 - o_u) >> 2, 0u, step, kRandkTag | (uint32_t)E.sf), s0, s1);
-        key[r][0] = x.x; key[r][1] = x.y; key[r][2] = x.z; key[r][3] = x.w;
+        uint4 x = make_uint4(0u, 0u, 0u, 0u);
+        if (nv > 0) x = philox(make_uint4((i0 - o_u) >> 2, 0u, step, kRandkTag | (uint32_t)sf), s0, s1);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (q < nv && (uint64_t)key[r][q] < tau_u) mask[r] |= 1u << q;
+        for (int q = 0; q < 4; ++q) {
+          kk[r][q] = ~word(x, q);
+          if (q < nv && (uint64_t)word(x, q) < tau_u) mk |= 1u << q;
+        }
       } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          key[r][q] = 0;
+          kk[r][q] = 0u;
           if (q < nv) {
             const uint32_t i = i0 + q;
-            const int l = uni ? E.sf : seg_of(i, E.sf, E.sl, T.seg_off);
-            key[r][q] = randk_key(i - (uint32_t)T.seg_off[l], (uint32_t)l, step, s0, s1);
-            if ((uint64_t)key[r][q] < T.seg_tau[l]) mask[r] |= 1u << q;
+            const int l = uni ? sf : seg_of(i, sf, sl, T.seg_off);
+            const uint32_t u = randk_key(i - (uint32_t)T.seg_off[l], (uint32_t)l, step, s0, s1);
+            kk[r][q] = ~u;
+            if ((uint64_t)u < T.seg_tau[l]) mk |= 1u << q;
           }
         }
       }
     }
-  }
-  uint32_t total;
-  ordered_positions(T, ws.st_stream, ws.diag, E, mask, gpre, gp, lds, total);
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    if (!mask[r]) continue;
-    const uint32_t i0 = E.lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    uint32_t pre = gpre[r];
+    mask[r] = mk;
+    uint32_t pre = 0, tot = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      if (mask[r] & (1u << q)) {
-        const uint32_t i = i0 + q;
-        const int l = uni ? E.sf : seg_of(i, E.sf, E.sl, T.seg_off);
-        const uint32_t pos = list_pos(T, E, gp, l, pre, total);
-        const uint32_t cap = (uint32_t)(T.rk_base[l + 1] - T.rk_base[l]);
-        if (pos < cap) {
-          const uint32_t at = (uint32_t)T.rk_base[l] + pos;
-          ws.list_idx[at] = i;
-          ws.list_val[at] = v[r][q];
-          ws.list_key[at] = key[r][q];
+      const uint64_t b = __ballot((mk >> q) & 1u);
+      pre += lanes_below(b);
+      tot += (uint32_t)__popcll(b);
+    }
+    lpre[r] = pre;
+    if (lane == 0) wt[r][wid] = tot;
+  }
+  __syncthreads();
+  uint32_t base = 0;
+  uint32_t* cidx = ws.cand_idx + (size_t)c * kTile;
+  float* cval = ws.cand_val + (size_t)c * kTile;
+  uint32_t* ckey = ws.cand_key + (size_t)c * kTile;
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    uint32_t rb = base;
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) rb += w < wid ? wt[r][w] : 0u;
+    if (mask[r]) {
+      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      uint32_t pos = rb + lpre[r];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if ((mask[r] >> q) & 1u) {
+          cidx[pos] = i0 + q;
+          cval[pos] = v[r][q];
+          ckey[pos] = kk[r][q];
+          ++pos;
         }
-        const int hb = T.seg_hb[l];
-        const int w = min(11, hb);
-        const uint32_t kk = ~key[r][q];
-        atomicAdd(hist_row(ws, 0, T.L, l) + ((kk >> (hb - w)) & ((1u << w) - 1u)), 1u);
-        ++pre;
       }
     }
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) base += wt[r][w];
   }
-  // per-segment candidate counts
-  for (int l = E.sf + (int)threadIdx.x; l <= E.sl; l += kNT) {
-    const uint32_t n = chunk_count(T, E, gp, l, total);
-    if (n) atomicAdd(ws.cnt + l, n);
-  }
-  arrive_and_resolve(ws.arrive, T.seg_nchunks, E.sf, E.sl, [&](int l) {
-    uint32_t* R = res_of(ws, l);
-    const uint32_t cnt = ld_acq(ws.cnt + l);
-    const uint32_t k = (uint32_t)T.seg_k[l];
-    const uint32_t cap = (uint32_t)(T.rk_base[l + 1] - T.rk_base[l]);
-    const int hb = T.seg_hb[l];
-    const int w = min(11, hb);
-    if (cnt < k || cnt > cap) {
-      if (threadIdx.x == 0) {
-        R[R_SLOW] = 1;
-        R[R_CNT] = 0;
-        atomicOr(ws.diag, kDiagSlowPath);
-      }
-      return;
-    }
-    uint32_t above;
-    const int bin = block_resolve<true>(hist_row(ws, 0, T.L, l), 1 << w, k, lds, above);
-    if (threadIdx.x == 0) {
-      const uint32_t top = hb >= 32 ? 0u : (0xFFFFFFFFu << hb);
-      R[R_PREFIX] = top | ((uint32_t)max(bin, 0) << (hb - w));
-      R[R_KNOWN] = (uint32_t)(32 - hb + w);
-      R[R_NEED] = k - above;
-      R[R_CNT] = cnt;
-      R[R_SLOW] = 0;
-    }
-  });
+  if (threadIdx.x == 0) ws.counts[c] = base;
 }
 
-// ---------------------------------------------------------------------------------------------
-// List selection: next radix level over the candidate lists, and the exact slow path.
-// KIND 0 = top-k (key = magnitude bits of the value), 1 = random-k (key = ~Philox key, so the
-// smallest random keys rank highest).  Ties between equal keys go to the lower list position,
-// which is the lower element index.
-// ---------------------------------------------------------------------------------------------
+// Exact selection over the whole segment (used when the candidates cannot contain the answer):
+// radix levels over the keys of all d_l elements, then an index-ordered emission.
 template <int KIND>
-__device__ __forceinline__ uint32_t list_key_of(const WS& ws, uint32_t p) {
-  if constexpr (KIND == 0) return mag_key(ws.list_val[p]);
-  else return ~ws.list_key[p];
-}
-
-struct ListGeom {
-  const int32_t* base;
-  const int32_t* nlch;
-  const int32_t* lsf;
-  const int32_t* lsl;
-  uint32_t nlchunks;
-};
-
-template <int KIND>
-__device__ __forceinline__ ListGeom list_geom(const Tables& T) {
-  if constexpr (KIND == 0) return ListGeom{T.tk_base, T.tk_nlch, T.tk_lsf, T.tk_lsl, (uint32_t)T.tk_nlchunks};
-  else return ListGeom{T.rk_base, T.rk_nlch, T.rk_lsf, T.rk_lsl, (uint32_t)T.rk_nlchunks};
-}
-
-// Exact single-workgroup selection over the whole segment (used when the list cannot hold the
-// answer).  Radix levels over the keys of all d_l elements, then an index-ordered emission.
-template <int KIND>
-__device__ void slow_select(const Tables& T, WS& ws, int l, const float* data, float* e_zero,
-                            uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1, uint32_t step,
-                            uint32_t* lhist, uint32_t* lds) {
-  uint32_t* R = res_of(ws, l);
+__device__ void slow_select(const Tables& T, int l, const float* data, float* e_zero, uint32_t* out_idx,
+                            float* out_val, uint32_t s0, uint32_t s1, uint32_t step, uint32_t* hist, uint32_t* lds) {
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
-  const uint32_t P = (uint32_t)T.seg_P[l];
-  uint32_t prefix, need;
-  int known;
-  if constexpr (KIND == 0) {
-    prefix = R[R_PREFIX];  // level 0 (bits 31:20) resolved by the histogram pass
-    need = R[R_NEED];
-    known = 12;
-  } else {
-    prefix = 0;
-    need = (uint32_t)T.seg_k[l];
-    known = 0;
-  }
-  auto keyat = [&](uint32_t j) -> uint32_t {
-    if constexpr (KIND == 0) return mag_key(data[o + j]);
-    else return ~randk_key(j, (uint32_t)l, step, s0, s1);
-  };
+  const uint32_t P = (uint32_t)T.seg_P[l], kl = (uint32_t)T.seg_k[l];
+  auto keyat = [&](uint32_t j) -> uint32_t { return sel_key<KIND>(o + j, data[o + j], o, l, step, s0, s1); };
+  uint32_t prefix = 0, need = kl;
+  int known = 0;
   while (known < 32) {
     const int w = min(11, 32 - known);
     const int shift = 32 - known - w;
-    for (int b = threadIdx.x; b < (1 << w); b += kNT) lhist[b] = 0;
+    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < n; j += kNT) {
+    for (uint32_t j = threadIdx.x; j < n; j += kSelNT) {
       const uint32_t k = keyat(j);
       if (known == 0 || (k >> (32 - known)) == (prefix >> (32 - known)))
-        atomicAdd(&lhist[(k >> shift) & ((1u << w) - 1u)], 1u);
+        atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u);
     }
     __syncthreads();
     uint32_t above;
-    const int bin = block_resolve<false>(lhist, 1 << w, need, lds, above);
+    const int bin = block_resolve<kSelNT>(hist, 1 << w, need, lds, above);
     prefix |= (uint32_t)max(bin, 0) << shift;
     need -= above;
     known += w;
   }
   const uint32_t Tk = prefix, r = need;
   uint32_t run_a = 0, run_b = 0;
-  for (uint32_t j0 = 0; j0 < n; j0 += kNT) {
+  for (uint32_t j0 = 0; j0 < n; j0 += kSelNT) {
     const uint32_t j = j0 + threadIdx.x;
-    uint32_t a = 0, b = 0, k = 0;
+    uint32_t a = 0, b = 0;
     if (j < n) {
-      k = keyat(j);
+      const uint32_t k = keyat(j);
       a = k > Tk;
       b = k == Tk;
     }
     uint32_t tot;
-    const uint32_t ex = block_excl_scan(a | (b << 16), lds, tot);
+    const uint32_t ex = block_excl_scan<kSelNT>(a | (b << 16), lds, tot);
     const uint32_t ea = run_a + (ex & 0xFFFFu), eb = run_b + (ex >> 16);
-    if ((a || (b && eb < r)) && ea + min(eb, r) < (uint32_t)T.seg_k[l]) {
+    if ((a || (b && eb < r)) && ea + min(eb, r) < kl) {
       const uint32_t pos = P + ea + min(eb, r);
       out_idx[pos] = o + j;
       out_val[pos] = data[o + j];
@@ -778,138 +640,261 @@ __device__ void slow_select(const Tables& T, WS& ws, int l, const float* data, f
     run_a += tot & 0xFFFFu;
     run_b += tot >> 16;
   }
+}
+
+// Per-segment exact selection among the candidates in the chunk slots, and the emission of the
+// k_l winners in index order (one workgroup per segment).  Every pass is wave-contiguous: wave w
+// owns a contiguous share of the flat (= index) order of the candidates and walks it 64 entries at
+// a time with kBatch loads in flight, so accesses stay coalesced.  The gather copies the
+// candidates to dense arrays at [o_l, o_l + N) (N <= d_l; keys to LDS when they fit), the radix
+// levels sweep the keys, and the emission uses in-wave ballot prefixes plus one scan of the wave
+// totals.  The row offsets and keys live either in LDS or in global memory; each placement is its
+// own instantiation so that every access has a known address space (no flat accesses, whose waits
+// would serialise the batches).
+// Last position m >= i with off[m] <= f (off strictly increasing over [0, n); off[i] <= f).
+__device__ __forceinline__ uint32_t advance_row(const uint32_t* off, uint32_t n, uint32_t i, uint32_t f) {
+  if (i + 1 >= n || off[i + 1] > f) return i;
+  uint32_t lo = i + 1, hi, step = 1;
+  while (true) {  // gallop until off[hi] > f
+    hi = lo + step;
+    if (hi >= n) {
+      hi = n;
+      break;
+    }
+    if (off[hi] > f) break;
+    lo = hi;
+    step <<= 1;
+  }
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (off[mid] <= f) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+struct SelSeg {
+  int l;
+  uint32_t o, kl, P, c0, nc, a0, b1, N;
+};
+
+template <int KIND, bool KEYS_LDS>
+__device__ __forceinline__ void select_emit_tail(const Tables& T, const WSel& ws, const SelSeg& S, const uint32_t* crow,
+                                                 const uint32_t* coff, uint32_t nnz, uint32_t* keys, float* e_zero,
+                                                 uint32_t* out_idx, float* out_val, uint32_t* hist, uint32_t* lds,
+                                                 uint32_t (*s_wtot)[kSelNT / 64]) {
+  constexpr int NW = kSelNT / 64;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const uint32_t N = S.N;
+  const uint32_t W0 = (uint32_t)(((uint64_t)N * wid) / NW), W1 = (uint32_t)(((uint64_t)N * (wid + 1)) / NW);
+  uint32_t* didx = ws.dense_idx + S.o;
+  float* dval = ws.dense_val + S.o;
+  // gather
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+  {
+    // m0: the non-empty row holding the wave's next flat position (wave-uniform).  For 64
+    // consecutive positions the rows involved are m0 .. m0+63 at most (every row is non-empty):
+    // each lane loads one row boundary and finds its own row by a shuffle binary search.
+    uint32_t m0 = advance_row(coff, nnz, 0, W0 < W1 ? W0 : 0u);
+    for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
+      size_t at[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const uint32_t fb = base + (uint32_t)u * 64u;  // wave-uniform
+        const uint32_t f = fb + lane;
+        const uint32_t mb = m0 + lane;
+        const uint32_t bnd = mb < nnz ? coff[mb] : 0xFFFFFFFFu;
+        const uint32_t rid = mb < nnz ? crow[mb] : 0u;
+        uint32_t j = 0;  // last j with boundary(m0 + j) <= f
+#pragma unroll
+        for (int st = 32; st > 0; st >>= 1) {
+          const uint32_t cand = j + (uint32_t)st;
+          const uint32_t bc = __shfl(bnd, (int)min(cand, 63u), 64);
+          if (cand < 64u && bc <= f) j = cand;
+        }
+        const uint32_t row = __shfl(rid, (int)j, 64), off = __shfl(bnd, (int)j, 64);
+        at[u] = f < W1 ? (size_t)(S.c0 + row) * kTile + (row == 0 ? S.a0 : 0u) + (f - off) : 0;
+        // row of the next wave-step's first position (fb + 64): lane 63's row, or the one after
+        const uint32_t j63 = __shfl(j, 63, 64);
+        uint32_t nb = __shfl(bnd, (int)min(j63 + 1u, 63u), 64);
+        if (j63 == 63u) nb = m0 + 64u < nnz ? coff[m0 + 64u] : 0xFFFFFFFFu;  // every row held one position
+        m0 += j63 + (nb <= fb + 64u ? 1u : 0u);
+      }
+      uint32_t ci[kBatch], ck[kBatch];
+      float cv[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const bool in = base + (uint32_t)u * 64u + lane < W1;
+        ci[u] = in ? ws.cand_idx[at[u]] : 0u;
+        cv[u] = in ? ws.cand_val[at[u]] : 0.0f;
+        ck[u] = in ? ws.cand_key[at[u]] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const uint32_t f = base + (uint32_t)u * 64u + lane;
+        if (f < W1) {
+          didx[f] = ci[u];
+          dval[f] = cv[u];
+          keys[f] = ck[u];
+          kand &= ck[u];
+          kor |= ck[u];
+        }
+      }
+    }
+  }
+  block_and_or(kand, kor, lds);  // also makes the gathered data visible to the workgroup
+  EFS_PHASE(3);
+  uint32_t Tk, r;
+  block_select(keys, N, S.kl, kand, kor, hist, lds, Tk, r);
+  EFS_PHASE(4);
+  // emission in flat (= index) order
+  uint32_t na = 0, nb = 0;
+  for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
+    uint32_t k[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t f = base + (uint32_t)u * 64u + lane;
+      k[u] = f < W1 ? keys[f] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool in = base + (uint32_t)u * 64u + lane < W1;
+      na += (uint32_t)__popcll(__ballot(in && k[u] > Tk));
+      nb += (uint32_t)__popcll(__ballot(in && k[u] == Tk));
+    }
+  }
+  if (lane == 0) {
+    s_wtot[0][wid] = na;
+    s_wtot[1][wid] = nb;
+  }
   __syncthreads();
+  uint32_t ra = 0, rb = 0;
+  for (int w = 0; w < wid; ++w) {
+    ra += s_wtot[0][w];
+    rb += s_wtot[1][w];
+  }
+  EFS_PHASE(5);
+  for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
+    uint32_t k[kBatch], ix[kBatch];
+    float vv[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const uint32_t f = base + (uint32_t)u * 64u + lane;
+      const bool in = f < W1;
+      k[u] = in ? keys[f] : 0u;
+      ix[u] = in ? didx[f] : 0u;
+      vv[u] = in ? dval[f] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool in = base + (uint32_t)u * 64u + lane < W1;
+      const bool a = in && k[u] > Tk, b = in && k[u] == Tk;
+      const uint64_t ma = __ballot(a), mb = __ballot(b);
+      const uint32_t ea = ra + lanes_below(ma), eb = rb + lanes_below(mb);
+      if ((a || (b && eb < r)) && ea + min(eb, r) < S.kl) {
+        const uint32_t pos = S.P + ea + min(eb, r);
+        out_idx[pos] = ix[u];
+        out_val[pos] = vv[u];
+        if (e_zero && ix[u] < (uint32_t)T.d) e_zero[ix[u]] = 0.0f;
+      }
+      ra += (uint32_t)__popcll(ma);
+      rb += (uint32_t)__popcll(mb);
+    }
+  }
+  EFS_PHASE(6);
   if (threadIdx.x == 0) {
-    R[R_DONE] = 1;
-    R[R_CNT] = 0;
+    uint32_t* R = res_of(ws, S.l);
+    R[R_T] = Tk;
+    R[R_R] = r;
+    R[R_N] = N;
+    R[R_SLOW] = 0;
   }
 }
 
-template <int KIND>
-__global__ __launch_bounds__(kNT) void k_list_level(Tables T, WS ws, int slot, const float* data, float* e_zero,
-                                                    uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1,
-                                                    uint32_t step) {
-  __shared__ uint32_t lhist[kHBins];
-  __shared__ uint32_t lds[kWaves];
-  const ListGeom G = list_geom<KIND>(T);
-  const uint32_t q = blockIdx.x;
-  const uint32_t lo = q * kLTile;
-  const int sf = G.lsf[q], sl = G.lsl[q];
-  for (int rr = 0; rr < kLRounds; ++rr) {
-    const uint32_t p = lo + (uint32_t)(rr * kNT) + threadIdx.x;
-    const int l = sf == sl ? sf : seg_of(p, sf, sl, G.base);
-    const uint32_t* R = res_of(ws, l);
-    if (p >= (uint32_t)G.base[l + 1] || R[R_SLOW] || R[R_KNOWN] >= 32) continue;
-    if (p >= (uint32_t)G.base[l] + R[R_CNT]) continue;
-    const uint32_t known = R[R_KNOWN], prefix = R[R_PREFIX];
-    const uint32_t k = list_key_of<KIND>(ws, p);
-    if ((k >> (32 - known)) != (prefix >> (32 - known))) continue;
-    const int w = min(11, 32 - (int)known);
-    const int shift = 32 - (int)known - w;
-    atomicAdd(hist_row(ws, slot, T.L, l) + ((k >> shift) & ((1u << w) - 1u)), 1u);
+// Row offsets of the segment's candidates, then either the exact whole-segment path (too few
+// candidates) or the selection over the candidates.
+template <int KIND, bool COFS_LDS>
+__device__ __forceinline__ void select_emit_body(const Tables& T, const WSel& ws, SelSeg S, uint32_t* crow,
+                                                 uint32_t* coff, const float* data, float* e_zero, uint32_t* out_idx,
+                                                 float* out_val, uint32_t s0, uint32_t s1, uint32_t step,
+                                                 uint32_t* hist, uint32_t* lds, uint32_t* s_keys,
+                                                 uint32_t (*s_wtot)[kSelNT / 64]) {
+  // non-empty chunk rows of the segment, compacted: crow = row id, coff = flat offset of its first
+  // candidate (strictly increasing)
+  uint32_t N = 0, nnz = 0;
+  for (uint32_t i0 = 0; i0 < S.nc; i0 += kSelNT) {
+    const uint32_t i = i0 + threadIdx.x;
+    uint32_t cnt = 0;
+    if (i < S.nc) cnt = (i == S.nc - 1 ? S.b1 : ws.counts[S.c0 + i]) - (i == 0 ? S.a0 : 0u);
+    uint32_t tot, totn;
+    const uint32_t ex = block_excl_scan<kSelNT>(cnt, lds, tot);
+    const uint32_t exn = block_excl_scan<kSelNT>(cnt ? 1u : 0u, lds, totn);
+    if (cnt) {
+      crow[nnz + exn] = i;
+      coff[nnz + exn] = N + ex;
+    }
+    N += tot;
+    nnz += totn;
   }
-  arrive_and_resolve(ws.arrive + (size_t)slot * T.L, G.nlch, sf, sl, [&](int l) {
-    uint32_t* R = res_of(ws, l);
-    if (R[R_SLOW]) {
-      if (!R[R_DONE]) slow_select<KIND>(T, ws, l, data, e_zero, out_idx, out_val, s0, s1, step, lhist, lds);
-      return;
-    }
-    const int known = (int)R[R_KNOWN];
-    if (known >= 32) return;
-    const int w = min(11, 32 - known);
-    const int shift = 32 - known - w;
-    uint32_t above;
-    const int bin = block_resolve<true>(hist_row(ws, slot, T.L, l), 1 << w, R[R_NEED], lds, above);
+  S.N = N;
+  if (N < S.kl) {  // the candidates cannot hold the answer: exact pass over the whole segment
+    slow_select<KIND>(T, S.l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
     if (threadIdx.x == 0) {
-      R[R_PREFIX] |= (uint32_t)max(bin, 0) << shift;
-      R[R_KNOWN] = (uint32_t)(known + w);
-      R[R_NEED] -= above;
+      uint32_t* R = res_of(ws, S.l);
+      R[R_SLOW] = 1;
+      R[R_N] = N;
+      atomicOr(ws.diag, kDiagSlowPath);
     }
-  });
+    return;
+  }
+  __syncthreads();
+  EFS_PHASE(2);
+  if (N <= kKeysLds)
+    select_emit_tail<KIND, true>(T, ws, S, crow, coff, nnz, s_keys, e_zero, out_idx, out_val, hist, lds, s_wtot);
+  else
+    select_emit_tail<KIND, false>(T, ws, S, crow, coff, nnz, ws.dense_key + S.o, e_zero, out_idx, out_val, hist, lds,
+                                  s_wtot);
 }
 
-// Emission: every list entry with key > T, plus the first r entries with key == T, written in
-// list (= index) order to the message; e is zeroed at the sent indices when fused.
 template <int KIND>
-__global__ __launch_bounds__(kNT) void k_list_emit(Tables T, WS ws, uint32_t* out_idx, float* out_val, float* e_zero) {
-  __shared__ uint32_t gp[kLTile];
-  __shared__ uint32_t lds[kWaves];
-  __shared__ uint32_t s_c, s_ea, s_eb;
-  const ListGeom G = list_geom<KIND>(T);
-  if (threadIdx.x == 0) s_c = atomicAdd(ws.tickets + 1, 1u);
+__global__ __launch_bounds__(kSelNT) void k_select_emit(Tables T, WSel ws, const float* data, float* e_zero,
+                                                        uint32_t* out_idx, float* out_val, uint32_t s0,
+                                                        uint32_t s1, uint32_t step) {
+  constexpr int NW = kSelNT / 64;
+  __shared__ uint32_t hist[kHBins];
+  __shared__ uint32_t lds[2 * NW];
+  __shared__ uint32_t s_crow[kCofsLds];
+  __shared__ uint32_t s_coff[kCofsLds];
+  __shared__ uint32_t s_keys[kKeysLds];
+  __shared__ uint32_t s_wtot[2][NW];
+  __shared__ uint32_t s_a0, s_b1;
+  SelSeg S;
+  S.l = blockIdx.x;
+  S.o = (uint32_t)T.seg_off[S.l];
+  const uint32_t e_ = (uint32_t)T.seg_off[S.l + 1];
+  S.kl = (uint32_t)T.seg_k[S.l];
+  S.P = (uint32_t)T.seg_P[S.l];
+  S.c0 = S.o / kTile;
+  S.nc = (e_ - 1) / kTile - S.c0 + 1;
+  const uint32_t c1 = S.c0 + S.nc - 1;
+  EFS_PHASE(0);
+  // candidates of this segment inside its first and last chunk (other segments may share them)
+  if (threadIdx.x == 0)
+    s_a0 = S.o > S.c0 * kTile ? lower_bound_u32(ws.cand_idx + (size_t)S.c0 * kTile, ws.counts[S.c0], S.o) : 0u;
+  if (threadIdx.x == 1)
+    s_b1 = e_ < min((uint32_t)T.d, (c1 + 1) * kTile)
+               ? lower_bound_u32(ws.cand_idx + (size_t)c1 * kTile, ws.counts[c1], e_)
+               : ws.counts[c1];
   __syncthreads();
-  const uint32_t q = s_c;
-  const uint32_t lo = q * kLTile, hi = lo + kLTile;
-  const int sf = G.lsf[q], sl = G.lsl[q];
-  const bool uni = sf == sl;
-  uint32_t fa[kLRounds], fb[kLRounds], pre[kLRounds];
-  uint32_t base = 0;
-#pragma unroll
-  for (int rr = 0; rr < kLRounds; ++rr) {
-    const uint32_t p = lo + (uint32_t)(rr * kNT) + threadIdx.x;
-    const int l = uni ? sf : seg_of(p, sf, sl, G.base);
-    const uint32_t* R = res_of(ws, l);
-    fa[rr] = fb[rr] = 0;
-    if (p < (uint32_t)G.base[l + 1] && !R[R_SLOW] && p < (uint32_t)G.base[l] + R[R_CNT]) {
-      const uint32_t k = list_key_of<KIND>(ws, p), Tk = R[R_PREFIX];
-      fa[rr] = k > Tk;
-      fb[rr] = k == Tk;
-    }
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan(fa[rr] | (fb[rr] << 16), lds, tot);
-    pre[rr] = base + ex;
-    gp[rr * kNT + threadIdx.x] = base + ex;
-    base += tot;
-  }
-  __syncthreads();
-  const uint32_t total = base;
-  // gp[x] is the packed exclusive prefix at list position lo + x (entry (rr, t) has x = rr*kNT + t).
-  auto prefix_at = [&](uint32_t p) -> uint32_t { return p >= hi ? total : gp[p - lo]; };
-  const uint32_t b_sl = (uint32_t)G.base[sl];
-  const uint32_t st_sl = max(b_sl, lo);
-  const uint32_t c_sl = total - prefix_at(st_sl);
-  const bool sl_cont = b_sl < lo;
-  const uint32_t b_sf = (uint32_t)G.base[sf];
-  const bool need_lb = b_sf < lo;
-  if (threadIdx.x == 0) {
-    lb_publish(ws.st_emit + q, sl_cont ? 1u : 2u, c_sl & 0xFFFFu, c_sl >> 16);
-    s_ea = 0;
-    s_eb = 0;
-  }
-  if (need_lb && threadIdx.x < 64) {
-    uint32_t ea, eb;
-    lb_lookback(ws.st_emit, (int)q, (int)(b_sf / kLTile), ea, eb, ws.diag);
-    if (threadIdx.x == 0) {
-      s_ea = ea;
-      s_eb = eb;
-      if (sl_cont) lb_publish(ws.st_emit + q, 2u, ea + (c_sl & 0xFFFFu), eb + (c_sl >> 16));
-    }
-  }
-  __syncthreads();
-#pragma unroll
-  for (int rr = 0; rr < kLRounds; ++rr) {
-    if (!(fa[rr] | fb[rr])) continue;
-    const uint32_t p = lo + (uint32_t)(rr * kNT) + threadIdx.x;
-    const int l = uni ? sf : seg_of(p, sf, sl, G.base);
-    const uint32_t* R = res_of(ws, l);
-    uint32_t a, b;
-    if (uni) {
-      a = s_ea + (pre[rr] & 0xFFFFu);
-      b = s_eb + (pre[rr] >> 16);
-    } else {
-      const uint32_t sp = prefix_at(max((uint32_t)G.base[l], lo));
-      a = (l == sf ? s_ea : 0u) + (pre[rr] & 0xFFFFu) - (sp & 0xFFFFu);
-      b = (l == sf ? s_eb : 0u) + (pre[rr] >> 16) - (sp >> 16);
-    }
-    const uint32_t r = R[R_NEED];
-    if ((fa[rr] || b < r) && a + min(b, r) < (uint32_t)T.seg_k[l]) {
-      const uint32_t pos = (uint32_t)T.seg_P[l] + a + min(b, r);
-      const uint32_t i = ws.list_idx[p];
-      out_idx[pos] = i;
-      out_val[pos] = ws.list_val[p];
-      if (e_zero && i < (uint32_t)T.d) e_zero[i] = 0.0f;
-    }
-  }
+  S.a0 = s_a0;
+  S.b1 = s_b1;
+  S.N = 0;
+  EFS_PHASE(1);
+  if (S.nc <= kCofsLds)
+    select_emit_body<KIND, true>(T, ws, S, s_crow, s_coff, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds,
+                                 s_keys, s_wtot);
+  else
+    select_emit_body<KIND, false>(T, ws, S, ws.cofs + 2 * (size_t)T.seg_cbase[S.l], ws.cofs + 2 * (size_t)T.seg_cbase[S.l] + S.nc,
+                                  data, e_zero, out_idx, out_val, s0, s1, step, hist, lds, s_keys, s_wtot);
 }
 
 }  // namespace efs

@@ -6,7 +6,9 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
+#include <string>
 #include <vector>
 
 #include "../../include/efsparse.h"
@@ -33,32 +35,9 @@ struct Blob {
   template <typename T> size_t add(const std::vector<T>& v) { return add(v.data(), v.size() * sizeof(T)); }
 };
 
-// Region table over a list space: region l is [base[l], base[l+1]); chunks of `tile` positions.
-void chunk_cover(const std::vector<int32_t>& base, int64_t total, uint32_t tile, std::vector<int32_t>& sf,
-                 std::vector<int32_t>& sl, std::vector<int32_t>& per_region) {
-  const int L = (int)base.size() - 1;
-  const int64_t n = (total + tile - 1) / tile;
-  sf.assign(n, 0);
-  sl.assign(n, 0);
-  int l = 0;
-  for (int64_t c = 0; c < n; ++c) {
-    const int64_t lo = c * tile, hi = std::min<int64_t>(total, lo + tile);
-    while (l + 1 < L && base[l + 1] <= lo) ++l;
-    sf[c] = l;
-    int m = l;
-    while (m + 1 < L && base[m + 1] <= hi - 1) ++m;
-    sl[c] = m;
-  }
-  per_region.assign(L, 0);
-  for (int r = 0; r < L; ++r) {
-    const int64_t first = base[r] / tile, last = (base[r + 1] - 1) / tile;
-    per_region[r] = (int32_t)(last - first + 1);
-  }
-}
-
 struct WsLayout {
-  size_t diag = 0, tickets = 0, arrive = 0, res = 0, cnt = 0, hist = 0, st_stream = 0, st_emit = 0;
-  size_t zero_bytes = 0, list_idx = 0, list_val = 0, list_key = 0, total = 0;
+  size_t diag = 0, res = 0, counts = 0, cofs = 0, cand_idx = 0, cand_val = 0, cand_key = 0, dense_idx = 0,
+         dense_val = 0, dense_key = 0, total = 0;
 };
 
 }  // namespace
@@ -69,19 +48,15 @@ struct ef_layout {
   double density = 0;
   int64_t block = 1;
   std::vector<int64_t> off64;
-  double rk_sigma = 10.0, rk_extra = 64.0, rk_capmult = 1.0, tk_mult = 2.0, tk_extra = 65536.0;
+  double rk_sigma = 10.0, rk_extra = 64.0, tk_sigma = 6.0, tk_extra = 8.0;
 
-  std::vector<int32_t> off, k, P, bl, nb, hb, nch, tk_base, tk_nlch, rk_base, rk_nlch;
-  std::vector<int32_t> csf, csl, tk_lsf, tk_lsl, rk_lsf, rk_lsl;
+  std::vector<int32_t> off, k, P, bl, nb, srank, cbase, csf, csl;
   std::vector<uint64_t> tau;
   int64_t K = 0;
-  int32_t nchunks = 0;
-  int64_t tk_cap = 0, rk_cap = 0;
-  int randk_levels = 1;  // list-level launches after the random-k candidate pass
+  int32_t nchunks = 0, ncrows = 0;
 
   Blob blob;
-  size_t o_off, o_k, o_P, o_bl, o_nb, o_hb, o_nch, o_tau, o_tkb, o_tkn, o_rkb, o_rkn, o_csf, o_csl, o_tlsf,
-      o_tlsl, o_rlsf, o_rlsl;
+  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_cbase, o_tau, o_csf, o_csl;
   Tables T{};
   bool bound = false;
 
@@ -97,11 +72,9 @@ void ef_layout::build() {
   P.assign(n + 1, 0);
   bl.resize(n);
   nb.resize(n);
-  hb.resize(n);
+  srank.resize(n);
   tau.resize(n);
-  tk_base.assign(n + 1, 0);
-  rk_base.assign(n + 1, 0);
-  randk_levels = 1;
+  cbase.assign(n + 1, 0);
   for (int l = 0; l < n; ++l) {
     const int64_t dl = off64[l + 1] - off64[l];
     // k per segment: round-half-up of density * d_l in double, clamped to [1, d_l]
@@ -112,34 +85,36 @@ void ef_layout::build() {
     const int64_t b = dl > block ? block : 1;
     bl[l] = (int32_t)b;
     nb[l] = (int32_t)((dl + b - 1) / b);
-    // random-k candidate bound: expected candidates mu = k + sigma*sqrt(k) + extra
+    // top-k: rank of the candidate threshold inside a sample of kSampleMax keys, so that the
+    // expected sample count above the true threshold plus tk_sigma standard deviations is covered
+    const double mus = (double)kSampleMax * (double)kl / (double)dl;
+    const double rs = std::ceil(mus + tk_sigma * std::sqrt(mus) + tk_extra);
+    srank[l] = (int32_t)std::min<double>(std::max<double>(rs, 1.0), (double)kSampleMax);
+    // random-k: keys below tau are candidates; expected count k + sigma * sqrt(k) + extra
     const double mu = (double)kl + rk_sigma * std::sqrt((double)kl) + rk_extra;
     const double p = mu / (double)dl;
     uint64_t t;
     if (p >= 1.0) t = 1ull << 32;
     else t = (uint64_t)std::ceil(std::max(p, 0.0) * 4294967296.0);
-    t = std::min<uint64_t>(std::max<uint64_t>(t, 2), 1ull << 32);
-    tau[l] = t;
-    int h = 0;
-    while (h < 32 && ((t - 1) >> h) != 0) ++h;
-    hb[l] = h;
-    const int rest = h - std::min(11, h);
-    randk_levels = std::max(randk_levels, (rest + 10) / 11);
-    const double E = (double)dl * (double)t / 4294967296.0;
-    const double capr = std::ceil(rk_capmult * (E + 10.0 * std::sqrt(E) + 64.0));
-    const int64_t rc = std::min<int64_t>(std::max<int64_t>((int64_t)capr, 1), dl);
-    rk_base[l + 1] = rk_base[l] + (int32_t)rc;
-    const double ct = std::ceil(tk_mult * (double)kl + tk_extra);
-    const int64_t tc = std::min<int64_t>(std::max<int64_t>((int64_t)ct, 1), dl);
-    tk_base[l + 1] = tk_base[l] + (int32_t)tc;
+    tau[l] = std::min<uint64_t>(std::max<uint64_t>(t, 1), 1ull << 32);
+    // per-segment scratch rows: one per data chunk the segment touches
+    const int64_t c0 = off64[l] / kTile, c1 = (off64[l + 1] - 1) / kTile;
+    cbase[l + 1] = cbase[l] + (int32_t)(c1 - c0 + 1);
   }
   K = P[n];
-  tk_cap = tk_base[n];
-  rk_cap = rk_base[n];
+  ncrows = cbase[n];
   nchunks = (int32_t)((d + kTile - 1) / kTile);
-  chunk_cover(off, d, kTile, csf, csl, nch);
-  chunk_cover(tk_base, tk_cap, kLTile, tk_lsf, tk_lsl, tk_nlch);
-  chunk_cover(rk_base, rk_cap, kLTile, rk_lsf, rk_lsl, rk_nlch);
+  csf.assign(nchunks, 0);
+  csl.assign(nchunks, 0);
+  int l = 0;
+  for (int32_t c = 0; c < nchunks; ++c) {
+    const int64_t lo = (int64_t)c * kTile, hi = std::min<int64_t>(d, lo + kTile);
+    while (l + 1 < n && off64[l + 1] <= lo) ++l;
+    csf[c] = l;
+    int m = l;
+    while (m + 1 < n && off64[m + 1] <= hi - 1) ++m;
+    csl[c] = m;
+  }
 
   blob = Blob();
   o_off = blob.add(off);
@@ -147,75 +122,57 @@ void ef_layout::build() {
   o_P = blob.add(P);
   o_bl = blob.add(bl);
   o_nb = blob.add(nb);
-  o_hb = blob.add(hb);
-  o_nch = blob.add(nch);
+  o_srank = blob.add(srank);
+  o_cbase = blob.add(cbase);
   o_tau = blob.add(tau);
-  o_tkb = blob.add(tk_base);
-  o_tkn = blob.add(tk_nlch);
-  o_rkb = blob.add(rk_base);
-  o_rkn = blob.add(rk_nlch);
   o_csf = blob.add(csf);
   o_csl = blob.add(csl);
-  o_tlsf = blob.add(tk_lsf);
-  o_tlsl = blob.add(tk_lsl);
-  o_rlsf = blob.add(rk_lsf);
-  o_rlsl = blob.add(rk_lsl);
   bound = false;
 }
 
 WsLayout ef_layout::ws_layout(int op) const {
+  (void)op;
   WsLayout w;
-  const size_t Ls = (size_t)L;
-  const size_t nl = op == EF_OP_TOPK ? tk_lsf.size() : rk_lsf.size();
-  const size_t cap = op == EF_OP_TOPK ? (size_t)tk_cap : (size_t)rk_cap;
   size_t at = 0;
   w.diag = at;
-  w.tickets = at + 4;
   at = 16;
-  w.arrive = at;
-  at += 3 * Ls * 4;
   w.res = at;
-  at += Ls * kResWords * 4;
-  w.cnt = at;
-  at += Ls * 4;
-  at = align_up(at, 16);
-  w.hist = at;
-  at += 3 * Ls * kHBins * 4;
-  at = align_up(at, 16);
-  w.st_stream = at;
-  at += (size_t)nchunks * 8;
-  w.st_emit = at;
-  at += nl * 8;
-  w.zero_bytes = align_up(at, 16);
-  at = align_up(at, kAlign);
-  w.list_idx = at;
-  at = align_up(at + cap * 4, kAlign);
-  w.list_val = at;
-  at = align_up(at + cap * 4, kAlign);
-  if (op == EF_OP_RANDK) {
-    w.list_key = at;
-    at = align_up(at + cap * 4, kAlign);
-  }
+  at = align_up(at + (size_t)L * kResWords * 4, 16);
+  w.counts = at;
+  at = align_up(at + (size_t)nchunks * 4, 16);
+  w.cofs = at;
+  at = align_up(at + (size_t)ncrows * 8, kAlign);
+  w.cand_idx = at;
+  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
+  w.cand_val = at;
+  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
+  w.cand_key = at;
+  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
+  w.dense_idx = at;
+  at = align_up(at + (size_t)d * 4, kAlign);
+  w.dense_val = at;
+  at = align_up(at + (size_t)d * 4, kAlign);
+  w.dense_key = at;
+  at = align_up(at + (size_t)d * 4, kAlign);
   w.total = at;
   return w;
 }
 
 namespace {
 
-WS make_ws(const WsLayout& l, void* base) {
+WSel make_ws(const WsLayout& l, void* base) {
   uint8_t* b = reinterpret_cast<uint8_t*>(base);
-  WS w;
+  WSel w;
   w.diag = reinterpret_cast<uint32_t*>(b + l.diag);
-  w.tickets = reinterpret_cast<uint32_t*>(b + l.tickets);
-  w.arrive = reinterpret_cast<uint32_t*>(b + l.arrive);
   w.res = reinterpret_cast<uint32_t*>(b + l.res);
-  w.cnt = reinterpret_cast<uint32_t*>(b + l.cnt);
-  w.hist = reinterpret_cast<uint32_t*>(b + l.hist);
-  w.st_stream = reinterpret_cast<uint64_t*>(b + l.st_stream);
-  w.st_emit = reinterpret_cast<uint64_t*>(b + l.st_emit);
-  w.list_idx = reinterpret_cast<uint32_t*>(b + l.list_idx);
-  w.list_val = reinterpret_cast<float*>(b + l.list_val);
-  w.list_key = l.list_key ? reinterpret_cast<uint32_t*>(b + l.list_key) : nullptr;
+  w.counts = reinterpret_cast<uint32_t*>(b + l.counts);
+  w.cofs = reinterpret_cast<uint32_t*>(b + l.cofs);
+  w.cand_idx = reinterpret_cast<uint32_t*>(b + l.cand_idx);
+  w.cand_val = reinterpret_cast<float*>(b + l.cand_val);
+  w.cand_key = reinterpret_cast<uint32_t*>(b + l.cand_key);
+  w.dense_idx = reinterpret_cast<uint32_t*>(b + l.dense_idx);
+  w.dense_val = reinterpret_cast<float*>(b + l.dense_val);
+  w.dense_key = reinterpret_cast<uint32_t*>(b + l.dense_key);
   return w;
 }
 
@@ -230,6 +187,57 @@ int hip_status(hipError_t e) {
 }
 
 int launched() { return hip_status(hipGetLastError()); }
+
+// ---- optional per-kernel timing: HIP events recorded around each launch on its stream ----
+struct TimingRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+struct TimingAgg {
+  std::string name;
+  double ms;
+  int64_t n;
+};
+std::mutex g_tm;
+bool g_timing = false;
+std::vector<TimingRec> g_pending;
+std::vector<hipEvent_t> g_pool;
+std::vector<TimingAgg> g_totals;
+
+hipEvent_t pool_event() {
+  if (!g_pool.empty()) {
+    hipEvent_t e = g_pool.back();
+    g_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+size_t timing_begin(const char* name, hipStream_t st) {
+  if (!g_timing) return 0;
+  std::lock_guard<std::mutex> lk(g_tm);
+  TimingRec r{name, pool_event(), pool_event()};
+  if (!r.a || !r.b) return 0;
+  (void)hipEventRecord(r.a, st);
+  g_pending.push_back(r);
+  return g_pending.size();
+}
+
+void timing_end(size_t slot, hipStream_t st) {
+  if (!slot) return;
+  std::lock_guard<std::mutex> lk(g_tm);
+  (void)hipEventRecord(g_pending[slot - 1].b, st);
+}
+
+// Every launch goes through this macro: the kernel is named after its expression.
+#define EF_LAUNCH(KERNEL, GRID, BLOCK, SHM, ST, ...)                 \
+  do {                                                               \
+    const size_t _slot = timing_begin(#KERNEL, ST);                  \
+    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHM, ST, __VA_ARGS__);   \
+    timing_end(_slot, ST);                                           \
+  } while (0)
 
 #define EF_TRY(x)              \
   do {                         \
@@ -251,14 +259,6 @@ int check_g(const void* g, int g_dtype) {
 bool vec_ok(const void* p) { return p && aligned(p, 16); }
 bool word_ok(const void* p) { return p && aligned(p, 4); }
 
-int fill_zero(void* ws, size_t bytes, hipStream_t st) {
-  const size_t words = bytes / 4;
-  if (!words) return EF_OK;
-  const size_t blocks = std::min<size_t>(1024, (words / 4 + kNT - 1) / kNT + 1);
-  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)blocks), dim3(kNT), 0, st, reinterpret_cast<uint32_t*>(ws), words);
-  return launched();
-}
-
 int check_ws(const ef_layout* L, int op, void* ws, size_t ws_bytes, WsLayout& wl) {
   wl = L->ws_layout(op);
   if (!ws || !aligned(ws, kAlign)) return EF_EINVAL;
@@ -266,62 +266,57 @@ int check_ws(const ef_layout* L, int op, void* ws, size_t ws_bytes, WsLayout& wl
   return EF_OK;
 }
 
-// Top-k: level-0 histogram (fused with the accumulate when g != null), candidate list, last
-// level, emission.
+// Top-k: sampled candidate threshold, fused accumulate + candidates, exact selection, emission.
 int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint32_t* idx,
              float* val, void* ws, size_t ws_bytes, void* stream) {
   WsLayout wl;
   EF_TRY(check_ws(L, EF_OP_TOPK, ws, ws_bytes, wl));
   hipStream_t st = S(stream);
-  WS w = make_ws(wl, ws);
+  WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT);
-  const dim3 lgrid((unsigned)L->tk_lsf.size());
-  EF_TRY(fill_zero(ws, wl.zero_bytes, st));
+  const dim3 grid((unsigned)L->nchunks), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
   if (g) {
-    if (g_dtype == EF_F32)
-      hipLaunchKernelGGL((k_topk_hist<0, true>), grid, blk, 0, st, T, g, src, e_fused, w);
-    else
-      hipLaunchKernelGGL((k_topk_hist<1, true>), grid, blk, 0, st, T, g, src, e_fused, w);
+    if (g_dtype == EF_F32) {
+      EF_LAUNCH((k_topk_sample<0, true>), sgrid, sblk, 0, st, T, g, src, w);
+      EF_TRY(launched());
+      EF_LAUNCH((k_stream_sel<0, 0, true>), grid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+    } else {
+      EF_LAUNCH((k_topk_sample<1, true>), sgrid, sblk, 0, st, T, g, src, w);
+      EF_TRY(launched());
+      EF_LAUNCH((k_stream_sel<0, 1, true>), grid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+    }
   } else {
-    hipLaunchKernelGGL((k_topk_hist<0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, w);
+    EF_LAUNCH((k_topk_sample<0, false>), sgrid, sblk, 0, st, T, nullptr, src, w);
+    EF_TRY(launched());
+    EF_LAUNCH((k_stream_sel<0, 0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
   }
   EF_TRY(launched());
   const float* acc = g ? e_fused : src;
-  hipLaunchKernelGGL(k_topk_emit, grid, blk, 0, st, T, acc, w);
-  EF_TRY(launched());
-  hipLaunchKernelGGL(k_list_level<0>, lgrid, blk, 0, st, T, w, 2, acc, e_fused, idx, val, 0u, 0u, 0u);
-  EF_TRY(launched());
-  hipLaunchKernelGGL(k_list_emit<0>, lgrid, blk, 0, st, T, w, idx, val, e_fused);
+  EF_LAUNCH(k_select_emit<0>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
   return launched();
 }
 
+// Random-k: fused accumulate + Philox candidates, exact selection, emission.
 int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint64_t seed,
               uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream) {
   WsLayout wl;
   EF_TRY(check_ws(L, EF_OP_RANDK, ws, ws_bytes, wl));
   hipStream_t st = S(stream);
-  WS w = make_ws(wl, ws);
+  WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT);
-  const dim3 lgrid((unsigned)L->rk_lsf.size());
+  const dim3 grid((unsigned)L->nchunks), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
-  EF_TRY(fill_zero(ws, wl.zero_bytes, st));
   if (g) {
     if (g_dtype == EF_F32)
-      hipLaunchKernelGGL((k_randk_stream<0, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
+      EF_LAUNCH((k_stream_sel<1, 0, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
     else
-      hipLaunchKernelGGL((k_randk_stream<1, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
+      EF_LAUNCH((k_stream_sel<1, 1, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
   } else {
-    hipLaunchKernelGGL((k_randk_stream<0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
+    EF_LAUNCH((k_stream_sel<1, 0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
   }
   EF_TRY(launched());
   const float* acc = g ? e_fused : src;
-  for (int lev = 0; lev < L->randk_levels; ++lev) {
-    hipLaunchKernelGGL(k_list_level<1>, lgrid, blk, 0, st, T, w, 1 + lev, acc, e_fused, idx, val, s0, s1, step);
-    EF_TRY(launched());
-  }
-  hipLaunchKernelGGL(k_list_emit<1>, lgrid, blk, 0, st, T, w, idx, val, e_fused);
+  EF_LAUNCH(k_select_emit<1>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
   return launched();
 }
 
@@ -343,10 +338,64 @@ const char* ef_status_string(int status) {
   }
 }
 
+#ifdef EFS_PHASE_TIMING
+int ef_debug_phases(unsigned long long* out) {
+  return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_efs_phase), sizeof(unsigned long long) * 64) == hipSuccess ? 0 : 4;
+}
+#endif
+
 int ef_last_hip_error(void) { return g_last_hip_error; }
 
 const char* ef_last_hip_error_string(void) {
   return g_last_hip_error ? hipGetErrorString((hipError_t)g_last_hip_error) : "no HIP error";
+}
+
+int ef_timing_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_tm);
+  g_timing = enable != 0;
+  return EF_OK;
+}
+
+int ef_timing_collect(void) {
+  std::lock_guard<std::mutex> lk(g_tm);
+  int rc = EF_OK;
+  for (const TimingRec& r : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.b) != hipSuccess || hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) rc = EF_EHIP;
+    TimingAgg* agg = nullptr;
+    for (TimingAgg& t : g_totals)
+      if (t.name == r.name) agg = &t;
+    if (!agg) {
+      g_totals.push_back(TimingAgg{r.name, 0.0, 0});
+      agg = &g_totals.back();
+    }
+    agg->ms += ms;
+    agg->n += 1;
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+  }
+  g_pending.clear();
+  return rc;
+}
+
+int ef_timing_count(void) {
+  std::lock_guard<std::mutex> lk(g_tm);
+  return (int)g_totals.size();
+}
+
+int ef_timing_get(int i, const char** name, double* total_ms, int64_t* launches) {
+  std::lock_guard<std::mutex> lk(g_tm);
+  if (i < 0 || i >= (int)g_totals.size() || !name || !total_ms || !launches) return EF_EINVAL;
+  *name = g_totals[i].name.c_str();
+  *total_ms = g_totals[i].ms;
+  *launches = g_totals[i].n;
+  return EF_OK;
+}
+
+int ef_timing_reset(void) {
+  std::lock_guard<std::mutex> lk(g_tm);
+  g_totals.clear();
+  return EF_OK;
 }
 
 int ef_layout_create(int64_t d, const int64_t* seg_offsets, int32_t n_seg, double density, int64_t block,
@@ -390,9 +439,8 @@ int ef_layout_tune(ef_layout* layout, int knob, double value) {
   switch (knob) {
     case EF_TUNE_RANDK_SIGMA: layout->rk_sigma = value; break;
     case EF_TUNE_RANDK_EXTRA: layout->rk_extra = value; break;
-    case EF_TUNE_TOPK_CAP_MULT: layout->tk_mult = value; break;
-    case EF_TUNE_TOPK_CAP_EXTRA: layout->tk_extra = value; break;
-    case EF_TUNE_RANDK_CAP_MULT: layout->rk_capmult = value; break;
+    case EF_TUNE_TOPK_SIGMA: layout->tk_sigma = value; break;
+    case EF_TUNE_TOPK_EXTRA: layout->tk_extra = value; break;
     default: return EF_EINVAL;
   }
   layout->build();
@@ -414,24 +462,15 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_P = reinterpret_cast<const int32_t*>(b + L->o_P);
   T.seg_bl = reinterpret_cast<const int32_t*>(b + L->o_bl);
   T.seg_nb = reinterpret_cast<const int32_t*>(b + L->o_nb);
-  T.seg_hb = reinterpret_cast<const int32_t*>(b + L->o_hb);
-  T.seg_nchunks = reinterpret_cast<const int32_t*>(b + L->o_nch);
+  T.seg_srank = reinterpret_cast<const int32_t*>(b + L->o_srank);
+  T.seg_cbase = reinterpret_cast<const int32_t*>(b + L->o_cbase);
   T.seg_tau = reinterpret_cast<const uint64_t*>(b + L->o_tau);
-  T.tk_base = reinterpret_cast<const int32_t*>(b + L->o_tkb);
-  T.tk_nlch = reinterpret_cast<const int32_t*>(b + L->o_tkn);
-  T.rk_base = reinterpret_cast<const int32_t*>(b + L->o_rkb);
-  T.rk_nlch = reinterpret_cast<const int32_t*>(b + L->o_rkn);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
   T.chunk_sl = reinterpret_cast<const int32_t*>(b + L->o_csl);
-  T.tk_lsf = reinterpret_cast<const int32_t*>(b + L->o_tlsf);
-  T.tk_lsl = reinterpret_cast<const int32_t*>(b + L->o_tlsl);
-  T.rk_lsf = reinterpret_cast<const int32_t*>(b + L->o_rlsf);
-  T.rk_lsl = reinterpret_cast<const int32_t*>(b + L->o_rlsl);
   T.d = (int32_t)L->d;
   T.L = L->L;
   T.nchunks = L->nchunks;
-  T.tk_nlchunks = (int32_t)L->tk_lsf.size();
-  T.rk_nlchunks = (int32_t)L->rk_lsf.size();
+  T.ncrows = L->ncrows;
   L->bound = true;
   return EF_OK;
 }
@@ -461,9 +500,9 @@ int ef_accumulate(const ef_layout* L, const void* g, int g_dtype, const float* e
   if (!vec_ok(e) || !vec_ok(acc)) return EF_EINVAL;
   const dim3 grid((unsigned)L->nchunks), blk(kNT);
   if (g_dtype == EF_F32)
-    hipLaunchKernelGGL(k_accumulate<0>, grid, blk, 0, S(stream), L->T.d, g, e, acc);
+    EF_LAUNCH(k_accumulate<0>, grid, blk, 0, S(stream), L->T.d, g, e, acc);
   else
-    hipLaunchKernelGGL(k_accumulate<1>, grid, blk, 0, S(stream), L->T.d, g, e, acc);
+    EF_LAUNCH(k_accumulate<1>, grid, blk, 0, S(stream), L->T.d, g, e, acc);
   return launched();
 }
 
@@ -502,7 +541,7 @@ int compress_randblock(const ef_layout* L, const float* acc, uint64_t seed, uint
   EF_TRY(check_bound(L));
   if (!vec_ok(acc) || !word_ok(start) || !word_ok(val)) return EF_EINVAL;
   const unsigned blocks = (unsigned)((L->K + kNT - 1) / kNT);
-  hipLaunchKernelGGL(k_randblock_gather, dim3(blocks), dim3(kNT), 0, S(stream), L->T, (int32_t)L->K, acc,
+  EF_LAUNCH(k_randblock_gather, dim3(blocks), dim3(kNT), 0, S(stream), L->T, (int32_t)L->K, acc,
                      (uint32_t)seed, (uint32_t)(seed >> 32), step, start, val);
   return launched();
 }
@@ -515,9 +554,9 @@ int ef_step_randblock(const ef_layout* L, const void* g, int g_dtype, float* e, 
   const dim3 grid((unsigned)L->nchunks), blk(kNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g_dtype == EF_F32)
-    hipLaunchKernelGGL(k_randblock_step<0>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
+    EF_LAUNCH(k_randblock_step<0>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
   else
-    hipLaunchKernelGGL(k_randblock_step<1>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
+    EF_LAUNCH(k_randblock_step<1>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
   return launched();
 }
 
@@ -528,17 +567,17 @@ int ef_update(const ef_layout* L, const float* acc, int msg_kind, const uint32_t
   const unsigned kblocks = (unsigned)((L->K + kNT - 1) / kNT);
   if (msg_kind == EF_MSG_SPARSE) {
     if (e != acc) {
-      hipLaunchKernelGGL(k_copy, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T.d, acc, e);
+      EF_LAUNCH(k_copy, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T.d, acc, e);
       EF_TRY(launched());
     }
-    hipLaunchKernelGGL(k_sparse_zero, dim3(kblocks), dim3(kNT), 0, st, L->T.d, (int32_t)L->K, m, e);
+    EF_LAUNCH(k_sparse_zero, dim3(kblocks), dim3(kNT), 0, st, L->T.d, (int32_t)L->K, m, e);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
     if (e == acc)
-      hipLaunchKernelGGL(k_block_zero, dim3(kblocks), dim3(kNT), 0, st, L->T, (int32_t)L->K, m, e);
+      EF_LAUNCH(k_block_zero, dim3(kblocks), dim3(kNT), 0, st, L->T, (int32_t)L->K, m, e);
     else
-      hipLaunchKernelGGL(k_block_update, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T, acc, m, e);
+      EF_LAUNCH(k_block_update, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T, acc, m, e);
     return launched();
   }
   return EF_EINVAL;
@@ -547,7 +586,7 @@ int ef_update(const ef_layout* L, const float* acc, int msg_kind, const uint32_t
 int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
                          int average, float* out, void* ws, size_t ws_bytes, void* stream) {
   EF_TRY(check_bound(L));
-  if (W < 1 || W > 65536) return EF_ERANGE;
+  if (W < 1 || W > 65535) return EF_ERANGE;
   if (!word_ok(m) || !word_ok(val) || !vec_ok(out)) return EF_EINVAL;
   hipStream_t st = S(stream);
   const dim3 grid((unsigned)L->nchunks), blk(kNT);
@@ -555,19 +594,17 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     const size_t need = ef_workspace_bytes(L, EF_OP_AGG_SPARSE, W);
     if (!ws || !aligned(ws, kAlign)) return EF_EINVAL;
     if (ws_bytes < need) return EF_EWORKSPACE;
-    const size_t entries = (size_t)W * (size_t)L->K;
-    const size_t blocks = (entries + kNT - 1) / kNT;
-    if (blocks > 0x7FFFFFFFu) return EF_ERANGE;
+    const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
     uint32_t* ts = reinterpret_cast<uint32_t*>(ws);
-    hipLaunchKernelGGL(k_agg_ranges, dim3((unsigned)blocks), blk, 0, st, L->T.d, W, (int32_t)L->K,
+    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K,
                        L->nchunks, m, ts);
     EF_TRY(launched());
-    hipLaunchKernelGGL(k_agg_sparse, grid, blk, 0, st, L->T.d, W, (int32_t)L->K, L->nchunks, m, val, ts,
+    EF_LAUNCH(k_agg_sparse, grid, blk, 0, st, L->T.d, W, (int32_t)L->K, L->nchunks, m, val, ts,
                        average, out);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
-    hipLaunchKernelGGL(k_agg_block, grid, blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
+    EF_LAUNCH(k_agg_block, grid, blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
     return launched();
   }
   return EF_EINVAL;

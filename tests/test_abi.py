@@ -107,9 +107,8 @@ def test_workspace_sizes():
     assert L.workspace_bytes(E.EF_OP_AGG_SPARSE, 8) >= 8 * (L.d // 8192 + 1) * 4
     assert L.workspace_bytes(E.EF_OP_AGG_SPARSE, 0) == 0
     assert L.workspace_bytes(99) == 0
-    # list capacity grows with the tuning knobs
-    big = E.Layout(1 << 20, None, 0.01, 1024, tune={E.EF_TUNE_TOPK_CAP_MULT: 8})
-    assert big.workspace_bytes(E.EF_OP_TOPK) > L.workspace_bytes(E.EF_OP_TOPK)
+    # candidate slots cover every element
+    assert L.workspace_bytes(E.EF_OP_TOPK) >= 8 * L.d
     assert E.lib().ef_workspace_diag_offset(L.handle, E.EF_OP_TOPK) == 0
     assert E.lib().ef_workspace_diag_offset(L.handle, E.EF_OP_RANDBLOCK) == ctypes.c_size_t(-1).value
 
