@@ -74,13 +74,11 @@ def alg_bytes_op(kind, d, K, L, W):
 
 
 def kernel_alg_bytes(name, d, K, L, W):
-    """Algorithmic bytes per launch of the streaming kernels (None for small helpers)."""
+    """Algorithmic bytes per launch of the streaming kernels (None for the small helpers)."""
     if name.startswith("k_randblock_step"):
         return 12 * d + 4 * K + 4 * L
-    if "k_topk_hist" in name or "k_randk_stream" in name:
+    if "k_stream_sel" in name and "true>" in name:  # fused: read g, read e, write e
         return 12 * d
-    if name.startswith("k_topk_emit"):
-        return 4 * d
     if name.startswith("k_agg_sparse"):
         return 4 * d + W * 8 * K
     if name.startswith("k_agg_block"):

@@ -193,8 +193,11 @@ int ef_step_randblock(const ef_layout* layout, const void* g, int g_dtype, float
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could
  * not contain the answer and the exact whole-segment path ran instead (a
- * slower path with the same result).  The word is only ever OR-ed: clear it to
- * watch a given call.  Returns (size_t)-1 for other ops. */
+ * slower path with the same result), and whose bit 2 is set if the per-row
+ * winner counts of a segment did not add up to k_l (an internal consistency
+ * check that should never fire; message writes stay inside the segment's
+ * range regardless).  The word is only ever OR-ed: clear it to watch a given
+ * call.  Returns (size_t)-1 for other ops. */
 size_t ef_workspace_diag_offset(const ef_layout* layout, int op);
 
 /* Per-kernel timing (diagnostics).  While enabled, every kernel the library

@@ -25,6 +25,7 @@ EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK = ra
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
 EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA = range(4)
 DIAG_SLOW_PATH = 2
+DIAG_COUNT_MISMATCH = 4
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2009_09271_amd.build` "

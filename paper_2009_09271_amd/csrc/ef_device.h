@@ -28,7 +28,9 @@ constexpr int kSelNT = 1024;                  // threads per workgroup of the pe
 constexpr uint32_t kTile = 8192;              // data elements per chunk
 constexpr int kRounds = kTile / (4 * kNT);    // float4 groups per thread per chunk
 constexpr int kHBins = 2048;                  // LDS histogram bins (11 bits per radix level)
-constexpr int kResWords = 8;                  // per-segment selection record (uint32 words)
+constexpr int kResWords = 16;                // per-segment selection record (uint32 words)
+constexpr int kSubLists = 16;                // a segment's list of undecided candidates is kept as 16
+                                              // sub-lists (row r appends to sub-list r % 16)
 constexpr int kSampleMax = 32768;             // top-k threshold sample size (keys held in LDS)
 constexpr int kSampleRun = 256;               // contiguous elements per sample run
 
@@ -37,13 +39,19 @@ constexpr uint32_t kRandblockTag = 0x02000000u;
 
 constexpr uint32_t kDiagSlowPath = 2u;
 
-// Per-segment selection record, uint32 words.
+// Per-segment selection record, uint32 words.  Key' is the selection key (top-k: magnitude bits;
+// random-k: complement of the Philox key), larger is better; among equal key' the lower index wins.
 enum : int {
-  R_THR = 0,    // top-k: candidate threshold key from the sample (keys >= R_THR are candidates)
-  R_T = 1,      // exact threshold key' of the selection
-  R_R = 2,      // how many entries with key' == R_T are sent (lowest indices first)
-  R_N = 3,      // candidates found for the segment
-  R_SLOW = 4,   // 1: the segment was resolved and written by the exact whole-segment path
+  R_A = 0,      // candidates: key' > R_A, or key' == R_A with index < R_IA
+  R_IA = 1,
+  R_T = 2,      // winners: key' > R_T, or key' == R_T with index < R_IT
+  R_IT = 3,
+  R_SLOW = 4,   // 1: the candidates cannot hold the answer; the segment is resolved over all of
+                //    its elements
+  R_MODE = 5,   // 1: the candidates are exactly the winners (threshold from the whole segment)
+  R_SH = 6,     // candidate histogram: bin shift
+  R_B = 7,      // candidate histogram: bin holding the k_l-th best candidate
+  R_NEED = 8,   // winners still needed from bin R_B
 };
 
 struct Tables {
@@ -52,12 +60,15 @@ struct Tables {
   const int32_t* seg_P;        // [L+1]
   const int32_t* seg_bl;       // [L]
   const int32_t* seg_nb;       // [L]
-  const int32_t* seg_srank;    // [L]  top-k: rank of the threshold inside the segment's sample
-  const int32_t* seg_cbase;    // [L+1] start of the segment's per-chunk scratch rows
-  const uint64_t* seg_tau;     // [L]  random-k: keys below tau are candidates
-  const int32_t* chunk_sf;     // [nchunks] first / last segment of each data chunk
+  const int32_t* seg_srank;    // [L]   top-k: rank of the candidate threshold inside the sample
+  const int32_t* seg_cbase;    // [L+1] first row of each segment (a row = segment x data tile)
+  const int32_t* seg_ro;       // [L+1] first top-k sample run of each segment
+  const uint64_t* seg_tau;     // [L]   random-k: Philox keys below tau are candidates
+  const uint32_t* seg_ulo;     // [L]   random-k: keys below ulo are winners if at most k_l are
+  const int32_t* chunk_sf;     // [nchunks] first / last segment of each data tile
   const int32_t* chunk_sl;
-  int32_t d, L, nchunks, ncrows;
+  const int32_t* row_seg;      // [nrows] segment of each row
+  int32_t d, L, nchunks, nrows, nruns;
 };
 
 // ---------------------------------------------------------------------------------------------
@@ -154,6 +165,53 @@ __device__ __forceinline__ void store4(float* p, uint32_t i0, int nv, const floa
   }
 }
 
+// Masked variants: vm has bit q set when element i0 + q is inside the row being processed.
+__device__ __forceinline__ uint32_t group_mask(uint32_t i0, uint32_t lo, uint32_t hi) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (i0 + q >= lo && i0 + q < hi) m |= 1u << q;
+  return m;
+}
+
+__device__ __forceinline__ void load4m(const float* p, uint32_t i0, uint32_t vm, float v[4]) {
+  if (vm == 0xFu) {
+    const f4 x = __builtin_nontemporal_load(reinterpret_cast<const f4*>(p + i0));
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = (vm >> q) & 1u ? p[i0 + q] : 0.0f;
+  }
+}
+
+template <int GDT>
+__device__ __forceinline__ void load4gm(const void* g, uint32_t i0, uint32_t vm, float v[4]) {
+  if constexpr (GDT == 0) {
+    load4m(reinterpret_cast<const float*>(g), i0, vm, v);
+  } else {
+    const uint16_t* p = reinterpret_cast<const uint16_t*>(g);
+    if (vm == 0xFu) {
+      const u2v x = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(p + i0));
+      v[0] = bf16_to_f32(x.x & 0xFFFFu); v[1] = bf16_to_f32(x.x >> 16);
+      v[2] = bf16_to_f32(x.y & 0xFFFFu); v[3] = bf16_to_f32(x.y >> 16);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = (vm >> q) & 1u ? bf16_to_f32(p[i0 + q]) : 0.0f;
+    }
+  }
+}
+
+__device__ __forceinline__ void store4m(float* p, uint32_t i0, uint32_t vm, const float v[4]) {
+  if (vm == 0xFu) {
+    const f4 x = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p + i0));
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if ((vm >> q) & 1u) p[i0 + q] = v[q];
+  }
+}
+
 // Segment containing element i, searching segments [sf, sl] (sf <= answer <= sl).
 __device__ __forceinline__ int seg_of(uint32_t i, int sf, int sl, const int32_t* off) {
   while (sf < sl) {
@@ -214,7 +272,7 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, u
 // reaches `need`.  Returns the bin (-1 if the histogram holds fewer than `need`) and, through
 // `above`, the count in strictly higher bins.  Every thread gets the result.
 template <int NT>
-__device__ int block_resolve(const uint32_t* hist, int nb, uint32_t need, uint32_t* lds, uint32_t& above) {
+__device__ __forceinline__ int block_resolve(const uint32_t* hist, int nb, uint32_t need, uint32_t* lds, uint32_t& above) {
   __shared__ int s_bin;
   __shared__ uint32_t s_above;
   constexpr int kMaxPer = (kHBins + NT - 1) / NT;

@@ -1,25 +1,27 @@
 // HIP kernels of the efsparse hot path (gfx950).
 //
-// Streaming kernels walk the gradient in chunks of kTile elements (one workgroup per chunk,
-// kRounds coalesced float4 groups per thread).  A chunk lies in one or more segments; the common
-// single-segment case takes uniform fast paths.
+// Streaming kernels walk the gradient in tiles of kTile elements (kRounds coalesced float4
+// groups per thread of a kNT-thread workgroup).  The selection kernels work on rows: a row is the
+// part of one segment inside one tile, so that every workgroup of the selection pipeline serves
+// exactly one segment.
 //
-// Top-k and random-k (Section 3) share one pipeline without any cross-workgroup synchronisation
-// inside a kernel:
-//   k_topk_sample   top-k only: per segment, a candidate threshold: exact (k-th largest key) for
-//                   segments of up to kSampleMax elements, otherwise from a sample of contiguous
-//                   runs spread over the segment, set so that the candidates very likely number
-//                   at least k_l.
-//   k_stream_sel    fused accumulate (acc = g + e, written to e) and candidate test (top-k: key >=
-//                   threshold; random-k: Philox key < tau_l, a binomial bound on k_l); every chunk
-//                   writes its candidates, in index order, to its own slot plus a count.
-//   k_select_emit   one workgroup per segment: gathers the segment's candidates, selects the k_l
-//                   winners exactly by radix levels (top-k: largest magnitude key; random-k:
-//                   smallest Philox key; ties to the lower index), writes them in index order to
-//                   the message and zeroes e there.  A segment with fewer than k_l candidates is
-//                   resolved exactly over all of its elements.
-// Block-random-k is one fused streaming pass (k_randblock_step).
-// The aggregate (Algorithm 1) accumulates each output tile in LDS in worker order.
+// Top-k and random-k (Section 3) share one pipeline; no kernel synchronises across workgroups:
+//   k_sample_gather  top-k only: the keys of a sample per segment (the whole segment when it has
+//   k_sample_select  at most kSampleMax elements, else runs spread over it); per segment either
+//                    the exact winner rule (small segments) or a candidate threshold set so that
+//                    the candidates very likely number at least k_l.
+//   k_randk_init     random-k only: clears the per-segment candidate histograms.
+//   k_stream_sel     per row: fused accumulate (acc = g + e, written to e), candidate test (top-k:
+//                    the rule above; random-k: Philox key < tau_l, a binomial bound on k_l), the
+//                    row's candidates in index order to its slot, and a histogram of them.
+//   k_resolve        per segment: the histogram bin holding the k_l-th best candidate.
+//   k_collect        per row: candidates above that bin are counted, those inside it are listed.
+//   k_select         per segment: the exact threshold among the listed candidates, then the
+//                    message offset of every row.
+//   k_emit           per row: the winners in index order to the message, e = +0 there.
+// A segment with fewer than k_l candidates is resolved exactly over all of its elements by
+// k_select.  Block-random-k is one fused streaming pass (k_randblock_step).  The aggregate
+// (Algorithm 1) accumulates each output tile in LDS in worker order.
 #pragma once
 
 #include "ef_device.h"
@@ -27,19 +29,52 @@
 namespace efs {
 
 struct WSel {
-  uint32_t* diag;       // [4]   diagnostics bits
-  uint32_t* res;        // [L][kResWords]
-  uint32_t* counts;     // [nchunks] candidates per chunk
-  uint32_t* cofs;       // [2 * ncrows] per segment: compacted non-empty chunk rows (ids, flat offsets)
-  uint32_t* cand_idx;   // [nchunks * kTile] per-chunk candidate slots
-  float* cand_val;      // [nchunks * kTile]
-  uint32_t* cand_key;   // [nchunks * kTile] selection key' of each candidate
-  uint32_t* dense_idx;  // [d] candidates of segment l, gathered to [o_l, o_l + N_l)
-  float* dense_val;     // [d]
-  uint32_t* dense_key;  // [d]
+  uint32_t* diag;      // [4]  diagnostics bits
+  uint32_t* res;       // [L][kResWords] per-segment selection record
+  uint32_t* hist;      // [L][kHCopies][kHBins] candidate histogram per segment, in copies that
+                       // spread the atomics of concurrent rows
+  uint32_t* samp;      // [nruns * kSampleRun] top-k sample keys
+  uint32_t* counts;    // [nrows] candidates per row
+  uint32_t* rcnt;      // [nrows] winners per row
+  uint32_t* roff;      // [nrows] message position of each row's first winner
+  uint32_t* lcnt;      // [L][kSubLists][kLineWords] sizes of the sub-lists, one cache line each
+  uint32_t* cand_idx;  // [nrows * kTile] per-row candidate slots, index order
+  float* cand_val;     // [nrows * kTile]
+  uint32_t* cand_key;  // [nrows * kTile] key' of each candidate
+  uint32_t* list_idx;  // [nrows * kTile] sub-lists of undecided candidates (see SubLists)
+  uint32_t* list_key;  // [nrows * kTile]
 };
 
 __device__ __forceinline__ uint32_t* res_of(const WSel& w, int l) { return w.res + (size_t)l * kResWords; }
+constexpr int kLineWords = 32;  // 128-byte L2 line: counters hit by many atomics get a line each
+__device__ __forceinline__ uint32_t* lcnt_of(const WSel& w, int l, uint32_t c) {
+  return w.lcnt + ((size_t)l * kSubLists + c) * kLineWords;
+}
+
+// Entry t of sub-list c of the segment whose rows start at r0 is stored in the slot of row
+// r0 + c + kSubLists * (t / kTile), at t % kTile.  Sub-list c only takes entries of the rows
+// r0 + c + kSubLists * j (at most kTile each), so it never runs past the segment's rows.
+__device__ __forceinline__ size_t sublist_pos(uint32_t r0, uint32_t c, uint32_t t) {
+  return (size_t)(r0 + c + kSubLists * (t / kTile)) * kTile + (t % kTile);
+}
+
+// The sub-lists of one segment read as one array of M[kSubLists] entries (any order).
+struct SubLists {
+  const uint32_t* arr;
+  uint32_t r0;
+  uint32_t M[kSubLists + 1];  // M[c]: entries in sub-lists before c
+  __device__ __forceinline__ uint32_t operator[](uint32_t f) const {
+    uint32_t c = 0, base = 0;
+#pragma unroll
+    for (int x = 1; x < kSubLists; ++x) {
+      if (f >= M[x]) {
+        c = (uint32_t)x;
+        base = M[x];
+      }
+    }
+    return arr[sublist_pos(r0, c, f - base)];
+  }
+};
 
 // ---------------------------------------------------------------------------------------------
 // Utility kernels
@@ -319,8 +354,12 @@ __device__ __forceinline__ uint32_t sel_key(uint32_t idx, float val, uint32_t o,
 }
 
 constexpr int kBatch = 8;             // independent loads in flight per thread in the selection passes
-constexpr uint32_t kKeysLds = 28672;   // candidate keys held in LDS (larger sets stay in global memory)
-constexpr uint32_t kCofsLds = 4096;    // chunk rows whose flat offsets stay in LDS
+constexpr uint32_t kListLds = 8192;    // listed candidates held in LDS by k_select
+constexpr uint32_t kRowsLds = 16384;   // rows per segment whose list additions k_select counts in LDS
+constexpr uint32_t kRankList = 256;    // lists up to this size are ranked directly (no radix levels)
+constexpr uint32_t kHistDirect = 256;  // rows with more candidates histogram them in LDS first
+constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
+constexpr uint32_t kDiagCount = 4u;    // diagnostics: the row counts of a segment did not add up to k_l
 
 // Workgroup-wide AND and OR of per-thread values; `lds` holds 2 * kSelNT / 64 words.
 __device__ __forceinline__ void block_and_or(uint32_t& a, uint32_t& o, uint32_t* lds) {
@@ -346,9 +385,9 @@ __device__ __forceinline__ void block_and_or(uint32_t& a, uint32_t& o, uint32_t*
   __syncthreads();
 }
 
-// Calls fn(key) for every keys[f], f < n, in a strided order with kBatch loads in flight.
-template <typename F>
-__device__ __forceinline__ void for_keys(const uint32_t* keys, uint32_t n, F fn) {
+// Calls fn(f, keys[f]) for every f < n, in a strided order with kBatch loads in flight.
+template <typename K, typename F>
+__device__ __forceinline__ void for_keys(const K& keys, uint32_t n, F fn) {
   for (uint32_t base = 0; base < n; base += (uint32_t)kSelNT * kBatch) {
     uint32_t k[kBatch];
 #pragma unroll
@@ -359,7 +398,7 @@ __device__ __forceinline__ void for_keys(const uint32_t* keys, uint32_t n, F fn)
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const uint32_t f = base + (uint32_t)u * kSelNT + threadIdx.x;
-      if (f < n) fn(k[u]);
+      if (f < n) fn(f, k[u]);
     }
   }
 }
@@ -368,7 +407,8 @@ __device__ __forceinline__ void for_keys(const uint32_t* keys, uint32_t n, F fn)
 // the keys > T plus the first r keys == T.  kand / kor are the AND and OR of all keys; the levels
 // (11 bits each) start at the highest bit in which the keys differ, so concentrated keys still
 // spread over the histogram.
-__device__ void block_select(const uint32_t* keys, uint32_t n, uint32_t need, uint32_t kand, uint32_t kor,
+template <typename K>
+__device__ __forceinline__ void block_select(const K& keys, uint32_t n, uint32_t need, uint32_t kand, uint32_t kor,
                              uint32_t* hist, uint32_t* lds, uint32_t& T_out, uint32_t& r_out) {
   const uint32_t diff = kand ^ kor;
   if (diff == 0) {  // all keys equal
@@ -386,7 +426,7 @@ __device__ void block_select(const uint32_t* keys, uint32_t n, uint32_t need, ui
     __syncthreads();
     const uint32_t pmask = known == 0 ? 0u : (0xFFFFFFFFu << (32 - known));
     const uint32_t want = prefix & pmask;
-    for_keys(keys, n, [&](uint32_t k) {
+    for_keys(keys, n, [&](uint32_t, uint32_t k) {
       if ((k & pmask) == want) atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u);
     });
     __syncthreads();
@@ -398,197 +438,6 @@ __device__ void block_select(const uint32_t* keys, uint32_t n, uint32_t need, ui
   }
   T_out = prefix;
   r_out = need;
-}
-
-// Top-k candidate threshold per segment (one workgroup per segment): the lower edge of the
-// 11-bit histogram bin (starting at the highest bit in which the sampled keys differ) that holds
-// the rank-th largest sampled key.  Exact k-th largest key when the whole segment fits the sample.
-template <int GDT, bool FUSED>
-__global__ __launch_bounds__(kSelNT) void k_topk_sample(Tables T, const void* g, const float* src, WSel ws) {
-  constexpr uint32_t runs = kSampleMax / kSampleRun;
-  __shared__ uint32_t keys[kSampleMax];
-  __shared__ uint32_t hist[kHBins];
-  __shared__ uint32_t lds[2 * kSelNT / 64];
-  __shared__ uint32_t run_start[runs];
-  const int l = blockIdx.x;
-  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
-  EFS_PHASE(8);
-  constexpr int per = kSampleMax / kSelNT;
-  const bool exact = n <= (uint32_t)kSampleMax;
-  const uint32_t m = exact ? n : (uint32_t)kSampleMax;
-  const uint32_t rank = exact ? (uint32_t)T.seg_k[l] : (uint32_t)T.seg_srank[l];
-  // runs of kSampleRun contiguous elements, evenly spaced over the segment
-  if (!exact && threadIdx.x < runs)
-    run_start[threadIdx.x] = o + (uint32_t)(((uint64_t)threadIdx.x * (n - kSampleRun)) / (runs - 1));
-  __syncthreads();
-  float a[per];
-#pragma unroll
-  for (int u = 0; u < per; ++u) {
-    const uint32_t j = (uint32_t)(u * kSelNT) + threadIdx.x;
-    const uint32_t i = exact ? o + j : run_start[j / kSampleRun] + j % kSampleRun;
-    a[u] = 0.0f;
-    if (j < m) {
-      if constexpr (FUSED) a[u] = load1g<GDT>(g, i) + src[i];
-      else a[u] = src[i];
-    }
-  }
-  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
-#pragma unroll
-  for (int u = 0; u < per; ++u) {
-    const uint32_t j = (uint32_t)(u * kSelNT) + threadIdx.x;
-    if (j < m) {
-      const uint32_t k = mag_key(a[u]);
-      keys[j] = k;
-      kand &= k;
-      kor |= k;
-    }
-  }
-  block_and_or(kand, kor, lds);
-  EFS_PHASE(9);
-  uint32_t thr;
-  if (exact) {
-    uint32_t r_unused;
-    block_select(keys, m, rank, kand, kor, hist, lds, thr, r_unused);
-  } else if (kand == kor) {
-    thr = kand;
-  } else {
-    const int h = 31 - __clz(kand ^ kor);
-    const int w = min(11, h + 1), shift = h + 1 - w;
-    const uint32_t prefix = h == 31 ? 0u : (kand & (0xFFFFFFFFu << (h + 1)));
-    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
-    __syncthreads();
-    for_keys(keys, m, [&](uint32_t k) { atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u); });
-    __syncthreads();
-    uint32_t above;
-    const int bin = block_resolve<kSelNT>(hist, 1 << w, rank, lds, above);
-    thr = prefix | ((uint32_t)max(bin, 0) << shift);
-  }
-  EFS_PHASE(11);
-  if (threadIdx.x == 0) res_of(ws, l)[R_THR] = thr;
-}
-
-// Fused accumulate + candidate test + per-chunk ordered compaction into the chunk's slot.
-template <int KIND, int GDT, bool FUSED>
-__global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
-                                                    uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
-  __shared__ uint32_t wt[kRounds][kNT / 64];
-  const uint32_t c = blockIdx.x;
-  const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
-  const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-  const bool uni = sf == sl;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const uint32_t o_u = (uint32_t)T.seg_off[sf];
-  uint32_t thr_u = 0;
-  uint64_t tau_u = 0;
-  if constexpr (KIND == 0) thr_u = res_of(ws, sf)[R_THR];
-  else tau_u = T.seg_tau[sf];
-  const bool aligned = uni && (o_u & 3u) == 0;
-
-  float v[kRounds][4];
-  if constexpr (FUSED) {
-    float gv[kRounds][4];
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-      load4g<GDT>(g, i0, nv, gv[r]);
-      load4(src, i0, nv, v[r]);
-    }
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
-      store4(acc_out, i0, nv, v[r]);
-    }
-  } else {
-#pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-      load4(src, i0, nv, v[r]);
-    }
-  }
-  // candidate flags; wave-level prefixes through ballots, one barrier for the whole chunk
-  uint32_t mask[kRounds], lpre[kRounds];
-  uint32_t kk[kRounds][4];  // key' of each element (random-k: ~Philox key)
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    uint32_t mk = 0;
-    if constexpr (KIND == 0) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        kk[r][q] = mag_key(v[r][q]);
-        if (q < nv) {
-          uint32_t thr = thr_u;
-          if (!uni) thr = res_of(ws, seg_of(i0 + q, sf, sl, T.seg_off))[R_THR];
-          if (kk[r][q] >= thr) mk |= 1u << q;
-        }
-      }
-    } else {
-      if (aligned) {
-        uint4 x = make_uint4(0u, 0u, 0u, 0u);
-        if (nv > 0) x = philox(make_uint4((i0 - o_u) >> 2, 0u, step, kRandkTag | (uint32_t)sf), s0, s1);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          kk[r][q] = ~word(x, q);
-          if (q < nv && (uint64_t)word(x, q) < tau_u) mk |= 1u << q;
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          kk[r][q] = 0u;
-          if (q < nv) {
-            const uint32_t i = i0 + q;
-            const int l = uni ? sf : seg_of(i, sf, sl, T.seg_off);
-            const uint32_t u = randk_key(i - (uint32_t)T.seg_off[l], (uint32_t)l, step, s0, s1);
-            kk[r][q] = ~u;
-            if ((uint64_t)u < T.seg_tau[l]) mk |= 1u << q;
-          }
-        }
-      }
-    }
-    mask[r] = mk;
-    uint32_t pre = 0, tot = 0;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint64_t b = __ballot((mk >> q) & 1u);
-      pre += lanes_below(b);
-      tot += (uint32_t)__popcll(b);
-    }
-    lpre[r] = pre;
-    if (lane == 0) wt[r][wid] = tot;
-  }
-  __syncthreads();
-  uint32_t base = 0;
-  uint32_t* cidx = ws.cand_idx + (size_t)c * kTile;
-  float* cval = ws.cand_val + (size_t)c * kTile;
-  uint32_t* ckey = ws.cand_key + (size_t)c * kTile;
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    uint32_t rb = base;
-#pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) rb += w < wid ? wt[r][w] : 0u;
-    if (mask[r]) {
-      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      uint32_t pos = rb + lpre[r];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if ((mask[r] >> q) & 1u) {
-          cidx[pos] = i0 + q;
-          cval[pos] = v[r][q];
-          ckey[pos] = kk[r][q];
-          ++pos;
-        }
-      }
-    }
-#pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) base += wt[r][w];
-  }
-  if (threadIdx.x == 0) ws.counts[c] = base;
 }
 
 // Exact selection over the whole segment (used when the candidates cannot contain the answer):
@@ -642,259 +491,765 @@ __device__ void slow_select(const Tables& T, int l, const float* data, float* e_
   }
 }
 
-// Per-segment exact selection among the candidates in the chunk slots, and the emission of the
-// k_l winners in index order (one workgroup per segment).  Every pass is wave-contiguous: wave w
-// owns a contiguous share of the flat (= index) order of the candidates and walks it 64 entries at
-// a time with kBatch loads in flight, so accesses stay coalesced.  The gather copies the
-// candidates to dense arrays at [o_l, o_l + N) (N <= d_l; keys to LDS when they fit), the radix
-// levels sweep the keys, and the emission uses in-wave ballot prefixes plus one scan of the wave
-// totals.  The row offsets and keys live either in LDS or in global memory; each placement is its
-// own instantiation so that every access has a known address space (no flat accesses, whose waits
-// would serialise the batches).
-// Last position m >= i with off[m] <= f (off strictly increasing over [0, n); off[i] <= f).
-__device__ __forceinline__ uint32_t advance_row(const uint32_t* off, uint32_t n, uint32_t i, uint32_t f) {
-  if (i + 1 >= n || off[i + 1] > f) return i;
-  uint32_t lo = i + 1, hi, step = 1;
-  while (true) {  // gallop until off[hi] > f
-    hi = lo + step;
-    if (hi >= n) {
-      hi = n;
-      break;
-    }
-    if (off[hi] > f) break;
-    lo = hi;
-    step <<= 1;
-  }
-  while (hi - lo > 1) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (off[mid] <= f) lo = mid; else hi = mid;
-  }
-  return lo;
+// ---------------------------------------------------------------------------------------------
+// Workgroup helpers of the per-segment kernels (kSelNT threads)
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* lds) {
+#pragma unroll
+  for (int s = 32; s > 0; s >>= 1) v = max(v, (uint32_t)__shfl_xor(v, s, 64));
+  constexpr int nw = kSelNT / 64;
+  if ((threadIdx.x & 63) == 0) lds[threadIdx.x >> 6] = v;
+  __syncthreads();
+  v = 0;
+#pragma unroll
+  for (int w = 0; w < nw; ++w) v = max(v, lds[w]);
+  __syncthreads();
+  return v;
 }
 
-struct SelSeg {
-  int l;
-  uint32_t o, kl, P, c0, nc, a0, b1, N;
-};
-
-template <int KIND, bool KEYS_LDS>
-__device__ __forceinline__ void select_emit_tail(const Tables& T, const WSel& ws, const SelSeg& S, const uint32_t* crow,
-                                                 const uint32_t* coff, uint32_t nnz, uint32_t* keys, float* e_zero,
-                                                 uint32_t* out_idx, float* out_val, uint32_t* hist, uint32_t* lds,
-                                                 uint32_t (*s_wtot)[kSelNT / 64]) {
+// Position of the r-th (1-based) entry equal to x among keys[0, m), in position order.  Each
+// wave owns a contiguous share of the positions; `lds` holds kSelNT / 64 words.
+__device__ __forceinline__ uint32_t block_nth_equal(const uint32_t* keys, uint32_t m, uint32_t x, uint32_t r, uint32_t* lds) {
+  __shared__ uint32_t s_pos;
   constexpr int NW = kSelNT / 64;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const uint32_t N = S.N;
-  const uint32_t W0 = (uint32_t)(((uint64_t)N * wid) / NW), W1 = (uint32_t)(((uint64_t)N * (wid + 1)) / NW);
-  uint32_t* didx = ws.dense_idx + S.o;
-  float* dval = ws.dense_val + S.o;
-  // gather
-  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
-  {
-    // m0: the non-empty row holding the wave's next flat position (wave-uniform).  For 64
-    // consecutive positions the rows involved are m0 .. m0+63 at most (every row is non-empty):
-    // each lane loads one row boundary and finds its own row by a shuffle binary search.
-    uint32_t m0 = advance_row(coff, nnz, 0, W0 < W1 ? W0 : 0u);
-    for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
-      size_t at[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const uint32_t fb = base + (uint32_t)u * 64u;  // wave-uniform
-        const uint32_t f = fb + lane;
-        const uint32_t mb = m0 + lane;
-        const uint32_t bnd = mb < nnz ? coff[mb] : 0xFFFFFFFFu;
-        const uint32_t rid = mb < nnz ? crow[mb] : 0u;
-        uint32_t j = 0;  // last j with boundary(m0 + j) <= f
-#pragma unroll
-        for (int st = 32; st > 0; st >>= 1) {
-          const uint32_t cand = j + (uint32_t)st;
-          const uint32_t bc = __shfl(bnd, (int)min(cand, 63u), 64);
-          if (cand < 64u && bc <= f) j = cand;
-        }
-        const uint32_t row = __shfl(rid, (int)j, 64), off = __shfl(bnd, (int)j, 64);
-        at[u] = f < W1 ? (size_t)(S.c0 + row) * kTile + (row == 0 ? S.a0 : 0u) + (f - off) : 0;
-        // row of the next wave-step's first position (fb + 64): lane 63's row, or the one after
-        const uint32_t j63 = __shfl(j, 63, 64);
-        uint32_t nb = __shfl(bnd, (int)min(j63 + 1u, 63u), 64);
-        if (j63 == 63u) nb = m0 + 64u < nnz ? coff[m0 + 64u] : 0xFFFFFFFFu;  // every row held one position
-        m0 += j63 + (nb <= fb + 64u ? 1u : 0u);
-      }
-      uint32_t ci[kBatch], ck[kBatch];
-      float cv[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const bool in = base + (uint32_t)u * 64u + lane < W1;
-        ci[u] = in ? ws.cand_idx[at[u]] : 0u;
-        cv[u] = in ? ws.cand_val[at[u]] : 0.0f;
-        ck[u] = in ? ws.cand_key[at[u]] : 0u;
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const uint32_t f = base + (uint32_t)u * 64u + lane;
-        if (f < W1) {
-          didx[f] = ci[u];
-          dval[f] = cv[u];
-          keys[f] = ck[u];
-          kand &= ck[u];
-          kor |= ck[u];
-        }
-      }
-    }
+  const uint32_t W0 = (uint32_t)(((uint64_t)m * wid) / NW), W1 = (uint32_t)(((uint64_t)m * (wid + 1)) / NW);
+  uint32_t cnt = 0;
+  for (uint32_t b = W0; b < W1; b += 64) {
+    const uint32_t f = b + lane;
+    cnt += (uint32_t)__popcll(__ballot(f < W1 && keys[f] == x));
   }
-  block_and_or(kand, kor, lds);  // also makes the gathered data visible to the workgroup
-  EFS_PHASE(3);
-  uint32_t Tk, r;
-  block_select(keys, N, S.kl, kand, kor, hist, lds, Tk, r);
-  EFS_PHASE(4);
-  // emission in flat (= index) order
-  uint32_t na = 0, nb = 0;
-  for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
-    uint32_t k[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const uint32_t f = base + (uint32_t)u * 64u + lane;
-      k[u] = f < W1 ? keys[f] : 0u;
+  if (lane == 0) lds[wid] = cnt;
+  if (threadIdx.x == 0) s_pos = m;
+  __syncthreads();
+  uint32_t before = 0;
+  for (int w = 0; w < wid; ++w) before += lds[w];
+  if (before < r && r <= before + cnt) {  // wave-uniform: this wave holds the r-th match
+    uint32_t run = before;
+    for (uint32_t b = W0; b < W1; b += 64) {
+      const uint32_t f = b + lane;
+      const bool t = f < W1 && keys[f] == x;
+      const uint64_t mk = __ballot(t);
+      const uint32_t c = (uint32_t)__popcll(mk);
+      if (run + c >= r) {
+        if (t && run + lanes_below(mk) + 1 == r) s_pos = f;
+        break;
+      }
+      run += c;
     }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const bool in = base + (uint32_t)u * 64u + lane < W1;
-      na += (uint32_t)__popcll(__ballot(in && k[u] > Tk));
-      nb += (uint32_t)__popcll(__ballot(in && k[u] == Tk));
-    }
-  }
-  if (lane == 0) {
-    s_wtot[0][wid] = na;
-    s_wtot[1][wid] = nb;
   }
   __syncthreads();
-  uint32_t ra = 0, rb = 0;
-  for (int w = 0; w < wid; ++w) {
-    ra += s_wtot[0][w];
-    rb += s_wtot[1][w];
-  }
-  EFS_PHASE(5);
-  for (uint32_t base = W0; base < W1; base += 64u * kBatch) {
-    uint32_t k[kBatch], ix[kBatch];
-    float vv[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const uint32_t f = base + (uint32_t)u * 64u + lane;
-      const bool in = f < W1;
-      k[u] = in ? keys[f] : 0u;
-      ix[u] = in ? didx[f] : 0u;
-      vv[u] = in ? dval[f] : 0.0f;
-    }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const bool in = base + (uint32_t)u * 64u + lane < W1;
-      const bool a = in && k[u] > Tk, b = in && k[u] == Tk;
-      const uint64_t ma = __ballot(a), mb = __ballot(b);
-      const uint32_t ea = ra + lanes_below(ma), eb = rb + lanes_below(mb);
-      if ((a || (b && eb < r)) && ea + min(eb, r) < S.kl) {
-        const uint32_t pos = S.P + ea + min(eb, r);
-        out_idx[pos] = ix[u];
-        out_val[pos] = vv[u];
-        if (e_zero && ix[u] < (uint32_t)T.d) e_zero[ix[u]] = 0.0f;
+  const uint32_t p = s_pos;
+  __syncthreads();
+  return p;
+}
+
+// The r-th smallest idx[j] (r >= 1, indices distinct) among the j < m with keys[j] == x: radix
+// levels over ~idx, whose largest values are the smallest indices.
+template <typename K>
+__device__ __forceinline__ uint32_t block_nth_smallest_tie(const K& keys, const K& idx, uint32_t m, uint32_t x,
+                                           uint32_t r, uint32_t* hist, uint32_t* lds) {
+  uint32_t prefix = 0, need = r;
+  int known = 0;
+  while (known < 32) {
+    const int w = min(11, 32 - known);
+    const int shift = 32 - known - w;
+    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
+    __syncthreads();
+    const uint32_t pmask = known == 0 ? 0u : (0xFFFFFFFFu << (32 - known));
+    for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
+      if (keys[j] == x) {
+        const uint32_t v = ~idx[j];
+        if ((v & pmask) == (prefix & pmask)) atomicAdd(&hist[(v >> shift) & ((1u << w) - 1u)], 1u);
       }
-      ra += (uint32_t)__popcll(ma);
-      rb += (uint32_t)__popcll(mb);
+    }
+    __syncthreads();
+    uint32_t above;
+    const int bin = block_resolve<kSelNT>(hist, 1 << w, need, lds, above);
+    prefix |= (uint32_t)max(bin, 0) << shift;
+    need -= above;
+    known += w;
+  }
+  return ~prefix;
+}
+
+// Candidate histogram bin of a top-k key (higher bins hold larger keys): (key - A) >> sh, clamped
+// to the last bin.
+__device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t sh) {
+  return min((key - A) >> sh, (uint32_t)kHBins - 1u);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Top-k sample
+// ---------------------------------------------------------------------------------------------
+// One workgroup of kSampleRun threads per run: a segment of up to kSampleMax elements is sampled
+// whole (runs of consecutive positions), a larger one by kSampleMax / kSampleRun runs of
+// kSampleRun contiguous elements evenly spread over it.  The runs of a sampled segment also clear
+// its candidate histogram (kHCopies * kHBins = kSampleMax words, one slice per run).
+static_assert(kHCopies * kHBins == kSampleMax, "one histogram slice per sample run");
+template <int GDT, bool FUSED>
+__global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, const void* g, const float* src, WSel ws) {
+  const uint32_t r = blockIdx.x;
+  const int l = seg_of(r, 0, T.L - 1, T.seg_ro);
+  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
+  const uint32_t q = r - (uint32_t)T.seg_ro[l];
+  uint32_t i;
+  bool in = true;
+  if (n <= (uint32_t)kSampleMax) {
+    const uint32_t j = q * kSampleRun + threadIdx.x;
+    in = j < n;
+    i = o + j;
+  } else {
+    constexpr uint32_t runs = kSampleMax / kSampleRun;
+    i = o + (uint32_t)(((uint64_t)q * (n - kSampleRun)) / (runs - 1)) + threadIdx.x;
+    ws.hist[(size_t)l * kHCopies * kHBins + q * kSampleRun + threadIdx.x] = 0u;
+  }
+  uint32_t key = 0;
+  if (in) {
+    float a;
+    if constexpr (FUSED) a = load1g<GDT>(g, i) + src[i];
+    else a = src[i];
+    key = mag_key(a);
+  }
+  ws.samp[(size_t)r * kSampleRun + threadIdx.x] = key;
+}
+
+// Per segment (one workgroup) the candidate rule of the streaming pass:
+//  * at most kSampleMax elements: the exact k_l-th largest key T over the whole segment and the
+//    bound I (one past the index of the last tie sent; ties go to lower indices); the candidates
+//    are then exactly the winners (mode 1).
+//  * larger segments: A = the lower edge of the bin of the top 11 key bits that holds the
+//    srank-th largest sampled key; every key >= A is a candidate, and the candidates are
+//    histogrammed by (key - A) >> sh with sh chosen so that the largest sampled key falls below
+//    bin 1024 (mode 0).
+__global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws) {
+  __shared__ uint32_t keys[kSampleMax];
+  __shared__ uint32_t hist[kHBins];
+  __shared__ uint32_t lds[2 * kSelNT / 64];
+  const int l = blockIdx.x;
+  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
+  const uint32_t* sk = ws.samp + (size_t)T.seg_ro[l] * kSampleRun;
+  uint32_t* R = res_of(ws, l);
+  if (n <= (uint32_t)kSampleMax) {
+    uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+    for_keys(sk, n, [&](uint32_t f, uint32_t k) {
+      keys[f] = k;
+      kand &= k;
+      kor |= k;
+    });
+    block_and_or(kand, kor, lds);  // its barriers also publish keys[]
+    uint32_t Tk, r;
+    block_select(keys, n, (uint32_t)T.seg_k[l], kand, kor, hist, lds, Tk, r);
+    const uint32_t it = o + block_nth_equal(keys, n, Tk, r, lds) + 1u;
+    if (threadIdx.x == 0) {
+      R[R_A] = Tk;
+      R[R_IA] = it;
+      R[R_T] = Tk;
+      R[R_IT] = it;
+      R[R_MODE] = 1;
+      R[R_SLOW] = 0;
+    }
+    return;
+  }
+  // sampled: bins of the top 11 key bits (8 exponent + 3 mantissa bits); keys stay in registers
+  for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
+  __syncthreads();
+  uint32_t kmax = 0u;
+  for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+    atomicAdd(&hist[k >> 20], 1u);
+    kmax = max(kmax, k);
+  });
+  __syncthreads();
+  kmax = block_max_u32(kmax, lds);
+  const uint32_t rank = (uint32_t)T.seg_srank[l];
+  uint32_t thr = 0;  // rank >= sample size: every element is a candidate
+  if (rank < (uint32_t)kSampleMax) {
+    uint32_t above;
+    const int bin = block_resolve<kSelNT>(hist, kHBins, rank, lds, above);
+    thr = (uint32_t)max(bin, 0) << 20;
+    if (bin >= 0 && hist[bin] > (uint32_t)kSampleMax / 8) {
+      // concentrated keys: refine inside the bin by the next 11 bits (sample re-read from L2)
+      __syncthreads();
+      for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
+      __syncthreads();
+      for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+        if ((k >> 20) == (uint32_t)bin) atomicAdd(&hist[(k >> 9) & (kHBins - 1)], 1u);
+      });
+      __syncthreads();
+      uint32_t above2;
+      const int bin2 = block_resolve<kSelNT>(hist, kHBins, rank - above, lds, above2);
+      thr |= (uint32_t)max(bin2, 0) << 9;
     }
   }
-  EFS_PHASE(6);
+  const uint32_t span = kmax - thr;
+  const uint32_t sh = span < 1024u ? 0u : (uint32_t)(32 - __clz(span)) - 10u;
   if (threadIdx.x == 0) {
-    uint32_t* R = res_of(ws, S.l);
-    R[R_T] = Tk;
-    R[R_R] = r;
-    R[R_N] = N;
+    R[R_A] = thr;
+    R[R_IA] = 0xFFFFFFFFu;
+    R[R_SH] = sh;
+    R[R_MODE] = 0;
     R[R_SLOW] = 0;
   }
 }
 
-// Row offsets of the segment's candidates, then either the exact whole-segment path (too few
-// candidates) or the selection over the candidates.
-template <int KIND, bool COFS_LDS>
-__device__ __forceinline__ void select_emit_body(const Tables& T, const WSel& ws, SelSeg S, uint32_t* crow,
-                                                 uint32_t* coff, const float* data, float* e_zero, uint32_t* out_idx,
-                                                 float* out_val, uint32_t s0, uint32_t s1, uint32_t step,
-                                                 uint32_t* hist, uint32_t* lds, uint32_t* s_keys,
-                                                 uint32_t (*s_wtot)[kSelNT / 64]) {
-  // non-empty chunk rows of the segment, compacted: crow = row id, coff = flat offset of its first
-  // candidate (strictly increasing)
-  uint32_t N = 0, nnz = 0;
-  for (uint32_t i0 = 0; i0 < S.nc; i0 += kSelNT) {
-    const uint32_t i = i0 + threadIdx.x;
-    uint32_t cnt = 0;
-    if (i < S.nc) cnt = (i == S.nc - 1 ? S.b1 : ws.counts[S.c0 + i]) - (i == 0 ? S.a0 : 0u);
-    uint32_t tot, totn;
-    const uint32_t ex = block_excl_scan<kSelNT>(cnt, lds, tot);
-    const uint32_t exn = block_excl_scan<kSelNT>(cnt ? 1u : 0u, lds, totn);
-    if (cnt) {
-      crow[nnz + exn] = i;
-      coff[nnz + exn] = N + ex;
-    }
-    N += tot;
-    nnz += totn;
+// ---------------------------------------------------------------------------------------------
+// Streaming pass: fused accumulate + candidate test + ordered compaction into the row's slot
+// (+ top-k: candidate histogram).  One workgroup per row.
+// ---------------------------------------------------------------------------------------------
+template <int KIND, int GDT, bool FUSED>
+__global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
+                                                    uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
+  __shared__ uint32_t wt[kRounds][kNT / 64];
+  __shared__ uint32_t s_hist[KIND == 0 ? kHBins : 1];
+  const uint32_t row = blockIdx.x;
+  const int l = T.row_seg[row];
+  const uint32_t o = (uint32_t)T.seg_off[l], e_ = (uint32_t)T.seg_off[l + 1];
+  const uint32_t tb = (o / kTile + (row - (uint32_t)T.seg_cbase[l])) * kTile;
+  const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t* R = res_of(ws, l);
+  uint32_t mode = 1, A = 0, IA = 0, sh = 0;
+  uint64_t tau = 0;
+  if constexpr (KIND == 0) {
+    mode = R[R_MODE];
+    A = R[R_A];
+    IA = R[R_IA];
+    sh = R[R_SH];
+  } else {
+    tau = T.seg_tau[l];
+    // the list counter of k_collect starts from zero (this kernel completes before it runs)
+    if (row == (uint32_t)T.seg_cbase[l] && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
   }
-  S.N = N;
-  if (N < S.kl) {  // the candidates cannot hold the answer: exact pass over the whole segment
-    slow_select<KIND>(T, S.l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
-    if (threadIdx.x == 0) {
-      uint32_t* R = res_of(ws, S.l);
-      R[R_SLOW] = 1;
-      R[R_N] = N;
-      atomicOr(ws.diag, kDiagSlowPath);
+
+  float v[kRounds][4];
+  uint32_t vm[kRounds];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) vm[r] = group_mask(tb + (uint32_t)(r * kNT + threadIdx.x) * 4u, lo, hi);
+  if constexpr (FUSED) {
+    float gv[kRounds][4];
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      load4gm<GDT>(g, i0, vm[r], gv[r]);
+      load4m(src, i0, vm[r], v[r]);
     }
-    return;
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
+      store4m(acc_out, i0, vm[r], v[r]);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kRounds; ++r) load4m(src, tb + (uint32_t)(r * kNT + threadIdx.x) * 4u, vm[r], v[r]);
+  }
+  // candidate flags; wave-level prefixes through ballots, one barrier for the whole row
+  uint32_t mask[kRounds], lpre[kRounds];
+  uint32_t kk[kRounds][4];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    uint32_t mk = 0;
+    if constexpr (KIND == 0) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        kk[r][q] = mag_key(v[r][q]);
+        if (((vm[r] >> q) & 1u) && (kk[r][q] > A || (kk[r][q] == A && i0 + q < IA))) mk |= 1u << q;
+      }
+    } else {
+      if ((o & 3u) == 0) {  // the float4 group is one Philox block
+        uint4 x = make_uint4(0u, 0u, 0u, 0u);
+        if (vm[r]) x = philox(make_uint4((i0 - o) >> 2, 0u, step, kRandkTag | (uint32_t)l), s0, s1);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          kk[r][q] = ~word(x, q);
+          if (((vm[r] >> q) & 1u) && (uint64_t)word(x, q) < tau) mk |= 1u << q;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          kk[r][q] = 0u;
+          if ((vm[r] >> q) & 1u) {
+            const uint32_t u = randk_key(i0 + q - o, (uint32_t)l, step, s0, s1);
+            kk[r][q] = ~u;
+            if ((uint64_t)u < tau) mk |= 1u << q;
+          }
+        }
+      }
+    }
+    mask[r] = mk;
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint64_t b = __ballot((mk >> q) & 1u);
+      pre += lanes_below(b);
+      tot += (uint32_t)__popcll(b);
+    }
+    lpre[r] = pre;
+    if (lane == 0) wt[r][wid] = tot;
   }
   __syncthreads();
-  EFS_PHASE(2);
-  if (N <= kKeysLds)
-    select_emit_tail<KIND, true>(T, ws, S, crow, coff, nnz, s_keys, e_zero, out_idx, out_val, hist, lds, s_wtot);
-  else
-    select_emit_tail<KIND, false>(T, ws, S, crow, coff, nnz, ws.dense_key + S.o, e_zero, out_idx, out_val, hist, lds,
-                                  s_wtot);
+  uint32_t base = 0;
+  uint32_t* cidx = ws.cand_idx + (size_t)row * kTile;
+  float* cval = ws.cand_val + (size_t)row * kTile;
+  uint32_t* ckey = ws.cand_key + (size_t)row * kTile;
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    uint32_t rb = base;
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) rb += w < wid ? wt[r][w] : 0u;
+    if (mask[r]) {
+      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      uint32_t pos = rb + lpre[r];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if ((mask[r] >> q) & 1u) {
+          cidx[pos] = i0 + q;
+          cval[pos] = v[r][q];
+          ckey[pos] = kk[r][q];
+          ++pos;
+        }
+      }
+    }
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) base += wt[r][w];
+  }
+  if (threadIdx.x == 0) ws.counts[row] = base;
+  if constexpr (KIND == 0) {
+    if (mode == 0 && base) {
+      uint32_t* gh = ws.hist + ((size_t)l * kHCopies + (row % kHCopies)) * kHBins;
+      if (base > kHistDirect) {  // many candidates: count them in LDS, then one atomic per used bin
+        for (int b = threadIdx.x; b < kHBins; b += kNT) s_hist[b] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if ((mask[r] >> q) & 1u) atomicAdd(&s_hist[cand_bin(kk[r][q], A, sh)], 1u);
+        __syncthreads();
+        for (int b = threadIdx.x; b < kHBins; b += kNT) {
+          const uint32_t c = s_hist[b];
+          if (c) atomicAdd(&gh[b], c);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if ((mask[r] >> q) & 1u) atomicAdd(&gh[cand_bin(kk[r][q], A, sh)], 1u);
+      }
+    }
+  }
 }
 
-template <int KIND>
-__global__ __launch_bounds__(kSelNT) void k_select_emit(Tables T, WSel ws, const float* data, float* e_zero,
-                                                        uint32_t* out_idx, float* out_val, uint32_t s0,
-                                                        uint32_t s1, uint32_t step) {
-  constexpr int NW = kSelNT / 64;
+// Top-k, per segment: the histogram bin B holding the k_l-th best candidate and how many winners
+// it still has to give; fewer than k_l candidates in all marks the segment for the exact path.
+__global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws) {
   __shared__ uint32_t hist[kHBins];
-  __shared__ uint32_t lds[2 * NW];
-  __shared__ uint32_t s_crow[kCofsLds];
-  __shared__ uint32_t s_coff[kCofsLds];
-  __shared__ uint32_t s_keys[kKeysLds];
-  __shared__ uint32_t s_wtot[2][NW];
-  __shared__ uint32_t s_a0, s_b1;
-  SelSeg S;
-  S.l = blockIdx.x;
-  S.o = (uint32_t)T.seg_off[S.l];
-  const uint32_t e_ = (uint32_t)T.seg_off[S.l + 1];
-  S.kl = (uint32_t)T.seg_k[S.l];
-  S.P = (uint32_t)T.seg_P[S.l];
-  S.c0 = S.o / kTile;
-  S.nc = (e_ - 1) / kTile - S.c0 + 1;
-  const uint32_t c1 = S.c0 + S.nc - 1;
-  EFS_PHASE(0);
-  // candidates of this segment inside its first and last chunk (other segments may share them)
-  if (threadIdx.x == 0)
-    s_a0 = S.o > S.c0 * kTile ? lower_bound_u32(ws.cand_idx + (size_t)S.c0 * kTile, ws.counts[S.c0], S.o) : 0u;
-  if (threadIdx.x == 1)
-    s_b1 = e_ < min((uint32_t)T.d, (c1 + 1) * kTile)
-               ? lower_bound_u32(ws.cand_idx + (size_t)c1 * kTile, ws.counts[c1], e_)
-               : ws.counts[c1];
+  __shared__ uint32_t lds[2 * kSelNT / 64];
+  const int l = blockIdx.x;
+  uint32_t* R = res_of(ws, l);
+  if (R[R_MODE] != 0) return;
+  const uint32_t* gh = ws.hist + (size_t)l * kHCopies * kHBins;
+  for (int b = threadIdx.x; b < kHBins; b += kSelNT) {
+    uint32_t c[kHCopies];
+#pragma unroll
+    for (int x = 0; x < kHCopies; ++x) c[x] = gh[x * kHBins + b];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int x = 0; x < kHCopies; ++x) sum += c[x];
+    hist[b] = sum;
+  }
   __syncthreads();
-  S.a0 = s_a0;
-  S.b1 = s_b1;
-  S.N = 0;
-  EFS_PHASE(1);
-  if (S.nc <= kCofsLds)
-    select_emit_body<KIND, true>(T, ws, S, s_crow, s_coff, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds,
-                                 s_keys, s_wtot);
-  else
-    select_emit_body<KIND, false>(T, ws, S, ws.cofs + 2 * (size_t)T.seg_cbase[S.l], ws.cofs + 2 * (size_t)T.seg_cbase[S.l] + S.nc,
-                                  data, e_zero, out_idx, out_val, s0, s1, step, hist, lds, s_keys, s_wtot);
+  const uint32_t kl = (uint32_t)T.seg_k[l];
+  uint32_t above;
+  const int bin = block_resolve<kSelNT>(hist, kHBins, kl, lds, above);
+  if (threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
+  if (threadIdx.x == 0) {
+    if (bin < 0) {
+      R[R_SLOW] = 1;
+      atomicOr(ws.diag, kDiagSlowPath);
+    } else {
+      R[R_B] = (uint32_t)bin;
+      R[R_NEED] = kl - above;
+    }
+  }
+}
+
+// Per row: candidates certain to win are counted; the undecided ones go to the segment's list (in
+// any order: the selection over the list does not depend on it; row r appends to sub-list
+// r % kSubLists, which spreads the atomics on the list counters).  Top-k: above / inside bin B of
+// a histogrammed segment.  Random-k: Philox key below ulo_l / in [ulo_l, tau_l).
+template <int KIND>
+__global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws) {
+  __shared__ uint32_t lds[kNT / 64];
+  __shared__ uint32_t s_base;
+  const uint32_t row = blockIdx.x;
+  const int l = T.row_seg[row];
+  uint32_t* R = res_of(ws, l);
+  uint32_t A = 0, sh = 0, B = 0, ulo = 0;
+  if constexpr (KIND == 0) {
+    if (R[R_SLOW] || R[R_MODE]) return;
+    A = R[R_A];
+    sh = R[R_SH];
+    B = R[R_B];
+  } else {
+    ulo = T.seg_ulo[l];
+  }
+  // class: 2 = certain winner, 1 = undecided (listed), 0 = loses
+  auto cls = [&](uint32_t k) -> uint32_t {
+    if constexpr (KIND == 0) {
+      const uint32_t b = cand_bin(k, A, sh);
+      return b > B ? 2u : (b == B ? 1u : 0u);
+    } else {
+      return ~k < ulo ? 2u : 1u;
+    }
+  };
+  const uint32_t cnt = ws.counts[row];
+  const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
+  uint32_t na = 0, ne = 0;
+  for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
+    const uint32_t c = cls(ck[j]);
+    na += c == 2u ? 1u : 0u;
+    ne += c == 1u ? 1u : 0u;
+  }
+  uint32_t tot;
+  const uint32_t ex = block_excl_scan<kNT>(na | (ne << 16), lds, tot);  // row totals <= kTile
+  const uint32_t tot_e = tot >> 16;
+  const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
+  if (threadIdx.x == 0) {
+    ws.rcnt[row] = tot & 0xFFFFu;
+    s_base = tot_e ? atomicAdd(lcnt_of(ws, l, c), tot_e) : 0u;
+  }
+  __syncthreads();
+  if (tot_e == 0) return;
+  const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
+  uint32_t t = s_base + (ex >> 16);
+  for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
+    const uint32_t k = ck[j];
+    if (cls(k) == 1u) {
+      const size_t p = sublist_pos(r0, c, t);
+      ws.list_key[p] = k;
+      ws.list_idx[p] = ci[j];
+      ++t;
+    }
+  }
+}
+
+// The need-th best (key' descending, then index ascending; 1 <= need <= m <= kRankList) of m
+// entries held in LDS, by counting for every entry the entries that beat it: four threads share an
+// entry, each comparing against every fourth entry.  Gives its key' and one past its index.
+__device__ __forceinline__ void rank_select(const uint32_t* sk, const uint32_t* si, uint32_t m, uint32_t need,
+                                            uint32_t& T_out, uint32_t& IT_out) {
+  __shared__ uint32_t s_t, s_it;
+  const uint32_t e = threadIdx.x >> 2, part = threadIdx.x & 3u;
+  uint32_t rank = 0, k = 0, i = 0;
+  if (e < m) {
+    k = sk[e];
+    i = si[e];
+    for (uint32_t j0 = part; j0 < m; j0 += 16u) {
+      uint32_t kj[4], ij[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t j = j0 + 4u * (uint32_t)u;
+        kj[u] = j < m ? sk[j] : 0u;
+        ij[u] = j < m ? si[j] : 0xFFFFFFFFu;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        rank += (j0 + 4u * (uint32_t)u < m && (kj[u] > k || (kj[u] == k && ij[u] < i))) ? 1u : 0u;
+    }
+  }
+  rank += __shfl_xor(rank, 1, 64);
+  rank += __shfl_xor(rank, 2, 64);
+  if (e < m && part == 0 && rank == need - 1) {
+    s_t = k;
+    s_it = i + 1u;
+  }
+  __syncthreads();
+  T_out = s_t;
+  IT_out = s_it;
+  __syncthreads();
+}
+
+// The need best of the m listed candidates (key' descending, then index ascending; 1 <= need <=
+// m): the key' T of the last winner and one past its index (every listed winner is key' > T, or
+// key' == T with index below that bound).  Radix levels of 11 bits narrow the key' range until
+// the bin holding the need-th best has at most kRankList entries; those are gathered and ranked.
+template <typename K>
+__device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint32_t m, uint32_t need,
+                                               uint32_t* hist, uint32_t* lds, uint32_t* gk, uint32_t* gi,
+                                               uint32_t& T_out, uint32_t& IT_out) {
+  __shared__ uint32_t s_n;
+  if (m <= kRankList) {
+    for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
+      gk[j] = key[j];
+      gi[j] = idx[j];
+    }
+    __syncthreads();
+    rank_select(gk, gi, m, need, T_out, IT_out);
+    return;
+  }
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+  for_keys(key, m, [&](uint32_t, uint32_t k) {
+    kand &= k;
+    kor |= k;
+  });
+  block_and_or(kand, kor, lds);
+  const uint32_t diff = kand ^ kor;
+  uint32_t prefix = kand, known = 32;  // all keys equal: nothing to resolve
+  uint32_t cnt = m;
+  if (diff) {
+    const int h = 31 - __clz(diff);
+    prefix = h == 31 ? 0u : (kand & (0xFFFFFFFFu << (h + 1)));
+    known = (uint32_t)(31 - h);
+    while (known < 32 && cnt > kRankList) {
+      const int w = min(11, 32 - (int)known);
+      const int shift = 32 - (int)known - w;
+      for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
+      __syncthreads();
+      const uint32_t pmask = known == 0 ? 0u : (0xFFFFFFFFu << (32 - known));
+      const uint32_t want = prefix & pmask;
+      for_keys(key, m, [&](uint32_t, uint32_t k) {
+        if ((k & pmask) == want) atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u);
+      });
+      __syncthreads();
+      uint32_t above;
+      const int bin = block_resolve<kSelNT>(hist, 1 << w, need, lds, above);
+      cnt = hist[max(bin, 0)];
+      __syncthreads();
+      prefix |= (uint32_t)max(bin, 0) << shift;
+      need -= above;
+      known += (uint32_t)w;
+    }
+  }
+  if (cnt <= kRankList) {  // gather the entries sharing the resolved prefix and rank them
+    const uint32_t pmask = known == 0 ? 0u : (known >= 32 ? 0xFFFFFFFFu : (0xFFFFFFFFu << (32 - known)));
+    const uint32_t want = prefix & pmask;
+    if (threadIdx.x == 0) s_n = 0;
+    __syncthreads();
+    for_keys(key, m, [&](uint32_t f, uint32_t k) {
+      if ((k & pmask) == want) {
+        const uint32_t p = atomicAdd(&s_n, 1u);
+        gk[p] = k;
+        gi[p] = idx[f];
+      }
+    });
+    __syncthreads();
+    rank_select(gk, gi, cnt, need, T_out, IT_out);
+    return;
+  }
+  // more than kRankList entries share the full key': ties ordered by index
+  T_out = prefix;
+  IT_out = need >= cnt ? 0xFFFFFFFFu : block_nth_smallest_tie(key, idx, m, prefix, need, hist, lds) + 1u;
+}
+
+// Per segment: the exact threshold among the listed candidates, then every row's message offset;
+// or the exact whole-segment path when the candidates cannot hold the answer.  Independent loads
+// are issued together (record, sub-list sizes, the rows' counts) to keep the chain of dependent
+// memory round trips short.
+template <int KIND>
+__global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const float* data, float* e_zero,
+                                                   uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1,
+                                                   uint32_t step) {
+  constexpr uint32_t kPer = 8;  // rows per thread held in registers (more are re-read)
+  __shared__ uint32_t hist[kHBins];
+  __shared__ uint32_t lds[2 * kSelNT / 64];
+  __shared__ uint32_t s_key[kListLds];
+  __shared__ uint32_t s_idx[kListLds];
+  __shared__ uint32_t s_add[kRowsLds];
+  __shared__ uint32_t s_gk[kRankList];
+  __shared__ uint32_t s_gi[kRankList];
+  const int l = blockIdx.x;
+  uint32_t* R = res_of(ws, l);
+  const uint32_t r0 = (uint32_t)T.seg_cbase[l], nr = (uint32_t)T.seg_cbase[l + 1] - r0;
+  const uint32_t kl = (uint32_t)T.seg_k[l];
+  const uint32_t per = (nr + kSelNT - 1) / kSelNT;
+  const uint32_t a = min(nr, threadIdx.x * per), b = min(nr, a + per);
+  const uint32_t* rc = ws.rcnt + r0;
+  const uint32_t* cc = ws.counts + r0;
+  // round trip 1: record, sub-list sizes, row counts
+  bool slow = false, listed = true;
+  uint32_t need = 0;
+  if constexpr (KIND == 0) {
+    slow = R[R_SLOW] != 0;
+    listed = R[R_MODE] == 0;
+    need = R[R_NEED];
+  }
+  uint32_t lc[kSubLists];
+#pragma unroll
+  for (int c = 0; c < kSubLists; ++c) lc[c] = *lcnt_of(ws, l, (uint32_t)c);
+  uint32_t cr[kPer], cn[kPer];
+#pragma unroll
+  for (uint32_t x = 0; x < kPer; ++x) {
+    cr[x] = a + x < b ? rc[a + x] : 0u;
+    cn[x] = a + x < b ? cc[a + x] : 0u;
+  }
+  if constexpr (KIND == 1) {
+    // random-k: the certain winners S (keys below ulo) and the candidates N decide whether the
+    // window [ulo, tau) holds the k_l-th smallest key
+    uint32_t sS = 0, sN = 0;
+#pragma unroll
+    for (uint32_t x = 0; x < kPer; ++x) {
+      sS += cr[x];
+      sN += cn[x];
+    }
+    for (uint32_t x = a + kPer; x < b; ++x) {
+      sS += rc[x];
+      sN += cc[x];
+    }
+    uint32_t S, N;
+    (void)block_excl_scan<kSelNT>(sS, lds, S);
+    (void)block_excl_scan<kSelNT>(sN, lds, N);
+    slow = S > kl || N < kl;
+    need = kl - S;
+    if (threadIdx.x == 0) {
+      R[R_SLOW] = slow ? 1u : 0u;
+      if (slow) atomicOr(ws.diag, kDiagSlowPath);
+    }
+  }
+  if (slow) {
+    slow_select<KIND>(T, l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
+    return;
+  }
+  const bool rows_lds = nr <= kRowsLds;
+  if (listed) {
+    const uint32_t o = (uint32_t)T.seg_off[l];
+    SubLists lk, li;
+    lk.arr = ws.list_key;
+    li.arr = ws.list_idx;
+    lk.r0 = li.r0 = r0;
+    uint32_t m = 0;
+#pragma unroll
+    for (int c = 0; c < kSubLists; ++c) {
+      lk.M[c] = li.M[c] = m;
+      m += lc[c];
+    }
+    lk.M[kSubLists] = li.M[kSubLists] = m;
+    const bool in_lds = m <= kListLds;
+    // round trip 2: the listed candidates
+    if (in_lds) {
+      for (uint32_t f0 = 0; f0 < m; f0 += (uint32_t)kSelNT * 4u) {
+        uint32_t kx[4], ix[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t f = f0 + (uint32_t)u * kSelNT + threadIdx.x;
+          kx[u] = f < m ? lk[f] : 0u;
+          ix[u] = f < m ? li[f] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t f = f0 + (uint32_t)u * kSelNT + threadIdx.x;
+          if (f < m) {
+            s_key[f] = kx[u];
+            s_idx[f] = ix[u];
+          }
+        }
+      }
+    }
+    if (rows_lds)
+      for (uint32_t x = threadIdx.x; x < nr; x += kSelNT) s_add[x] = 0;
+    __syncthreads();
+    // need == 0 (random-k only): the certain winners, keys below ulo, are all the winners
+    uint32_t Tk = KIND == 1 ? ~T.seg_ulo[l] : 0u, IT = 0;
+    if (need > 0) {
+      if (in_lds) list_threshold(s_key, s_idx, m, need, hist, lds, s_gk, s_gi, Tk, IT);
+      else list_threshold(lk, li, m, need, hist, lds, s_gk, s_gi, Tk, IT);
+      // the list's winners join their rows' counts
+      const uint32_t c0 = o / kTile;
+      for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
+        const uint32_t k = in_lds ? s_key[j] : lk[j];
+        const uint32_t i = in_lds ? s_idx[j] : li[j];
+        if (k > Tk || (k == Tk && i < IT)) {
+          if (rows_lds) atomicAdd(&s_add[i / kTile - c0], 1u);
+          else atomicAdd(&ws.rcnt[r0 + (i / kTile - c0)], 1u);
+        }
+      }
+    }
+    if (threadIdx.x == 0) {
+      R[R_T] = Tk;
+      R[R_IT] = IT;
+    }
+    if (!rows_lds) {
+      // the additions went to global memory: order them before re-reading the counts
+      __threadfence();
+      __syncthreads();
+#pragma unroll
+      for (uint32_t x = 0; x < kPer; ++x) cr[x] = a + x < b ? rc[a + x] : 0u;
+    }
+    __syncthreads();
+  }
+  // row offsets: exclusive scan of the rows' winner counts (mode 1: every candidate wins)
+  const uint32_t* cnt = listed ? rc : cc;
+  const bool add = listed && rows_lds;
+  uint32_t w[kPer], sum = 0;
+#pragma unroll
+  for (uint32_t x = 0; x < kPer; ++x) {
+    w[x] = (listed ? cr[x] : cn[x]) + (add && a + x < b ? s_add[a + x] : 0u);
+    sum += w[x];
+  }
+  for (uint32_t x = a + kPer; x < b; ++x) sum += cnt[x] + (add ? s_add[x] : 0u);
+  uint32_t tot;
+  const uint32_t ex = block_excl_scan<kSelNT>(sum, lds, tot);
+  uint32_t run = (uint32_t)T.seg_P[l] + ex;
+  uint32_t* roff = ws.roff + r0;
+#pragma unroll
+  for (uint32_t x = 0; x < kPer; ++x) {
+    if (a + x < b) roff[a + x] = run;
+    run += w[x];
+  }
+  for (uint32_t x = a + kPer; x < b; ++x) {
+    roff[x] = run;
+    run += cnt[x] + (add ? s_add[x] : 0u);
+  }
+  if (threadIdx.x == 0 && tot != kl) atomicOr(ws.diag, kDiagCount);
+}
+
+// Per row: the winners, in index order, to the message at the row's offset; e = +0 there.
+__global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws, float* e_zero, uint32_t* out_idx, float* out_val) {
+  __shared__ uint32_t s_wt[kNT / 64];
+  const uint32_t row = blockIdx.x;
+  const int l = T.row_seg[row];
+  const uint32_t* R = res_of(ws, l);
+  if (R[R_SLOW]) return;
+  const uint32_t Tk = R[R_T], IT = R[R_IT];
+  const uint32_t cnt = ws.counts[row], pend = (uint32_t)T.seg_P[l + 1];
+  uint32_t base = ws.roff[row];
+  const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
+  const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
+  const float* cv = ws.cand_val + (size_t)row * kTile;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (uint32_t j0 = 0; j0 < cnt; j0 += kNT) {
+    const uint32_t j = j0 + threadIdx.x;
+    const bool in = j < cnt;
+    uint32_t k = 0, i = 0;
+    float v = 0.0f;
+    if (in) {
+      k = ck[j];
+      i = ci[j];
+      v = cv[j];
+    }
+    const bool win = in && (k > Tk || (k == Tk && i < IT));
+    const uint64_t bw = __ballot(win);
+    if (lane == 0) s_wt[wid] = (uint32_t)__popcll(bw);
+    __syncthreads();
+    uint32_t wo = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) {
+      const uint32_t x = s_wt[w];
+      wo += w < wid ? x : 0u;
+      tot += x;
+    }
+    __syncthreads();
+    const uint32_t pos = base + wo + lanes_below(bw);
+    if (win && pos < pend) {
+      out_idx[pos] = i;
+      out_val[pos] = v;
+      if (e_zero) e_zero[i] = 0.0f;
+    }
+    base += tot;
+  }
 }
 
 }  // namespace efs

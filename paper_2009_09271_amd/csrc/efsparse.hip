@@ -36,8 +36,8 @@ struct Blob {
 };
 
 struct WsLayout {
-  size_t diag = 0, res = 0, counts = 0, cofs = 0, cand_idx = 0, cand_val = 0, cand_key = 0, dense_idx = 0,
-         dense_val = 0, dense_key = 0, total = 0;
+  size_t diag = 0, res = 0, hist = 0, samp = 0, counts = 0, rcnt = 0, roff = 0, lcnt = 0, cand_idx = 0, cand_val = 0,
+         cand_key = 0, list_idx = 0, list_key = 0, total = 0;
 };
 
 }  // namespace
@@ -50,13 +50,15 @@ struct ef_layout {
   std::vector<int64_t> off64;
   double rk_sigma = 10.0, rk_extra = 64.0, tk_sigma = 6.0, tk_extra = 8.0;
 
-  std::vector<int32_t> off, k, P, bl, nb, srank, cbase, csf, csl;
+  std::vector<int32_t> off, k, P, bl, nb, srank, cbase, ro, csf, csl, rseg;
   std::vector<uint64_t> tau;
+  std::vector<uint32_t> ulo;
   int64_t K = 0;
-  int32_t nchunks = 0, ncrows = 0;
+  int32_t nchunks = 0, nrows = 0, nruns = 0;
+  bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
 
   Blob blob;
-  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_cbase, o_tau, o_csf, o_csl;
+  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
   Tables T{};
   bool bound = false;
 
@@ -74,7 +76,10 @@ void ef_layout::build() {
   nb.resize(n);
   srank.resize(n);
   tau.resize(n);
+  ulo.resize(n);
   cbase.assign(n + 1, 0);
+  ro.assign(n + 1, 0);
+  all_exact = true;
   for (int l = 0; l < n; ++l) {
     const int64_t dl = off64[l + 1] - off64[l];
     // k per segment: round-half-up of density * d_l in double, clamped to [1, d_l]
@@ -97,12 +102,28 @@ void ef_layout::build() {
     if (p >= 1.0) t = 1ull << 32;
     else t = (uint64_t)std::ceil(std::max(p, 0.0) * 4294967296.0);
     tau[l] = std::min<uint64_t>(std::max<uint64_t>(t, 1), 1ull << 32);
-    // per-segment scratch rows: one per data chunk the segment touches
+    // keys below ulo are expected k - sigma * sqrt(k) - extra times: all winners unless more than k
+    const double mlo = (double)kl - rk_sigma * std::sqrt((double)kl) - rk_extra;
+    const double plo = mlo / (double)dl;
+    uint64_t u = 0;
+    if (plo >= 1.0) u = tau[l];
+    else if (plo > 0.0) u = (uint64_t)std::floor(plo * 4294967296.0);
+    u = std::min<uint64_t>(u, tau[l]);
+    ulo[l] = (uint32_t)std::min<uint64_t>(u, 0xFFFFFFFFull);
+    // rows: one per data tile the segment touches
     const int64_t c0 = off64[l] / kTile, c1 = (off64[l + 1] - 1) / kTile;
     cbase[l + 1] = cbase[l] + (int32_t)(c1 - c0 + 1);
+    // top-k sample runs: the whole segment when it fits the sample, else kSampleMax / kSampleRun
+    const int64_t runs = dl <= kSampleMax ? (dl + kSampleRun - 1) / kSampleRun : kSampleMax / kSampleRun;
+    ro[l + 1] = ro[l] + (int32_t)runs;
+    if (dl > kSampleMax) all_exact = false;
   }
   K = P[n];
-  ncrows = cbase[n];
+  nrows = cbase[n];
+  nruns = ro[n];
+  rseg.resize(nrows);
+  for (int l = 0; l < n; ++l)
+    for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) rseg[r] = l;
   nchunks = (int32_t)((d + kTile - 1) / kTile);
   csf.assign(nchunks, 0);
   csl.assign(nchunks, 0);
@@ -124,36 +145,37 @@ void ef_layout::build() {
   o_nb = blob.add(nb);
   o_srank = blob.add(srank);
   o_cbase = blob.add(cbase);
+  o_ro = blob.add(ro);
   o_tau = blob.add(tau);
+  o_ulo = blob.add(ulo);
   o_csf = blob.add(csf);
   o_csl = blob.add(csl);
+  o_rseg = blob.add(rseg);
   bound = false;
 }
 
 WsLayout ef_layout::ws_layout(int op) const {
-  (void)op;
   WsLayout w;
   size_t at = 0;
-  w.diag = at;
-  at = 16;
-  w.res = at;
-  at = align_up(at + (size_t)L * kResWords * 4, 16);
-  w.counts = at;
-  at = align_up(at + (size_t)nchunks * 4, 16);
-  w.cofs = at;
-  at = align_up(at + (size_t)ncrows * 8, kAlign);
-  w.cand_idx = at;
-  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
-  w.cand_val = at;
-  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
-  w.cand_key = at;
-  at = align_up(at + (size_t)nchunks * kTile * 4, kAlign);
-  w.dense_idx = at;
-  at = align_up(at + (size_t)d * 4, kAlign);
-  w.dense_val = at;
-  at = align_up(at + (size_t)d * 4, kAlign);
-  w.dense_key = at;
-  at = align_up(at + (size_t)d * 4, kAlign);
+  auto take = [&](size_t bytes) {
+    const size_t a = at;
+    at = align_up(at + bytes, kAlign);
+    return a;
+  };
+  const size_t rows = (size_t)nrows, slots = rows * kTile;
+  w.diag = take(16);
+  w.res = take((size_t)L * kResWords * 4);
+  w.hist = take((size_t)L * kHCopies * kHBins * 4);
+  w.samp = op == EF_OP_TOPK ? take((size_t)nruns * kSampleRun * 4) : 0;
+  w.counts = take(rows * 4);
+  w.rcnt = take(rows * 4);
+  w.roff = take(rows * 4);
+  w.lcnt = take((size_t)L * kSubLists * kLineWords * 4);
+  w.cand_idx = take(slots * 4);
+  w.cand_val = take(slots * 4);
+  w.cand_key = take(slots * 4);
+  w.list_idx = take(slots * 4);
+  w.list_key = take(slots * 4);
   w.total = at;
   return w;
 }
@@ -165,14 +187,17 @@ WSel make_ws(const WsLayout& l, void* base) {
   WSel w;
   w.diag = reinterpret_cast<uint32_t*>(b + l.diag);
   w.res = reinterpret_cast<uint32_t*>(b + l.res);
+  w.hist = reinterpret_cast<uint32_t*>(b + l.hist);
+  w.samp = reinterpret_cast<uint32_t*>(b + l.samp);
   w.counts = reinterpret_cast<uint32_t*>(b + l.counts);
-  w.cofs = reinterpret_cast<uint32_t*>(b + l.cofs);
+  w.rcnt = reinterpret_cast<uint32_t*>(b + l.rcnt);
+  w.roff = reinterpret_cast<uint32_t*>(b + l.roff);
+  w.lcnt = reinterpret_cast<uint32_t*>(b + l.lcnt);
   w.cand_idx = reinterpret_cast<uint32_t*>(b + l.cand_idx);
   w.cand_val = reinterpret_cast<float*>(b + l.cand_val);
   w.cand_key = reinterpret_cast<uint32_t*>(b + l.cand_key);
-  w.dense_idx = reinterpret_cast<uint32_t*>(b + l.dense_idx);
-  w.dense_val = reinterpret_cast<float*>(b + l.dense_val);
-  w.dense_key = reinterpret_cast<uint32_t*>(b + l.dense_key);
+  w.list_idx = reinterpret_cast<uint32_t*>(b + l.list_idx);
+  w.list_key = reinterpret_cast<uint32_t*>(b + l.list_key);
   return w;
 }
 
@@ -266,7 +291,8 @@ int check_ws(const ef_layout* L, int op, void* ws, size_t ws_bytes, WsLayout& wl
   return EF_OK;
 }
 
-// Top-k: sampled candidate threshold, fused accumulate + candidates, exact selection, emission.
+// Top-k: sample -> candidate rule -> fused accumulate + candidates -> bin of the k-th ->
+// collect -> exact threshold and row offsets -> emission.
 int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint32_t* idx,
              float* val, void* ws, size_t ws_bytes, void* stream) {
   WsLayout wl;
@@ -274,29 +300,45 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
   hipStream_t st = S(stream);
   WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
+  const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
+  const dim3 pgrid((unsigned)L->nruns), pblk(kSampleRun);
   if (g) {
     if (g_dtype == EF_F32) {
-      EF_LAUNCH((k_topk_sample<0, true>), sgrid, sblk, 0, st, T, g, src, w);
+      EF_LAUNCH((k_sample_gather<0, true>), pgrid, pblk, 0, st, T, g, src, w);
       EF_TRY(launched());
-      EF_LAUNCH((k_stream_sel<0, 0, true>), grid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+      EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
+      EF_TRY(launched());
+      EF_LAUNCH((k_stream_sel<0, 0, true>), rgrid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
     } else {
-      EF_LAUNCH((k_topk_sample<1, true>), sgrid, sblk, 0, st, T, g, src, w);
+      EF_LAUNCH((k_sample_gather<1, true>), pgrid, pblk, 0, st, T, g, src, w);
       EF_TRY(launched());
-      EF_LAUNCH((k_stream_sel<0, 1, true>), grid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+      EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
+      EF_TRY(launched());
+      EF_LAUNCH((k_stream_sel<0, 1, true>), rgrid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
     }
   } else {
-    EF_LAUNCH((k_topk_sample<0, false>), sgrid, sblk, 0, st, T, nullptr, src, w);
+    EF_LAUNCH((k_sample_gather<0, false>), pgrid, pblk, 0, st, T, nullptr, src, w);
     EF_TRY(launched());
-    EF_LAUNCH((k_stream_sel<0, 0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
+    EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
+    EF_TRY(launched());
+    EF_LAUNCH((k_stream_sel<0, 0, false>), rgrid, blk, 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
   }
   EF_TRY(launched());
+  if (!L->all_exact) {
+    EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w);
+    EF_TRY(launched());
+    EF_LAUNCH(k_collect<0>, rgrid, blk, 0, st, T, w);
+    EF_TRY(launched());
+  }
   const float* acc = g ? e_fused : src;
-  EF_LAUNCH(k_select_emit<0>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
+  EF_LAUNCH(k_select<0>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
+  EF_TRY(launched());
+  EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();
 }
 
-// Random-k: fused accumulate + Philox candidates, exact selection, emission.
+// Random-k: fused accumulate + Philox candidates -> collect (certain winners counted, the window
+// [ulo, tau) listed) -> exact threshold and row offsets -> emission.
 int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint64_t seed,
               uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream) {
   WsLayout wl;
@@ -304,19 +346,23 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
   hipStream_t st = S(stream);
   WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
+  const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g) {
     if (g_dtype == EF_F32)
-      EF_LAUNCH((k_stream_sel<1, 0, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
+      EF_LAUNCH((k_stream_sel<1, 0, true>), rgrid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
     else
-      EF_LAUNCH((k_stream_sel<1, 1, true>), grid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
+      EF_LAUNCH((k_stream_sel<1, 1, true>), rgrid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
   } else {
-    EF_LAUNCH((k_stream_sel<1, 0, false>), grid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
+    EF_LAUNCH((k_stream_sel<1, 0, false>), rgrid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
   }
   EF_TRY(launched());
+  EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
+  EF_TRY(launched());
   const float* acc = g ? e_fused : src;
-  EF_LAUNCH(k_select_emit<1>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
+  EF_LAUNCH(k_select<1>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
+  EF_TRY(launched());
+  EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();
 }
 
@@ -464,13 +510,17 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_nb = reinterpret_cast<const int32_t*>(b + L->o_nb);
   T.seg_srank = reinterpret_cast<const int32_t*>(b + L->o_srank);
   T.seg_cbase = reinterpret_cast<const int32_t*>(b + L->o_cbase);
+  T.seg_ro = reinterpret_cast<const int32_t*>(b + L->o_ro);
+  T.row_seg = reinterpret_cast<const int32_t*>(b + L->o_rseg);
   T.seg_tau = reinterpret_cast<const uint64_t*>(b + L->o_tau);
+  T.seg_ulo = reinterpret_cast<const uint32_t*>(b + L->o_ulo);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
   T.chunk_sl = reinterpret_cast<const int32_t*>(b + L->o_csl);
   T.d = (int32_t)L->d;
   T.L = L->L;
   T.nchunks = L->nchunks;
-  T.ncrows = L->ncrows;
+  T.nrows = L->nrows;
+  T.nruns = L->nruns;
   L->bound = true;
   return EF_OK;
 }

@@ -43,6 +43,7 @@ def _run_steps(c, kind, g_list, e, seed=0, composed=True):
         assert_msg_equal(kind, (m, val), (wm, wval), f"{kind} step {step}")
         assert_f32_equal(ed, we, f"{kind} e' step {step}")
         diag = c.L.diag(ws, c.E.EF_OP_TOPK if kind == "topk" else c.E.EF_OP_RANDK)
+        assert not diag & c.E.DIAG_COUNT_MISMATCH, f"{kind} row counts inconsistent at step {step}"
         if composed:
             ed2 = dev(e)
             m2, val2 = c.step_composed(kind, g, ed2, seed, step)
@@ -159,3 +160,37 @@ def test_topk_flat_layered_scales():
     g = np.concatenate([rng.laplace(0, s, n) for n, s in zip(sizes, scales)]).astype(np.float32)
     c = Case([0, len(g)], 0.001)
     _run_steps(c, "topk", [g, g * 0.5], np.zeros(len(g), np.float32))
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_workspace_reused_with_stale_contents(kind):
+    """One workspace, filled with stale bytes, serves several calls (and the other selection op):
+    nothing may depend on its previous contents."""
+    import torch
+    announce(kind, "stale workspace")
+    offs = [0, 3, 40000, 40001, 90001, 200000]
+    c = Case(offs, 0.01)
+    n = max(c.L.workspace_bytes(c.E.EF_OP_TOPK), c.L.workspace_bytes(c.E.EF_OP_RANDK))
+    ws = torch.full((n,), 0xA5, dtype=torch.uint8, device="cuda")
+    g, e = _inputs(c.d, 31)
+    for step in range(3):
+        ed = dev(e)
+        other = "randk" if kind == "topk" else "topk"
+        c.step(other, g, dev(e), 5, step, ws=ws)  # leaves its own state behind
+        m, val, _ = c.step(kind, g, ed, 5, step, ws=ws)
+        (wm, wval), we = c.oracle_step(kind, g, e, 5, step)
+        assert_msg_equal(kind, (m, val), (wm, wval), f"{kind} step {step}")
+        assert_f32_equal(ed, we, f"{kind} e' step {step}")
+        e = we
+        g = g * np.float32(0.5)
+
+
+def test_topk_concentrated_magnitudes():
+    """A sampled segment whose keys all share their top 11 bits: the candidate threshold is refined
+    inside that bin (otherwise every element would become a candidate)."""
+    announce("topk concentrated")
+    rng = np.random.default_rng(23)
+    d = 200000
+    g = ((1.0 + 0.1 * rng.random(d)) * rng.choice([-1.0, 1.0], d)).astype(np.float32)
+    c = Case([0, d], 0.01)
+    _run_steps(c, "topk", [g, g], np.zeros(d, np.float32))
