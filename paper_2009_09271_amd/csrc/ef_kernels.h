@@ -259,8 +259,12 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 // Aggregate (Algorithm 1): out = (sum over workers in order, from +0) / W.  One workgroup per
 // output tile of kTile elements accumulates in LDS; a barrier separates consecutive workers.
 // ---------------------------------------------------------------------------------------------
-// tile_start[w][tau] = first entry of message w whose index lies in tile >= tau (tau = 0..nt).
-// Grid: (ceil(K / kNT), W).
+// Output tiles of the sparse aggregate: kAggTile elements, kAggRounds float4 groups per thread.
+constexpr uint32_t kAggTile = 4096;
+constexpr int kAggRounds = (int)kAggTile / (4 * kNT);
+
+// tile_start[w][tau] = first entry of message w whose index lies in an aggregate tile >= tau
+// (tau = 0..nt).  Grid: (ceil(K / kNT), W).
 __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
                                                     uint32_t* tile_start) {
   const uint32_t j = blockIdx.x * kNT + threadIdx.x;
@@ -268,7 +272,7 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
   if (j >= (uint32_t)K) return;
   const uint32_t* m = idx + (size_t)w * K;
   uint32_t* ts = tile_start + (size_t)w * (nt + 1);
-  auto tile = [&](uint32_t i) -> int { return i < (uint32_t)d ? (int)(i / kTile) : nt; };
+  auto tile = [&](uint32_t i) -> int { return i < (uint32_t)d ? (int)(i / kAggTile) : nt; };
   const int tj = tile(m[j]);
   const int tp = j == 0 ? -1 : tile(m[j - 1]);
   for (int tau = tp + 1; tau <= tj; ++tau) ts[tau] = j;
@@ -276,68 +280,225 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
     for (int tau = tj + 1; tau <= nt; ++tau) ts[tau] = (uint32_t)K;
 }
 
-__device__ __forceinline__ void agg_write(float* out, uint32_t lo, uint32_t hi, const float* acc,
-                                          int average, float fW) {
+constexpr int kAggW = 64;           // workers whose tile ranges are held in LDS at once
+constexpr int kAggStage = 512;      // message entries staged in LDS per pass (2 per thread)
+constexpr int kAggStarts = 1024;    // block starts (workers x segments of the tile) held in LDS
+
+// Worker w of the group (0 <= w < nw) whose staged entries [pre[w], pre[w + 1]) contain f.
+__device__ __forceinline__ int agg_worker_of(const uint32_t* pre, int nw, uint32_t f) {
+  int a = 0, b = nw - 1;
+  while (a < b) {
+    const int mid = (a + b + 1) >> 1;
+    if (pre[mid] <= f) a = mid; else b = mid - 1;
+  }
+  return a;
+}
+
+// One workgroup per output tile of kAggTile elements, summed in an LDS tile.  Per group of up to
+// kAggW workers: the tile's entry range of every worker in one round trip, then passes of up to
+// kAggStage entries staged in LDS in worker order (loads in flight together).  Within a pass an
+// LDS bitmap finds the positions hit more than once: the others take their value at once (no
+// ordering question), the shared ones are summed in worker order, either by the first entry of
+// each shared position walking the pass's shared entries (few of them) or worker by worker with
+// a barrier after each (many).  Passes, and groups, follow each other in worker order.
+constexpr int kAggScanMax = 64;
+
+__global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
+                                                    const uint32_t* idx, const float* val,
+                                                    const uint32_t* tile_start, int average, float* out) {
+  constexpr int kU = kAggStage / kNT;  // staged entries per thread and pass (2)
+  static_assert(kU == 2, "the shared-entry compaction packs two 16-bit counts");
+  __shared__ float acc[kAggTile];
+  __shared__ uint32_t s_pre[kAggW + 1];
+  __shared__ uint32_t s_a[kAggW];
+  __shared__ uint32_t s_i[kAggStage];
+  __shared__ float s_v[kAggStage];
+  __shared__ uint32_t s_cf[kAggStage];  // staged positions of the shared entries, ascending
+  __shared__ uint32_t s_seen[kAggTile / 32];
+  __shared__ uint32_t s_multi[kAggTile / 32];
+  __shared__ uint32_t lds[kNT / 64];
+  const uint32_t tau = blockIdx.x;
+  const uint32_t lo = tau * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
+  for (uint32_t x = threadIdx.x; x < kAggTile; x += kNT) acc[x] = 0.0f;
+  for (int w0 = 0; w0 < W; w0 += kAggW) {
+    const int nw = min(kAggW, W - w0);
+    uint32_t ra = 0, cnt = 0;
+    if ((int)threadIdx.x < nw) {
+      const uint32_t* ts = tile_start + (size_t)(w0 + threadIdx.x) * (nt + 1);
+      ra = min(ts[tau], (uint32_t)K);
+      const uint32_t rb = min(ts[tau + 1], (uint32_t)K);
+      cnt = rb > ra ? rb - ra : 0u;
+    }
+    uint32_t tot;
+    const uint32_t ex = block_excl_scan<kNT>(cnt, lds, tot);
+    if ((int)threadIdx.x < nw) {
+      s_pre[threadIdx.x] = ex;
+      s_a[threadIdx.x] = ra;
+    }
+    if (threadIdx.x == 0) s_pre[nw] = tot;
+    __syncthreads();
+    for (uint32_t f0 = 0; f0 < tot; f0 += kAggStage) {
+      const uint32_t f1 = min(tot, f0 + (uint32_t)kAggStage), n = f1 - f0;
+      uint32_t si[kU];
+      float sv[kU];
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
+      for (int u = 0; u < kU; ++u) {
+        const uint32_t f = f0 + (uint32_t)(u * kNT) + threadIdx.x;
+        si[u] = 0xFFFFFFFFu;
+        sv[u] = 0.0f;
+        if (f < f1) {
+          const int w = agg_worker_of(s_pre, nw, f);
+          const size_t j = (size_t)(w0 + w) * K + s_a[w] + (f - s_pre[w]);
+          si[u] = idx[j];
+          sv[u] = val[j];
+        }
+        if (si[u] < lo || si[u] >= hi) si[u] = 0xFFFFFFFFu;  // outside the tile: ignored
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        s_i[u * kNT + threadIdx.x] = si[u];
+        s_v[u * kNT + threadIdx.x] = sv[u];
+      }
+      for (uint32_t x = threadIdx.x; x < kAggTile / 32; x += kNT) {
+        s_seen[x] = 0;
+        s_multi[x] = 0;
+      }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        if (si[u] != 0xFFFFFFFFu) {
+          const uint32_t x = si[u] - lo, bit = 1u << (x & 31u);
+          if (atomicOr(&s_seen[x >> 5], bit) & bit) atomicOr(&s_multi[x >> 5], bit);
+        }
+      }
+      __syncthreads();
+      // single entries add at once; shared ones are compacted in staged order
+      uint32_t shared_u = 0;
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        if (si[u] != 0xFFFFFFFFu) {
+          const uint32_t x = si[u] - lo;
+          if ((s_multi[x >> 5] >> (x & 31u)) & 1u) shared_u |= 1u << u;
+          else acc[x] += sv[u];
+        }
+      }
+      uint32_t ctot;
+      const uint32_t cex = block_excl_scan<kNT>((shared_u & 1u) | ((shared_u >> 1) << 16), lds, ctot);
+      const uint32_t n0 = ctot & 0xFFFFu, cn = n0 + (ctot >> 16);
+      if (shared_u & 1u) s_cf[cex & 0xFFFFu] = threadIdx.x;
+      if (shared_u & 2u) s_cf[n0 + (cex >> 16)] = kNT + threadIdx.x;
+      __syncthreads();
+      if (cn > 0 && cn <= (uint32_t)kAggScanMax) {
+        if (threadIdx.x < cn) {
+          const uint32_t i = s_i[s_cf[threadIdx.x]];
+          bool first = true;
+          for (uint32_t e = 0; e < threadIdx.x; ++e) first = first && s_i[s_cf[e]] != i;
+          if (first) {
+            float sum = acc[i - lo];
+            for (uint32_t e = threadIdx.x; e < cn; ++e)
+              if (s_i[s_cf[e]] == i) sum += s_v[s_cf[e]];
+            acc[i - lo] = sum;
+          }
+        }
+      } else if (cn > 0) {
+        const int wa = agg_worker_of(s_pre, nw, f0), wb = agg_worker_of(s_pre, nw, f1 - 1);
+        for (int w = wa; w <= wb; ++w) {
+          const uint32_t ea = lower_bound_u32(s_cf, cn, max(s_pre[w], f0) - f0);
+          const uint32_t eb = lower_bound_u32(s_cf, cn, min(s_pre[w + 1], f1) - f0);
+          if (ea >= eb) continue;
+          for (uint32_t e = ea + threadIdx.x; e < eb; e += kNT) {
+            const uint32_t fe = s_cf[e];
+            acc[s_i[fe] - lo] += s_v[fe];
+          }
+          __syncthreads();
+        }
+      }
+      __syncthreads();  // staging buffers are rewritten by the next pass
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kAggRounds; ++r) {
     const uint32_t x = (uint32_t)(r * kNT + threadIdx.x) * 4u;
     const uint32_t i0 = lo + x;
     const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
     float v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(acc[x + q], fW) : acc[x + q];
+    for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(acc[x + q], (float)W) : acc[x + q];
     store4(out, i0, nv, v);
   }
 }
 
-__global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
-                                                    const uint32_t* idx, const float* val,
-                                                    const uint32_t* tile_start, int average, float* out) {
-  __shared__ float acc[kTile];
-  const uint32_t tau = blockIdx.x;
-  const uint32_t lo = tau * kTile, hi = min((uint32_t)d, lo + kTile);
-  for (uint32_t x = threadIdx.x; x < kTile; x += kNT) acc[x] = 0.0f;
-  __syncthreads();
-  for (int w = 0; w < W; ++w) {
-    const uint32_t* ts = tile_start + (size_t)w * (nt + 1);
-    const uint32_t a = min(ts[tau], (uint32_t)K), b = min(ts[tau + 1], (uint32_t)K);
-    const uint32_t* m = idx + (size_t)w * K;
-    const float* v = val + (size_t)w * K;
-    for (uint32_t j = a + threadIdx.x; j < b; j += kNT) {
-      const uint32_t i = m[j];
-      if (i >= lo && i < hi) acc[i - lo] += v[j];
-    }
-    __syncthreads();
-  }
-  agg_write(out, lo, hi, acc, average, (float)W);
-}
+// One workgroup per data tile, sums held in registers (each thread its kRounds float4 groups).
+// Per pass over up to kAggSegs segments of the tile and a group of workers, the segments' sizes
+// and the workers' block starts come in one round trip; then, for every worker in order and every
+// segment, the run pieces that meet the tile are added element by element (each element gets at
+// most one value per worker, and the segments of a tile are disjoint).
+constexpr int kAggSegs = 64;
 
 __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t K, const uint32_t* start,
                                                    const float* val, int average, float* out) {
-  __shared__ float acc[kTile];
+  __shared__ uint32_t s_st[kAggStarts];
+  __shared__ uint32_t s_seg[4][kAggSegs];  // o, n, k, P of the pass's segments
   const uint32_t c = blockIdx.x;
   const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
   const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-  for (uint32_t x = threadIdx.x; x < kTile; x += kNT) acc[x] = 0.0f;
-  __syncthreads();
-  for (int w = 0; w < W; ++w) {
-    const uint32_t* st = start + (size_t)w * T.L;
-    const float* v = val + (size_t)w * K;
-    for (int l = sf; l <= sl; ++l) {
-      const uint32_t o = T.seg_off[l], n = T.seg_off[l + 1] - o, k = T.seg_k[l], P = T.seg_P[l];
-      const uint32_t s = st[l] % n;
-      // run piece 1: local [s, min(s + k, n)), t = j - s;  piece 2: local [0, s + k - n), t = j + n - s
-      const uint32_t e1 = min(s + k, n);
-      const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + e1);
-      for (uint32_t i = a1 + threadIdx.x; i < b1; i += kNT) acc[i - lo] += v[P + (i - o - s)];
-      if (s + k > n) {
-        const uint32_t a2 = max(lo, o), b2 = min(hi, o + (s + k - n));
-        for (uint32_t i = a2 + threadIdx.x; i < b2; i += kNT) acc[i - lo] += v[P + (i - o + n - s)];
+  float a[kRounds][4];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
+  for (int l0 = sf; l0 <= sl; l0 += kAggSegs) {
+    const int ns = min(kAggSegs, sl - l0 + 1);
+    const int gw = kAggStarts / ns;  // workers per group
+    for (int w0 = 0; w0 < W; w0 += gw) {
+      const int nw = min(gw, W - w0);
+      if ((int)threadIdx.x < ns) {
+        const int l = l0 + threadIdx.x;
+        s_seg[0][threadIdx.x] = (uint32_t)T.seg_off[l];
+        s_seg[1][threadIdx.x] = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
+        s_seg[2][threadIdx.x] = (uint32_t)T.seg_k[l];
+        s_seg[3][threadIdx.x] = (uint32_t)T.seg_P[l];
       }
+      for (int x = threadIdx.x; x < nw * ns; x += kNT) {
+        const int w = x / ns, l = l0 + x % ns;
+        const uint32_t n = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
+        s_st[x] = start[(size_t)(w0 + w) * T.L + l] % n;
+      }
+      __syncthreads();
+      for (int w = 0; w < nw; ++w) {
+        const float* v = val + (size_t)(w0 + w) * K;
+        for (int x = 0; x < ns; ++x) {
+          const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], P = s_seg[3][x];
+          const uint32_t s = s_st[w * ns + x];
+          // run piece 1: global [o + s, o + min(s + k, n)), t = i - o - s;
+          // run piece 2: global [o, o + s + k - n), t = i - o + n - s
+          const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + min(s + k, n));
+          const uint32_t a2 = max(lo, o), b2 = s + k > n ? min(hi, o + (s + k - n)) : 0u;
+          if (a1 >= b1 && a2 >= b2) continue;
+#pragma unroll
+          for (int r = 0; r < kRounds; ++r) {
+            const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const uint32_t i = i0 + q;
+              if (i >= a1 && i < b1) a[r][q] += v[P + (i - o - s)];
+              else if (i >= a2 && i < b2) a[r][q] += v[P + (i - o + n - s)];
+            }
+          }
+        }
+      }
+      __syncthreads();  // s_st and s_seg are rewritten by the next group
     }
-    __syncthreads();
   }
-  agg_write(out, lo, hi, acc, average, (float)W);
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    float v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(a[r][q], (float)W) : a[r][q];
+    store4(out, i0, nv, v);
+  }
 }
 
 // ---------------------------------------------------------------------------------------------

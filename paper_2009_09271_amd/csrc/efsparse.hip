@@ -21,6 +21,7 @@ namespace {
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int32_t agg_tiles(int64_t d) { return (int32_t)((d + kAggTile - 1) / kAggTile); }
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // Packs int32 / uint64 host arrays into one blob with 256-byte aligned sub-arrays.
@@ -533,7 +534,7 @@ size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W) {
     case EF_OP_RANDBLOCK: return 0;
     case EF_OP_AGG_SPARSE:
       if (W < 1) return 0;
-      return align_up((size_t)W * ((size_t)layout->nchunks + 1) * 4, kAlign);
+      return align_up((size_t)W * ((size_t)agg_tiles(layout->d) + 1) * 4, kAlign);
     case EF_OP_AGG_BLOCK: return 0;
     default: return 0;
   }
@@ -646,11 +647,11 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     if (ws_bytes < need) return EF_EWORKSPACE;
     const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
     uint32_t* ts = reinterpret_cast<uint32_t*>(ws);
-    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K,
-                       L->nchunks, m, ts);
+    const int32_t nt = agg_tiles(L->d);
+    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts);
     EF_TRY(launched());
-    EF_LAUNCH(k_agg_sparse, grid, blk, 0, st, L->T.d, W, (int32_t)L->K, L->nchunks, m, val, ts,
-                       average, out);
+    EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), blk, 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average,
+              out);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {

@@ -122,3 +122,49 @@ def test_randblock_deterministic_and_shared_seed():
     a = c.step("randblock", g, dev(e), 11, 4)
     b = c.step("randblock", g, dev(e), 11, 4)
     assert np.array_equal(host(a[0]), host(b[0])) and np.array_equal(bits(host(a[1])), bits(host(b[1])))
+
+
+@pytest.mark.parametrize("W,rho", [(70, 0.002), (70, 0.05), (4, 0.5)], ids=["regs-2groups", "lds-2groups", "lds-dense"])
+def test_aggregate_sparse_modes(W, rho):
+    """Tiles summed in registers (few entries) and in LDS (many), more than one worker group of
+    ranges, and several staging passes per group."""
+    announce("aggregate modes", W, rho)
+    c = Case([0, 3, 9000, 9001, 20000], rho)
+    rng = np.random.default_rng(int(W * 1000 * rho))
+    msgs = []
+    for w in range(W):
+        acc = (rng.standard_normal(c.d) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+        msgs.append(O.compress_randk(acc, c.offs, c.ks, 7 + w, 1))
+    for average in (True, False):
+        _agg_check(c, "sparse", msgs, W, average)
+
+
+@pytest.mark.parametrize("W", [3, 20, 70])
+def test_aggregate_block_many_segments_per_tile(W):
+    """150 segments of 7 elements share the first tile (more than one pass of segments and, with
+    many workers, more than one group of block starts)."""
+    announce("aggregate block segments", W)
+    offs = list(range(0, 7 * 151, 7)) + [30000]
+    c = Case(offs, 0.3, 4)
+    rng = np.random.default_rng(W)
+    msgs = []
+    for w in range(W):
+        acc = rng.standard_normal(c.d).astype(np.float32)
+        msgs.append(O.compress_randblock(acc, c.offs, c.ks, 4, 50 + w, 2))
+    for average in (True, False):
+        _agg_check(c, "block", msgs, W, average)
+
+
+@pytest.mark.parametrize("W,rho", [(4, 0.002), (16, 0.05)], ids=["few-shared", "many-shared"])
+def test_aggregate_sparse_shared_coordinates(W, rho):
+    """Random-k with one seed for all workers (every position is hit by every worker): the shared
+    positions are summed in worker order, by walking (few) or worker by worker (many)."""
+    announce("aggregate shared", W, rho)
+    c = Case([0, 3, 9000, 9001, 20000], rho)
+    rng = np.random.default_rng(W)
+    msgs = []
+    for w in range(W):
+        acc = (rng.standard_normal(c.d) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+        msgs.append(O.compress_randk(acc, c.offs, c.ks, 1234, 3))
+    for average in (True, False):
+        _agg_check(c, "sparse", msgs, W, average)
