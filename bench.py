@@ -86,43 +86,54 @@ def kernel_alg_bytes(name, d, K, L, W):
     return None
 
 
-def cpu_baseline(wl, offs, ks, variants, W, g0, budget_note):
-    """Time the CPU oracle on one worker's step per variant plus one aggregate per
-    variant, and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
+def cpu_baseline(wl, offs, ks, variants, W, grads, budget_note):
+    """Time the CPU oracle on a bounded sample of worker steps plus one aggregate per variant,
+    and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
     from oracle import efsparse_oracle as O
     from threadpoolctl import threadpool_limits
     with threadpool_limits(1):
-        return _cpu_baseline(O, wl, offs, ks, variants, W, g0, budget_note)
+        return _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note)
 
 
-def _cpu_baseline(O, wl, offs, ks, variants, W, g0, budget_note):
+def _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note, min_s=10.0):
+    """Workers 0, 1, ... (as many as it takes to pass min_s seconds, at most W) each run one
+    fused step per variant; each variant also aggregates W copies of worker 0's message."""
+    from workloads import worker_seed
     d = offs[-1]
     e0 = np.zeros(d, np.float32)
-    t_steps, t_aggs, parts = 0.0, 0.0, []
-    from workloads import worker_seed
-    for kind, b in variants:
-        t0 = time.perf_counter()
-        (m, val), _ = O.ef_step(kind, g0, e0, offs, ks, seed=worker_seed(wl, 0), step=0, block=b)
-        t1 = time.perf_counter()
-        if kind == "randblock":
-            O.decompress_aggregate_block(d, offs, ks, [m] * W, [val] * W)
-        else:
-            O.decompress_aggregate_sparse(d, [m] * W, [val] * W)
-        t2 = time.perf_counter()
-        t_steps += t1 - t0
-        t_aggs += t2 - t1
-        parts.append(f"{vname((kind, b))} step {t1 - t0:.2f}s + aggregate {t2 - t1:.2f}s")
-    est_step_s = W * t_steps + t_aggs
+    t_steps = {v: [] for v in variants}
+    t_aggs, parts, spent = {}, [], 0.0
+    nw = 0
+    while nw < W and (nw == 0 or spent < min_s):
+        for kind, b in variants:
+            t0 = time.perf_counter()
+            (m, val), _ = O.ef_step(kind, grads[nw], e0, offs, ks, seed=worker_seed(wl, nw), step=0, block=b)
+            t1 = time.perf_counter()
+            t_steps[(kind, b)].append(t1 - t0)
+            spent += t1 - t0
+            if nw == 0:
+                if kind == "randblock":
+                    O.decompress_aggregate_block(d, offs, ks, [m] * W, [val] * W)
+                else:
+                    O.decompress_aggregate_sparse(d, [m] * W, [val] * W)
+                t_aggs[(kind, b)] = time.perf_counter() - t1
+                spent += t_aggs[(kind, b)]
+        nw += 1
+    est_step_s = 0.0
+    for v in variants:
+        mean = sum(t_steps[v]) / len(t_steps[v])
+        est_step_s += W * mean + t_aggs[v]
+        parts.append(f"{vname(v)} step {mean:.2f}s + aggregate {t_aggs[v]:.2f}s")
     value = len(variants) * W * d / est_step_s
     return {
         "value": value,
         "unit": "elements/s",
         "cores": 1,
         "kind": "oracle",
-        "sample": (f"worker 0, step 0 of the same workload: one fused step per variant and one "
-                   f"aggregate of W={W} messages per variant ({'; '.join(parts)}); the step time is "
-                   f"scaled as W x steps + aggregates; NumPy, 1 thread{budget_note}"),
-        "measured_s": t_steps + t_aggs,
+        "sample": (f"step 0 of workers 0..{nw - 1} of the same workload: one fused step per worker and "
+                   f"variant, and one aggregate of W={W} messages per variant (means: {'; '.join(parts)}); "
+                   f"scaled to the GPU step as W x step + aggregate per variant; NumPy, 1 thread{budget_note}"),
+        "measured_s": round(spent, 2),
     }
 
 
@@ -138,6 +149,11 @@ def main():
     ap.add_argument("--variants", default="topk,randk,randblock")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="N",
+                    help="first launch the library's plain copy kernel N times on d floats (a known "
+                         "4d-byte read + 4d-byte write per launch) to calibrate HBM byte counters")
+    ap.add_argument("--streams", type=int, default=3,
+                    help="HIP streams the simulated workers are spread over (plus one for the aggregates)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -171,6 +187,14 @@ def main():
     K, L = lay0.K, lay0.n_seg
 
     g = [torch.from_numpy(x).to(dev) for x in grads]
+    if args.calibrate_copy:
+        src_c = torch.randn(d, device=dev)
+        dst_c = torch.empty(d, device=dev)
+        none = torch.full((K,), d, dtype=torch.int32, device=dev)  # out-of-range: nothing zeroed
+        for _ in range(args.calibrate_copy):
+            E.ef_update(lay0, src_c, E.EF_MSG_SPARSE, none, dst_c)
+        torch.cuda.synchronize()
+        del src_c, dst_c, none
     e = {vname(v): [torch.zeros(d, dtype=torch.float32, device=dev) for _ in range(W)] for v in variants}
     msg = {}
     for v in variants:
@@ -178,28 +202,63 @@ def main():
         msg[vname(v)] = (torch.empty((W, n_m), dtype=torch.int32, device=dev),
                          torch.empty((W, K), dtype=torch.float32, device=dev))
     out = {vname(v): torch.empty(d, dtype=torch.float32, device=dev) for v in variants}
-    ws_topk = lay0.workspace(E.EF_OP_TOPK, 1, dev)
-    ws_randk = lay0.workspace(E.EF_OP_RANDK, 1, dev)
+    S = max(1, args.streams)
+    kinds = {k for k, _ in variants}
+    ws_topk = [lay0.workspace(E.EF_OP_TOPK, 1, dev) for _ in range(S)] if "topk" in kinds else None
+    ws_randk = [lay0.workspace(E.EF_OP_RANDK, 1, dev) for _ in range(S)] if "randk" in kinds else None
     ws_agg = lay0.workspace(E.EF_OP_AGG_SPARSE, W, dev)
+    # worker streams and one aggregate stream, all at the default priority
+    wstreams = [torch.cuda.Stream(dev) for _ in range(S)]
+    astream = torch.cuda.Stream(dev)
 
-    def run_variant(v, t):
+    def worker_step(v, w, t, slot):
         kind, b = v
         lay = layouts[b if kind == "randblock" else 1]
         mi, mv = msg[vname(v)]
         ev = e[vname(v)]
-        for w in range(W):
-            if kind == "topk":
-                E.ef_step_topk(lay, g[w], ev[w], mi[w], mv[w], ws_topk)
-            elif kind == "randk":
-                E.ef_step_randk(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], ws_randk)
-            else:
-                E.ef_step_randblock(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w])
+        if kind == "topk":
+            E.ef_step_topk(lay, g[w], ev[w], mi[w], mv[w], ws_topk[slot])
+        elif kind == "randk":
+            E.ef_step_randk(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], ws_randk[slot])
+        else:
+            E.ef_step_randblock(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w])
+
+    def aggregate(v):
+        kind, b = v
+        lay = layouts[b if kind == "randblock" else 1]
+        mi, mv = msg[vname(v)]
         kindm = E.EF_MSG_BLOCK if kind == "randblock" else E.EF_MSG_SPARSE
         E.decompress_aggregate(lay, kindm, W, mi, mv, out[vname(v)], ws_agg if kindm == E.EF_MSG_SPARSE else None)
 
-    def run_step(t):
-        for v in variants:
-            run_variant(v, t)
+    def run_step(t, vs=None):
+        """One step.  Block-random-k variants run first on one stream (pure streaming kernels gain
+        nothing from overlap, and their launches stay clean to time).  Then the top-k / random-k
+        variants: worker w on stream w % S, so the short selection kernels of one worker overlap
+        the streaming pass of another; each variant's aggregate runs on its own stream once the
+        variant's W messages are written, overlapping the next variant's workers."""
+        vs = vs or variants
+        cur = torch.cuda.current_stream(dev)
+        s0 = wstreams[0]
+        s0.wait_stream(cur)
+        with torch.cuda.stream(s0):
+            for v in vs:
+                if v[0] == "randblock":
+                    for w in range(W):
+                        worker_step(v, w, t, 0)
+                    aggregate(v)
+        conc = [v for v in vs if v[0] != "randblock"]
+        for st in wstreams[1:] + [astream]:
+            st.wait_stream(s0)
+        for v in conc:
+            for w in range(W):
+                with torch.cuda.stream(wstreams[w % S]):
+                    worker_step(v, w, t, w % S)
+            for st in wstreams:
+                astream.wait_stream(st)
+            with torch.cuda.stream(astream):
+                aggregate(v)
+        for st in wstreams + [astream]:
+            cur.wait_stream(st)
 
     step_no = 0
     for _ in range(args.warmup):
@@ -219,18 +278,16 @@ def main():
     elems_per_step = len(variants) * W * d
     value = elems_per_step / (ms_per_step / 1e3)
 
-    # ---- per-variant breakdown (events on the stream the library launches on) -----------------
+    # ---- per-variant breakdown: the same schedule with one variant at a time ----------------
     per = {}
-    stream = torch.cuda.current_stream(dev)
     for v in variants:
-        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            run_variant(v, step_no)
-            step_no += 1
-        b_.record(stream)
         torch.cuda.synchronize()
-        ms = a.elapsed_time(b_) / args.steps
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            run_step(step_no, [v])
+            step_no += 1
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t1) * 1e3 / args.steps
         step_b, agg_b = alg_bytes_op(v[0], d, K, L, W)
         per[vname(v)] = {
             "ms_per_step": round(ms, 4),
@@ -262,15 +319,23 @@ def main():
         dom = next(iter(kernels))
         ab = kernel_alg_bytes(dom, d, K, L, W)
         if ab is not None:
+            from paper_2009_09271_amd.rocprof_summary import read_traffic
             achieved = ab / (kernels[dom]["avg_us"] * 1e-6) / 1e9
+            base = dom.strip("(").split("<")[0]
+            tfile = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                                 f"{base}_{wl.name}_{args.scope}_traffic.md")
+            traffic = read_traffic(tfile, base)
             roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                        "alg_bytes_per_launch": ab, "avg_launch_us": kernels[dom]["avg_us"]}
+                        "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": round(traffic) if traffic is not None else None,
+                        "alg_bytes_per_launch": ab, "avg_launch_us": kernels[dom]["avg_us"],
+                        "traffic_source": os.path.relpath(tfile, os.path.dirname(os.path.abspath(__file__)))
+                        if traffic is not None else None}
 
     cpu = None
     if not args.no_cpu_baseline:
         ks = [int(k) for k in lay0.segment_k()]
-        cpu = cpu_baseline(wl, offs, ks, variants, W, grads[0], "")
+        cpu = cpu_baseline(wl, offs, ks, variants, W, grads, "")
 
     line = {
         "metric": METRIC,
@@ -292,6 +357,7 @@ def main():
                          f"+ one aggregate per variant per step"),
             "d": d, "segments": L, "K": K, "W": W, "density": density,
             "variants": [vname(v) for v in variants], "scope": args.scope,
+            "streams": f"{S} worker streams + 1 aggregate stream",
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

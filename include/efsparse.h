@@ -201,7 +201,9 @@ int ef_step_randblock(const ef_layout* layout, const void* g, int g_dtype, float
 size_t ef_workspace_diag_offset(const ef_layout* layout, int op);
 
 /* Per-kernel timing (diagnostics).  While enabled, every kernel the library
- * launches is bracketed by two HIP events recorded on the launch's stream.
+ * launches carries a start and a stop HIP event that the runtime binds to the
+ * kernel's own dispatch on its stream (hipExtLaunchKernelGGL), so a launch's
+ * duration is its execution time.
  * ef_timing_collect waits for the recorded events and adds each launch's
  * duration to a per-kernel total; ef_timing_get reads total i (kernel name in
  * static storage owned by the library, total milliseconds, launch count).

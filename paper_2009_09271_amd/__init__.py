@@ -236,7 +236,7 @@ def lib():
 
 
 def timing_enable(on=True):
-    """Record HIP events around every library kernel launch (see ef_timing_enable)."""
+    """Time every library kernel launch with dispatch-bound HIP events (see ef_timing_enable)."""
     _check(_lib.ef_timing_enable(1 if on else 0), "ef_timing_enable")
 
 

@@ -1,6 +1,7 @@
 // efsparse host library: layouts, argument checking, workspace layout and kernel launches.
 // The C ABI is declared in include/efsparse.h.
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -241,28 +242,27 @@ hipEvent_t pool_event() {
   return e;
 }
 
-size_t timing_begin(const char* name, hipStream_t st) {
-  if (!g_timing) return 0;
+// While timing is on, a launch gets a start and a stop event that the runtime ties to the kernel's
+// own dispatch (hipExtLaunchKernelGGL), so the elapsed time is the kernel's execution alone.
+bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
+  if (!g_timing) return false;
   std::lock_guard<std::mutex> lk(g_tm);
   TimingRec r{name, pool_event(), pool_event()};
-  if (!r.a || !r.b) return 0;
-  (void)hipEventRecord(r.a, st);
+  if (!r.a || !r.b) return false;
   g_pending.push_back(r);
-  return g_pending.size();
-}
-
-void timing_end(size_t slot, hipStream_t st) {
-  if (!slot) return;
-  std::lock_guard<std::mutex> lk(g_tm);
-  (void)hipEventRecord(g_pending[slot - 1].b, st);
+  *a = r.a;
+  *b = r.b;
+  return true;
 }
 
 // Every launch goes through this macro: the kernel is named after its expression.
-#define EF_LAUNCH(KERNEL, GRID, BLOCK, SHM, ST, ...)                 \
-  do {                                                               \
-    const size_t _slot = timing_begin(#KERNEL, ST);                  \
-    hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHM, ST, __VA_ARGS__);   \
-    timing_end(_slot, ST);                                           \
+#define EF_LAUNCH(KERNEL, GRID, BLOCK, SHM, ST, ...)                                   \
+  do {                                                                                 \
+    hipEvent_t _ea = nullptr, _eb = nullptr;                                           \
+    if (timing_slot(#KERNEL, &_ea, &_eb))                                              \
+      hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHM, ST, _ea, _eb, 0u, __VA_ARGS__); \
+    else                                                                               \
+      hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHM, ST, __VA_ARGS__);                  \
   } while (0)
 
 #define EF_TRY(x)              \
