@@ -105,8 +105,9 @@ def pmc(fetch_csv, write_csv, kernel, calib, calib_bytes, alg_bytes, out, comman
 
 
 def read_traffic(path, kernel):
-    """Scaled HBM bytes per launch of `kernel` from a `pmc` summary, or None when the summary is
-    missing, is for another kernel, or was taken on different kernel sources."""
+    """Scaled HBM bytes per launch of the kernel whose name starts with `kernel` from a `pmc`
+    summary, or None when the summary is missing, is for another kernel, or was taken on
+    different kernel sources."""
     if not os.path.exists(path):
         return None
     vals = {}
@@ -116,7 +117,7 @@ def read_traffic(path, kernel):
         elif ":" in line and line.split(":")[0] in ("traffic_bytes_per_launch", "kernel"):
             k, v = line.split(":", 1)
             vals[k] = v.strip()
-    if vals.get("hash") != kernel_source_hash() or not kernel.startswith(vals.get("kernel", "\0")):
+    if vals.get("hash") != kernel_source_hash() or not vals.get("kernel", "").startswith(kernel):
         return None
     try:
         return float(vals["traffic_bytes_per_launch"])
