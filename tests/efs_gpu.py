@@ -111,3 +111,67 @@ def assert_f32_equal(got, want, where=""):
     got = host(got) if not isinstance(got, np.ndarray) else got
     bad = np.nonzero(bits(got) != bits(want))[0]
     assert bad.size == 0, f"{where}: {bad.size} mismatching elements, first {bad[:5]}: {got[bad[:5]]} vs {want[bad[:5]]}"
+
+
+# ---- exact certificates for sizes where the full oracle sort is too slow ------------------------
+# Each checks the definition directly: the sent set is unique given (key order, index order), so
+# these properties hold for the oracle's answer and for no other set.
+
+def _check_message_and_residual(acc, idx, val, e_new, where):
+    idx = np.asarray(idx).view(np.uint32).astype(np.int64)
+    assert np.array_equal(bits(val), bits(acc[idx])), f"{where}: values differ from acc at the indices"
+    want = acc.copy()
+    want[idx] = 0.0
+    assert_f32_equal(e_new, want, f"{where}: residual")
+    return idx
+
+
+def certify_topk(acc, offs, ks, idx, val, e_new, where="topk"):
+    """Per segment: k sorted distinct indices inside it; every unsent key <= the smallest sent key
+    T; among keys equal to T the sent ones have the lower indices."""
+    idx = _check_message_and_residual(acc, idx, val, e_new, where)
+    key = acc.view(np.uint32) & np.uint32(0x7FFFFFFF)
+    P = 0
+    for l, k in enumerate(ks):
+        o, n = offs[l], offs[l + 1] - offs[l]
+        S = idx[P:P + k] - o
+        P += k
+        assert S.size == k and S.min() >= 0 and S.max() < n and np.all(np.diff(S) > 0), f"{where} seg {l}: support"
+        seg = key[o:o + n]
+        T = seg[S].min()
+        sel = np.zeros(n, dtype=bool)
+        sel[S] = True
+        assert np.where(sel, np.uint32(0), seg).max() <= T, f"{where} seg {l}: an unsent key beats a sent one"
+        tie_sent = S[seg[S] == T]
+        tie_unsent = np.nonzero(~sel & (seg == T))[0]
+        if tie_unsent.size:
+            assert tie_sent.max() < tie_unsent.min(), f"{where} seg {l}: ties must go to lower indices"
+
+
+def certify_randk(acc, offs, ks, idx, val, e_new, seed, step, where="randk"):
+    """Per segment, with the oracle's Philox keys u: every unsent u >= the largest sent u T; among
+    keys equal to T the sent ones have the lower indices."""
+    idx = _check_message_and_residual(acc, idx, val, e_new, where)
+    P = 0
+    for l, k in enumerate(ks):
+        o, n = offs[l], offs[l + 1] - offs[l]
+        S = idx[P:P + k] - o
+        P += k
+        assert S.size == k and S.min() >= 0 and S.max() < n and np.all(np.diff(S) > 0), f"{where} seg {l}: support"
+        u = O.randk_keys(n, l, seed, step)
+        T = u[S].max()
+        sel = np.zeros(n, dtype=bool)
+        sel[S] = True
+        assert np.where(sel, np.uint32(0xFFFFFFFF), u).min() >= T, f"{where} seg {l}: an unsent key beats a sent one"
+        tie_sent = S[u[S] == T]
+        tie_unsent = np.nonzero(~sel & (u == T))[0]
+        if tie_unsent.size:
+            assert tie_sent.max() < tie_unsent.min(), f"{where} seg {l}: ties must go to lower indices"
+
+
+def synthetic_sparse_messages(d, K, W, seed):
+    """W messages of K ascending distinct indices with random values (seeded; message shape only)."""
+    rng = np.random.default_rng(seed)
+    idx = np.stack([np.sort(rng.choice(d, size=K, replace=False)) for _ in range(W)]).astype(np.uint32)
+    val = rng.standard_normal((W, K)).astype(np.float32)
+    return idx, val
