@@ -37,6 +37,7 @@ struct WSel {
   uint32_t* counts;    // [nrows] candidates per row
   uint32_t* rcnt;      // [nrows] winners per row
   uint32_t* roff;      // [nrows] message position of each row's first winner
+  uint32_t* rtie;      // [nrows] top-k: candidates in the threshold bin when that bin is the key A
   uint32_t* lcnt;      // [L][kSubLists][kLineWords] sizes of the sub-lists, one cache line each
   uint32_t* cand_idx;  // [nrows * kTile] per-row candidate slots, index order
   float* cand_val;     // [nrows * kTile]
@@ -734,10 +735,12 @@ __device__ __forceinline__ uint32_t block_nth_smallest_tie(const K& keys, const 
   return ~prefix;
 }
 
-// Candidate histogram bin of a top-k key (higher bins hold larger keys): (key - A) >> sh, clamped
-// to the last bin.
+// Candidate histogram bin of a top-k key >= A (higher bins hold larger keys).  Bin 0 holds the
+// key A alone, so that a threshold landing on a value shared by very many elements (exact zeros,
+// say) is recognised as a pure tie; larger keys go to 1 + ((key - A - 1) >> sh), clamped to the
+// last bin.
 __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t sh) {
-  return min((key - A) >> sh, (uint32_t)kHBins - 1u);
+  return key == A ? 0u : 1u + min((key - A - 1u) >> sh, (uint32_t)kHBins - 2u);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1069,6 +1072,7 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws) {
   };
   const uint32_t cnt = ws.counts[row];
   const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
+  const bool tie_bin = KIND == 0 && B == 0;  // the threshold bin is the single key A: count, do not list
   uint32_t na = 0, ne = 0;
   for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
     const uint32_t c = cls(ck[j]);
@@ -1079,6 +1083,13 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws) {
   const uint32_t ex = block_excl_scan<kNT>(na | (ne << 16), lds, tot);  // row totals <= kTile
   const uint32_t tot_e = tot >> 16;
   const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
+  if (tie_bin) {
+    if (threadIdx.x == 0) {
+      ws.rcnt[row] = tot & 0xFFFFu;
+      ws.rtie[row] = tot_e;
+    }
+    return;
+  }
   if (threadIdx.x == 0) {
     ws.rcnt[row] = tot & 0xFFFFu;
     s_base = tot_e ? atomicAdd(lcnt_of(ws, l, c), tot_e) : 0u;
@@ -1275,7 +1286,49 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
     return;
   }
   const bool rows_lds = nr <= kRowsLds;
-  if (listed) {
+  bool tie = false;
+  if constexpr (KIND == 0) tie = listed && R[R_B] == 0;
+  if (tie) {
+    // The threshold bin is the key A alone: the first `need` candidates equal to A, in index
+    // order, win.  Rows hold their candidates in index order, so a scan of the rows' tie counts
+    // finds the row of the last winner, and one pass over that row finds the winner itself.
+    __shared__ uint32_t s_row, s_rank;
+    const uint32_t* rt = ws.rtie + r0;
+    uint32_t tl[kPer], st = 0;
+#pragma unroll
+    for (uint32_t x = 0; x < kPer; ++x) {
+      tl[x] = a + x < b ? rt[a + x] : 0u;
+      st += tl[x];
+    }
+    for (uint32_t x = a + kPer; x < b; ++x) st += rt[x];
+    uint32_t totT;
+    uint32_t before = block_excl_scan<kSelNT>(st, lds, totT);
+    uint32_t* rcw = ws.rcnt + r0;
+    for (uint32_t x = a; x < b; ++x) {
+      const uint32_t t = x - a < kPer ? tl[x - a] : rt[x];
+      const uint32_t take = min(t, need > before ? need - before : 0u);
+      if (before < need && need <= before + t) {
+        s_row = x;
+        s_rank = need - before;
+      }
+      if (x - a < kPer) {
+#pragma unroll
+        for (uint32_t y = 0; y < kPer; ++y)
+          if (y == x - a) cr[y] += take;
+      } else {
+        rcw[x] += take;  // re-read by this thread below
+      }
+      before += t;
+    }
+    __syncthreads();
+    const uint32_t row = r0 + s_row;
+    const uint32_t p = block_nth_equal(ws.cand_key + (size_t)row * kTile, ws.counts[row], R[R_A], s_rank, lds);
+    if (threadIdx.x == 0) {
+      R[R_T] = R[R_A];
+      R[R_IT] = ws.cand_idx[(size_t)row * kTile + p] + 1u;
+    }
+  }
+  if (listed && !tie) {
     const uint32_t o = (uint32_t)T.seg_off[l];
     SubLists lk, li;
     lk.arr = ws.list_key;
@@ -1343,7 +1396,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
   }
   // row offsets: exclusive scan of the rows' winner counts (mode 1: every candidate wins)
   const uint32_t* cnt = listed ? rc : cc;
-  const bool add = listed && rows_lds;
+  const bool add = listed && rows_lds && !tie;
   uint32_t w[kPer], sum = 0;
 #pragma unroll
   for (uint32_t x = 0; x < kPer; ++x) {

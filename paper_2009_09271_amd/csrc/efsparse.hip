@@ -38,7 +38,7 @@ struct Blob {
 };
 
 struct WsLayout {
-  size_t diag = 0, res = 0, hist = 0, samp = 0, counts = 0, rcnt = 0, roff = 0, lcnt = 0, cand_idx = 0, cand_val = 0,
+  size_t diag = 0, res = 0, hist = 0, samp = 0, counts = 0, rcnt = 0, roff = 0, rtie = 0, lcnt = 0, cand_idx = 0, cand_val = 0,
          cand_key = 0, list_idx = 0, list_key = 0, total = 0;
 };
 
@@ -172,6 +172,7 @@ WsLayout ef_layout::ws_layout(int op) const {
   w.counts = take(rows * 4);
   w.rcnt = take(rows * 4);
   w.roff = take(rows * 4);
+  w.rtie = take(rows * 4);
   w.lcnt = take((size_t)L * kSubLists * kLineWords * 4);
   w.cand_idx = take(slots * 4);
   w.cand_val = take(slots * 4);
@@ -194,6 +195,7 @@ WSel make_ws(const WsLayout& l, void* base) {
   w.counts = reinterpret_cast<uint32_t*>(b + l.counts);
   w.rcnt = reinterpret_cast<uint32_t*>(b + l.rcnt);
   w.roff = reinterpret_cast<uint32_t*>(b + l.roff);
+  w.rtie = reinterpret_cast<uint32_t*>(b + l.rtie);
   w.lcnt = reinterpret_cast<uint32_t*>(b + l.lcnt);
   w.cand_idx = reinterpret_cast<uint32_t*>(b + l.cand_idx);
   w.cand_val = reinterpret_cast<float*>(b + l.cand_val);

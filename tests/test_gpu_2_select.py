@@ -194,3 +194,30 @@ def test_topk_concentrated_magnitudes():
     g = ((1.0 + 0.1 * rng.random(d)) * rng.choice([-1.0, 1.0], d)).astype(np.float32)
     c = Case([0, d], 0.01)
     _run_steps(c, "topk", [g, g], np.zeros(d, np.float32))
+
+
+@pytest.mark.parametrize("zero_frac,rho", [(0.9, 0.2), (0.9, 0.05), (0.5, 0.6)], ids=["k>nonzeros", "k<nonzeros", "half-zero"])
+@pytest.mark.parametrize("layered", [False, True], ids=["flat", "layers"])
+def test_topk_threshold_on_a_massive_tie(zero_frac, rho, layered):
+    """Most elements exactly zero (embedding rows without tokens): when k exceeds the nonzeros the
+    threshold is the key 0 itself and the zeros are taken by index; the threshold bin is then a
+    pure tie, resolved from per-row tie counts."""
+    announce("topk massive tie", zero_frac, rho, layered)
+    rng = np.random.default_rng(24)
+    d = 300000
+    offs = [0, 123457, 123461, d] if layered else [0, d]
+    c = Case(offs, rho)
+    g = (rng.standard_normal(d) * 1e-3).astype(np.float32)
+    g[rng.random(d) < zero_frac] = 0.0
+    g[::7] = np.where(g[::7] == 0.0, np.float32(-0.0), g[::7])
+    _run_steps(c, "topk", [g, g * np.float32(0.5)], np.zeros(d, np.float32))
+
+
+def test_topk_threshold_on_a_repeated_value():
+    """A value repeated many times right at the threshold (quantised gradients)."""
+    announce("topk repeated value")
+    rng = np.random.default_rng(25)
+    d = 250000
+    g = rng.choice(np.array([0.5, -0.5, 0.25, 0.125, 1.0], np.float32), size=d, p=[0.3, 0.3, 0.2, 0.15, 0.05])
+    c = Case([0, d], 0.2)
+    _run_steps(c, "topk", [g, g], np.zeros(d, np.float32))
