@@ -61,6 +61,7 @@ struct Tables {
   const int32_t* seg_bl;       // [L]
   const int32_t* seg_nb;       // [L]
   const int32_t* seg_srank;    // [L]   top-k: rank of the candidate threshold inside the sample
+  const int32_t* seg_urank;    // [L]   top-k: sample rank bounding the k-th key from above
   const int32_t* seg_cbase;    // [L+1] first row of each segment (a row = segment x data tile)
   const int32_t* seg_ro;       // [L+1] first top-k sample run of each segment
   const uint64_t* seg_tau;     // [L]   random-k: Philox keys below tau are candidates

@@ -519,7 +519,7 @@ constexpr int kBatch = 8;             // independent loads in flight per thread 
 constexpr uint32_t kListLds = 8192;    // listed candidates held in LDS by k_select
 constexpr uint32_t kRowsLds = 16384;   // rows per segment whose list additions k_select counts in LDS
 constexpr uint32_t kRankList = 256;    // lists up to this size are ranked directly (no radix levels)
-constexpr uint32_t kHistDirect = 256;  // rows with more candidates histogram them in LDS first
+constexpr uint32_t kHistDirect = 32;   // rows with more candidates histogram them in LDS first
 constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
 constexpr uint32_t kDiagCount = 4u;    // diagnostics: the row counts of a segment did not add up to k_l
 
@@ -783,12 +783,15 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, const vo
 //    bound I (one past the index of the last tie sent; ties go to lower indices); the candidates
 //    are then exactly the winners (mode 1).
 //  * larger segments: A = the lower edge of the bin of the top 11 key bits that holds the
-//    srank-th largest sampled key; every key >= A is a candidate, and the candidates are
-//    histogrammed by (key - A) >> sh with sh chosen so that the largest sampled key falls below
-//    bin 1024 (mode 0).
+//    srank-th largest sampled key (srank: the expected rank of the k_l-th key in the sample plus
+//    a margin); every key >= A is a candidate.  The candidates are histogrammed in bins of 2^sh
+//    keys above A, sh chosen so that the range up to the urank-th sampled key (the expected rank
+//    minus the margin) spans about 1024 bins: the k_l-th key very likely falls inside it, and the
+//    bins there are as narrow as the sample allows (mode 0).
 __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[kHBins];
+  __shared__ uint32_t hist2[kHBins];
   __shared__ uint32_t lds[2 * kSelNT / 64];
   const int l = blockIdx.x;
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
@@ -825,27 +828,30 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws) {
   });
   __syncthreads();
   kmax = block_max_u32(kmax, lds);
-  const uint32_t rank = (uint32_t)T.seg_srank[l];
-  uint32_t thr = 0;  // rank >= sample size: every element is a candidate
-  if (rank < (uint32_t)kSampleMax) {
+  // Key edge of the rank-th largest sampled key: the lower (or upper) edge of its top-11-bit bin,
+  // refined by the next 11 bits when that bin holds many sampled keys (concentrated values).
+  auto rank_edge = [&](uint32_t rank, bool upper) -> uint32_t {
     uint32_t above;
     const int bin = block_resolve<kSelNT>(hist, kHBins, rank, lds, above);
-    thr = (uint32_t)max(bin, 0) << 20;
-    if (bin >= 0 && hist[bin] > (uint32_t)kSampleMax / 8) {
-      // concentrated keys: refine inside the bin by the next 11 bits (sample re-read from L2)
-      __syncthreads();
-      for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
-      __syncthreads();
-      for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
-        if ((k >> 20) == (uint32_t)bin) atomicAdd(&hist[(k >> 9) & (kHBins - 1)], 1u);
-      });
-      __syncthreads();
-      uint32_t above2;
-      const int bin2 = block_resolve<kSelNT>(hist, kHBins, rank - above, lds, above2);
-      thr |= (uint32_t)max(bin2, 0) << 9;
-    }
-  }
-  const uint32_t span = kmax - thr;
+    if (bin < 0) return 0u;
+    if (hist[bin] <= (uint32_t)kSampleMax / 8) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
+    for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist2[b] = 0;
+    __syncthreads();
+    for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+      if ((k >> 20) == (uint32_t)bin) atomicAdd(&hist2[(k >> 9) & (kHBins - 1)], 1u);
+    });
+    __syncthreads();
+    uint32_t above2;
+    const int bin2 = block_resolve<kSelNT>(hist2, kHBins, rank - above, lds, above2);
+    return ((uint32_t)bin << 20) + (((uint32_t)max(bin2, 0) + (upper ? 1u : 0u)) << 9);
+  };
+  const uint32_t rank = (uint32_t)T.seg_srank[l], urank = (uint32_t)T.seg_urank[l];
+  // rank >= sample size: every element is a candidate
+  const uint32_t thr = rank < (uint32_t)kSampleMax ? rank_edge(rank, false) : 0u;
+  // the bins resolve the range up to the upper edge of where the k-th key very likely lies
+  uint32_t top = rank_edge(urank, true);
+  if (top <= thr || top > kmax) top = kmax;
+  const uint32_t span = top - thr;
   const uint32_t sh = span < 1024u ? 0u : (uint32_t)(32 - __clz(span)) - 10u;
   if (threadIdx.x == 0) {
     R[R_A] = thr;

@@ -52,7 +52,7 @@ struct ef_layout {
   std::vector<int64_t> off64;
   double rk_sigma = 10.0, rk_extra = 64.0, tk_sigma = 6.0, tk_extra = 8.0;
 
-  std::vector<int32_t> off, k, P, bl, nb, srank, cbase, ro, csf, csl, rseg;
+  std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg;
   std::vector<uint64_t> tau;
   std::vector<uint32_t> ulo;
   int64_t K = 0;
@@ -60,7 +60,7 @@ struct ef_layout {
   bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
 
   Blob blob;
-  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
+  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
   Tables T{};
   bool bound = false;
 
@@ -77,6 +77,7 @@ void ef_layout::build() {
   bl.resize(n);
   nb.resize(n);
   srank.resize(n);
+  urank.resize(n);
   tau.resize(n);
   ulo.resize(n);
   cbase.assign(n + 1, 0);
@@ -97,6 +98,8 @@ void ef_layout::build() {
     const double mus = (double)kSampleMax * (double)kl / (double)dl;
     const double rs = std::ceil(mus + tk_sigma * std::sqrt(mus) + tk_extra);
     srank[l] = (int32_t)std::min<double>(std::max<double>(rs, 1.0), (double)kSampleMax);
+    const double ru = std::floor(mus - tk_sigma * std::sqrt(mus));
+    urank[l] = (int32_t)std::min<double>(std::max<double>(ru, 1.0), (double)kSampleMax);
     // random-k: keys below tau are candidates; expected count k + sigma * sqrt(k) + extra
     const double mu = (double)kl + rk_sigma * std::sqrt((double)kl) + rk_extra;
     const double p = mu / (double)dl;
@@ -146,6 +149,7 @@ void ef_layout::build() {
   o_bl = blob.add(bl);
   o_nb = blob.add(nb);
   o_srank = blob.add(srank);
+  o_urank = blob.add(urank);
   o_cbase = blob.add(cbase);
   o_ro = blob.add(ro);
   o_tau = blob.add(tau);
@@ -512,6 +516,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_bl = reinterpret_cast<const int32_t*>(b + L->o_bl);
   T.seg_nb = reinterpret_cast<const int32_t*>(b + L->o_nb);
   T.seg_srank = reinterpret_cast<const int32_t*>(b + L->o_srank);
+  T.seg_urank = reinterpret_cast<const int32_t*>(b + L->o_urank);
   T.seg_cbase = reinterpret_cast<const int32_t*>(b + L->o_cbase);
   T.seg_ro = reinterpret_cast<const int32_t*>(b + L->o_ro);
   T.row_seg = reinterpret_cast<const int32_t*>(b + L->o_rseg);
