@@ -519,6 +519,7 @@ constexpr int kBatch = 8;             // independent loads in flight per thread 
 constexpr uint32_t kListLds = 8192;    // listed candidates held in LDS by k_select
 constexpr uint32_t kRowsLds = 16384;   // rows per segment whose list additions k_select counts in LDS
 constexpr uint32_t kRankList = 256;    // lists up to this size are ranked directly (no radix levels)
+constexpr uint32_t kBigK = 1u << 20;   // layouts with a k_l this large count row winners in parallel
 constexpr uint32_t kHistDirect = 32;   // rows with more candidates histogram them in LDS first
 constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
 constexpr uint32_t kDiagCount = 4u;    // diagnostics: the row counts of a segment did not add up to k_l
@@ -1226,8 +1227,10 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
 // Per segment: the exact threshold among the listed candidates, then every row's message offset;
 // or the exact whole-segment path when the candidates cannot hold the answer.  Independent loads
 // are issued together (record, sub-list sizes, the rows' counts) to keep the chain of dependent
-// memory round trips short.
-template <int KIND>
+// memory round trips short.  BIG (layouts with a very large k_l): only the threshold; the rows'
+// winners are then counted by k_rowcount and scanned by k_rowscan, both spread over many
+// workgroups, instead of one workgroup adding the list's winners to their rows.
+template <int KIND, bool BIG>
 __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const float* data, float* e_zero,
                                                    uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1,
                                                    uint32_t step) {
@@ -1378,7 +1381,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
       else list_threshold(lk, li, m, need, hist, lds, s_gk, s_gi, Tk, IT);
       // the list's winners join their rows' counts
       const uint32_t c0 = o / kTile;
-      for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
+      for (uint32_t j = threadIdx.x; j < (BIG ? 0u : m); j += kSelNT) {
         const uint32_t k = in_lds ? s_key[j] : lk[j];
         const uint32_t i = in_lds ? s_idx[j] : li[j];
         if (k > Tk || (k == Tk && i < IT)) {
@@ -1391,7 +1394,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
       R[R_T] = Tk;
       R[R_IT] = IT;
     }
-    if (!rows_lds) {
+    if (!BIG && !rows_lds) {
       // the additions went to global memory: order them before re-reading the counts
       __threadfence();
       __syncthreads();
@@ -1400,6 +1403,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
     }
     __syncthreads();
   }
+  if constexpr (BIG) return;
   // row offsets: exclusive scan of the rows' winner counts (mode 1: every candidate wins)
   const uint32_t* cnt = listed ? rc : cc;
   const bool add = listed && rows_lds && !tie;
@@ -1424,6 +1428,83 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
     run += cnt[x] + (add ? s_add[x] : 0u);
   }
   if (threadIdx.x == 0 && tot != kl) atomicOr(ws.diag, kDiagCount);
+}
+
+// Large layouts, per row: how many of the row's candidates win (all of them in mode 1).
+template <int KIND>
+__global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws) {
+  __shared__ uint32_t lds[kNT / 64];
+  const uint32_t row = blockIdx.x;
+  const int l = T.row_seg[row];
+  const uint32_t* R = res_of(ws, l);
+  if (R[R_SLOW]) return;
+  const uint32_t cnt = ws.counts[row];
+  uint32_t won = 0;
+  if (KIND == 1 || R[R_MODE] == 0) {
+    const uint32_t Tk = R[R_T], IT = R[R_IT];
+    const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
+    const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
+    for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
+      const uint32_t k = ck[j];
+      won += (k > Tk || (k == Tk && ci[j] < IT)) ? 1u : 0u;
+    }
+  } else {
+    won = threadIdx.x == 0 ? cnt : 0u;
+  }
+  uint32_t tot;
+  (void)block_excl_scan<kNT>(won, lds, tot);
+  if (threadIdx.x == 0) ws.rcnt[row] = tot;
+}
+
+// Large layouts, per segment: message offset of every row (exclusive scan of the winner counts),
+// in tiles of kSelNT * 8 rows: coalesced loads into LDS, eight consecutive rows per thread, a
+// workgroup scan, coalesced stores.
+__global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws) {
+  constexpr uint32_t kU = 8, kTl = kSelNT * kU;
+  __shared__ uint32_t lds[2 * kSelNT / 64];
+  __shared__ uint32_t s_c[kTl + kTl / 32];
+  auto pad = [](uint32_t i) { return i + (i >> 5); };
+  const int l = blockIdx.x;
+  const uint32_t* R = res_of(ws, l);
+  if (R[R_SLOW]) return;
+  const uint32_t r0 = (uint32_t)T.seg_cbase[l], nr = (uint32_t)T.seg_cbase[l + 1] - r0;
+  const uint32_t* cnt = ws.rcnt + r0;
+  uint32_t* roff = ws.roff + r0;
+  uint32_t carry = (uint32_t)T.seg_P[l], total = 0;
+  for (uint32_t t0 = 0; t0 < nr; t0 += kTl) {
+    uint32_t v[kU];
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) {
+      const uint32_t x = t0 + u * kSelNT + threadIdx.x;
+      v[u] = x < nr ? cnt[x] : 0u;
+    }
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) s_c[pad(u * kSelNT + threadIdx.x)] = v[u];
+    __syncthreads();
+    uint32_t sum = 0;
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) {
+      v[u] = s_c[pad(threadIdx.x * kU + u)];
+      sum += v[u];
+    }
+    uint32_t tot;
+    uint32_t run = carry + block_excl_scan<kSelNT>(sum, lds, tot);
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) {
+      s_c[pad(threadIdx.x * kU + u)] = run;
+      run += v[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (uint32_t u = 0; u < kU; ++u) {
+      const uint32_t x = t0 + u * kSelNT + threadIdx.x;
+      if (x < nr) roff[x] = s_c[pad(u * kSelNT + threadIdx.x)];
+    }
+    __syncthreads();
+    carry += tot;
+    total += tot;
+  }
+  if (threadIdx.x == 0 && total != (uint32_t)T.seg_k[l]) atomicOr(ws.diag, kDiagCount);
 }
 
 // Per row: the winners, in index order, to the message at the row's offset; e = +0 there.

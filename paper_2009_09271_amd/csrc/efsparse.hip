@@ -4,6 +4,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -58,6 +59,7 @@ struct ef_layout {
   int64_t K = 0;
   int32_t nchunks = 0, nrows = 0, nruns = 0;
   bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
+  bool big = false;        // some k_l is large: row winners are counted by many workgroups
 
   Blob blob;
   size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
@@ -124,6 +126,7 @@ void ef_layout::build() {
     if (dl > kSampleMax) all_exact = false;
   }
   K = P[n];
+  big = *std::max_element(k.begin(), k.end()) >= kBigK;
   nrows = cbase[n];
   nruns = ro[n];
   rseg.resize(nrows);
@@ -338,7 +341,15 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
     EF_TRY(launched());
   }
   const float* acc = g ? e_fused : src;
-  EF_LAUNCH(k_select<0>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
+  if (L->big) {
+    EF_LAUNCH((k_select<0, true>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
+    EF_TRY(launched());
+    EF_LAUNCH(k_rowcount<0>, rgrid, blk, 0, st, T, w);
+    EF_TRY(launched());
+    EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w);
+  } else {
+    EF_LAUNCH((k_select<0, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
+  }
   EF_TRY(launched());
   EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();
@@ -367,7 +378,15 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
   EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
   EF_TRY(launched());
   const float* acc = g ? e_fused : src;
-  EF_LAUNCH(k_select<1>, sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
+  if (L->big) {
+    EF_LAUNCH((k_select<1, true>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
+    EF_TRY(launched());
+    EF_LAUNCH(k_rowcount<1>, rgrid, blk, 0, st, T, w);
+    EF_TRY(launched());
+    EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w);
+  } else {
+    EF_LAUNCH((k_select<1, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
+  }
   EF_TRY(launched());
   EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();

@@ -221,3 +221,14 @@ def test_topk_threshold_on_a_repeated_value():
     g = rng.choice(np.array([0.5, -0.5, 0.25, 0.125, 1.0], np.float32), size=d, p=[0.3, 0.3, 0.2, 0.15, 0.05])
     c = Case([0, d], 0.2)
     _run_steps(c, "topk", [g, g], np.zeros(d, np.float32))
+
+
+@pytest.mark.parametrize("offs", [[0, 3000000], [0, 5, 1234567, 1234570, 3000000]], ids=["flat", "ragged"])
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+@pytest.mark.parametrize("ties", [False, True], ids=["smooth", "ties"])
+def test_large_k_row_counting(offs, kind, ties):
+    """k_l above 2^20: the row winners are counted and scanned by the many-workgroup kernels."""
+    announce(kind, "large k", offs[-1], ties)
+    c = Case(offs, 0.6)
+    g, e = _inputs(c.d, 31, ties=ties)
+    _run_steps(c, kind, [g, g * np.float32(0.5)], e, seed=17, composed=False)
