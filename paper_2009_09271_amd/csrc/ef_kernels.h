@@ -281,6 +281,13 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
     for (int tau = tj + 1; tau <= nt; ++tau) ts[tau] = (uint32_t)K;
 }
 
+// out = sum / W in IEEE float32.  For W a power of two the quotient is the exact scaling
+// sum * (1 / W), which rounds identically (both are the one correctly rounded result of the same
+// real number), and a multiply costs one instruction instead of a division sequence.
+__device__ __forceinline__ float agg_scale(float sum, int32_t W, bool pow2, float inv) {
+  return pow2 ? sum * inv : __fdiv_rn(sum, (float)W);
+}
+
 constexpr int kAggW = 64;           // workers whose tile ranges are held in LDS at once
 constexpr int kAggStage = 512;      // message entries staged in LDS per pass (2 per thread)
 constexpr int kAggStarts = 1024;    // block starts (workers x segments of the tile) held in LDS
@@ -295,7 +302,9 @@ __device__ __forceinline__ int agg_worker_of(const uint32_t* pre, int nw, uint32
   return a;
 }
 
-// One workgroup per output tile of kAggTile elements, summed in an LDS tile.  Per group of up to
+// Persistent workgroups, each walking output tiles of kAggTile elements (tile blockIdx.x, then
+// every gridDim.x-th), summed in an LDS tile; the next tile's ranges are loaded while the current
+// one is summed and stored.  Per group of up to
 // kAggW workers: the tile's entry range of every worker in one round trip, then passes of up to
 // kAggStage entries staged in LDS in worker order (loads in flight together).  Within a pass an
 // LDS bitmap finds the positions hit more than once: the others take their value at once (no
@@ -318,187 +327,241 @@ __global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_
   __shared__ uint32_t s_seen[kAggTile / 32];
   __shared__ uint32_t s_multi[kAggTile / 32];
   __shared__ uint32_t lds[kNT / 64];
-  const uint32_t tau = blockIdx.x;
-  const uint32_t lo = tau * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
-  for (uint32_t x = threadIdx.x; x < kAggTile; x += kNT) acc[x] = 0.0f;
-  for (int w0 = 0; w0 < W; w0 += kAggW) {
-    const int nw = min(kAggW, W - w0);
-    uint32_t ra = 0, cnt = 0;
-    if ((int)threadIdx.x < nw) {
-      const uint32_t* ts = tile_start + (size_t)(w0 + threadIdx.x) * (nt + 1);
-      ra = min(ts[tau], (uint32_t)K);
-      const uint32_t rb = min(ts[tau + 1], (uint32_t)K);
-      cnt = rb > ra ? rb - ra : 0u;
+  const bool pow2 = (W & (W - 1)) == 0;
+  const float inv = 1.0f / (float)W;  // exact when W is a power of two
+  // the first worker group's ranges of the next tile are loaded one tile ahead
+  uint32_t pa = 0, pb = 0;
+  auto prefetch = [&](uint32_t t) {
+    if ((int)threadIdx.x < min(W, kAggW) && t < (uint32_t)nt) {
+      const uint32_t* ts = tile_start + (size_t)threadIdx.x * (nt + 1);
+      pa = ts[t];
+      pb = ts[t + 1];
     }
-    uint32_t tot;
-    const uint32_t ex = block_excl_scan<kNT>(cnt, lds, tot);
-    if ((int)threadIdx.x < nw) {
-      s_pre[threadIdx.x] = ex;
-      s_a[threadIdx.x] = ra;
-    }
-    if (threadIdx.x == 0) s_pre[nw] = tot;
-    __syncthreads();
-    for (uint32_t f0 = 0; f0 < tot; f0 += kAggStage) {
-      const uint32_t f1 = min(tot, f0 + (uint32_t)kAggStage), n = f1 - f0;
-      uint32_t si[kU];
-      float sv[kU];
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const uint32_t f = f0 + (uint32_t)(u * kNT) + threadIdx.x;
-        si[u] = 0xFFFFFFFFu;
-        sv[u] = 0.0f;
-        if (f < f1) {
-          const int w = agg_worker_of(s_pre, nw, f);
-          const size_t j = (size_t)(w0 + w) * K + s_a[w] + (f - s_pre[w]);
-          si[u] = idx[j];
-          sv[u] = val[j];
+  };
+  prefetch(blockIdx.x);
+  for (uint32_t tau = blockIdx.x; tau < (uint32_t)nt; tau += gridDim.x) {
+    const uint32_t lo = tau * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
+    for (uint32_t x = threadIdx.x; x < kAggTile; x += kNT) acc[x] = 0.0f;
+    for (int w0 = 0; w0 < W; w0 += kAggW) {
+      const int nw = min(kAggW, W - w0);
+      uint32_t ra = 0, cnt = 0;
+      if ((int)threadIdx.x < nw) {
+        uint32_t rb;
+        if (w0 == 0) {
+          ra = min(pa, (uint32_t)K);
+          rb = min(pb, (uint32_t)K);
+        } else {
+          const uint32_t* ts = tile_start + (size_t)(w0 + threadIdx.x) * (nt + 1);
+          ra = min(ts[tau], (uint32_t)K);
+          rb = min(ts[tau + 1], (uint32_t)K);
         }
-        if (si[u] < lo || si[u] >= hi) si[u] = 0xFFFFFFFFu;  // outside the tile: ignored
+        cnt = rb > ra ? rb - ra : 0u;
       }
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        s_i[u * kNT + threadIdx.x] = si[u];
-        s_v[u * kNT + threadIdx.x] = sv[u];
+      if (w0 == 0) prefetch(tau + gridDim.x);
+      uint32_t tot;
+      const uint32_t ex = block_excl_scan<kNT>(cnt, lds, tot);
+      if ((int)threadIdx.x < nw) {
+        s_pre[threadIdx.x] = ex;
+        s_a[threadIdx.x] = ra;
       }
-      for (uint32_t x = threadIdx.x; x < kAggTile / 32; x += kNT) {
-        s_seen[x] = 0;
-        s_multi[x] = 0;
-      }
+      if (threadIdx.x == 0) s_pre[nw] = tot;
       __syncthreads();
+      for (uint32_t f0 = 0; f0 < tot; f0 += kAggStage) {
+        const uint32_t f1 = min(tot, f0 + (uint32_t)kAggStage);
+        uint32_t si[kU];
+        float sv[kU];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        if (si[u] != 0xFFFFFFFFu) {
-          const uint32_t x = si[u] - lo, bit = 1u << (x & 31u);
-          if (atomicOr(&s_seen[x >> 5], bit) & bit) atomicOr(&s_multi[x >> 5], bit);
+        for (int u = 0; u < kU; ++u) {
+          const uint32_t f = f0 + (uint32_t)(u * kNT) + threadIdx.x;
+          si[u] = 0xFFFFFFFFu;
+          sv[u] = 0.0f;
+          if (f < f1) {
+            const int w = agg_worker_of(s_pre, nw, f);
+            const size_t j = (size_t)(w0 + w) * K + s_a[w] + (f - s_pre[w]);
+            si[u] = idx[j];
+            sv[u] = val[j];
+          }
+          if (si[u] < lo || si[u] >= hi) si[u] = 0xFFFFFFFFu;  // outside the tile: ignored
         }
-      }
-      __syncthreads();
-      // single entries add at once; shared ones are compacted in staged order
-      uint32_t shared_u = 0;
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        if (si[u] != 0xFFFFFFFFu) {
-          const uint32_t x = si[u] - lo;
-          if ((s_multi[x >> 5] >> (x & 31u)) & 1u) shared_u |= 1u << u;
-          else acc[x] += sv[u];
+        for (int u = 0; u < kU; ++u) {
+          s_i[u * kNT + threadIdx.x] = si[u];
+          s_v[u * kNT + threadIdx.x] = sv[u];
         }
-      }
-      uint32_t ctot;
-      const uint32_t cex = block_excl_scan<kNT>((shared_u & 1u) | ((shared_u >> 1) << 16), lds, ctot);
-      const uint32_t n0 = ctot & 0xFFFFu, cn = n0 + (ctot >> 16);
-      if (shared_u & 1u) s_cf[cex & 0xFFFFu] = threadIdx.x;
-      if (shared_u & 2u) s_cf[n0 + (cex >> 16)] = kNT + threadIdx.x;
-      __syncthreads();
-      if (cn > 0 && cn <= (uint32_t)kAggScanMax) {
-        if (threadIdx.x < cn) {
-          const uint32_t i = s_i[s_cf[threadIdx.x]];
-          bool first = true;
-          for (uint32_t e = 0; e < threadIdx.x; ++e) first = first && s_i[s_cf[e]] != i;
-          if (first) {
-            float sum = acc[i - lo];
-            for (uint32_t e = threadIdx.x; e < cn; ++e)
-              if (s_i[s_cf[e]] == i) sum += s_v[s_cf[e]];
-            acc[i - lo] = sum;
+        for (uint32_t x = threadIdx.x; x < kAggTile / 32; x += kNT) {
+          s_seen[x] = 0;
+          s_multi[x] = 0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          if (si[u] != 0xFFFFFFFFu) {
+            const uint32_t x = si[u] - lo, bit = 1u << (x & 31u);
+            if (atomicOr(&s_seen[x >> 5], bit) & bit) atomicOr(&s_multi[x >> 5], bit);
           }
         }
-      } else if (cn > 0) {
-        const int wa = agg_worker_of(s_pre, nw, f0), wb = agg_worker_of(s_pre, nw, f1 - 1);
-        for (int w = wa; w <= wb; ++w) {
-          const uint32_t ea = lower_bound_u32(s_cf, cn, max(s_pre[w], f0) - f0);
-          const uint32_t eb = lower_bound_u32(s_cf, cn, min(s_pre[w + 1], f1) - f0);
-          if (ea >= eb) continue;
-          for (uint32_t e = ea + threadIdx.x; e < eb; e += kNT) {
-            const uint32_t fe = s_cf[e];
-            acc[s_i[fe] - lo] += s_v[fe];
+        __syncthreads();
+        // single entries add at once; shared ones are compacted in staged order
+        uint32_t shared_u = 0;
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          if (si[u] != 0xFFFFFFFFu) {
+            const uint32_t x = si[u] - lo;
+            if ((s_multi[x >> 5] >> (x & 31u)) & 1u) shared_u |= 1u << u;
+            else acc[x] += sv[u];
           }
-          __syncthreads();
         }
+        uint32_t ctot;
+        const uint32_t cex = block_excl_scan<kNT>((shared_u & 1u) | ((shared_u >> 1) << 16), lds, ctot);
+        const uint32_t n0 = ctot & 0xFFFFu, cn = n0 + (ctot >> 16);
+        if (shared_u & 1u) s_cf[cex & 0xFFFFu] = threadIdx.x;
+        if (shared_u & 2u) s_cf[n0 + (cex >> 16)] = kNT + threadIdx.x;
+        __syncthreads();
+        if (cn > 0 && cn <= (uint32_t)kAggScanMax) {
+          if (threadIdx.x < cn) {
+            const uint32_t i = s_i[s_cf[threadIdx.x]];
+            bool first = true;
+            for (uint32_t e = 0; e < threadIdx.x; ++e) first = first && s_i[s_cf[e]] != i;
+            if (first) {
+              float sum = acc[i - lo];
+              for (uint32_t e = threadIdx.x; e < cn; ++e)
+                if (s_i[s_cf[e]] == i) sum += s_v[s_cf[e]];
+              acc[i - lo] = sum;
+            }
+          }
+        } else if (cn > 0) {
+          const int wa = agg_worker_of(s_pre, nw, f0), wb = agg_worker_of(s_pre, nw, f1 - 1);
+          for (int w = wa; w <= wb; ++w) {
+            const uint32_t ea = lower_bound_u32(s_cf, cn, max(s_pre[w], f0) - f0);
+            const uint32_t eb = lower_bound_u32(s_cf, cn, min(s_pre[w + 1], f1) - f0);
+            if (ea >= eb) continue;
+            for (uint32_t e = ea + threadIdx.x; e < eb; e += kNT) {
+              const uint32_t fe = s_cf[e];
+              acc[s_i[fe] - lo] += s_v[fe];
+            }
+            __syncthreads();
+          }
+        }
+        __syncthreads();  // staging buffers are rewritten by the next pass
       }
-      __syncthreads();  // staging buffers are rewritten by the next pass
     }
-  }
 #pragma unroll
-  for (int r = 0; r < kAggRounds; ++r) {
-    const uint32_t x = (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const uint32_t i0 = lo + x;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float v[4];
+    for (int r = 0; r < kAggRounds; ++r) {
+      const uint32_t x = (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const uint32_t i0 = lo + x;
+      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+      float v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(acc[x + q], (float)W) : acc[x + q];
-    store4(out, i0, nv, v);
+      for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(acc[x + q], W, pow2, inv) : acc[x + q];
+      store4(out, i0, nv, v);
+    }
+    __syncthreads();  // the next tile clears acc
   }
 }
 
-// One workgroup per data tile, sums held in registers (each thread its kRounds float4 groups).
-// Per pass over up to kAggSegs segments of the tile and a group of workers, the segments' sizes
-// and the workers' block starts come in one round trip; then, for every worker in order and every
-// segment, the run pieces that meet the tile are added element by element (each element gets at
-// most one value per worker, and the segments of a tile are disjoint).
+// Persistent workgroups, each walking half data tiles (blockIdx.x, then every gridDim.x-th), sums
+// held in registers (each thread its kRounds / 2 float4 groups).  Per pass over up to kAggSegs
+// segments of the tile and a group of workers, the segments' sizes and the workers' block starts
+// come in one round trip, and stay cached while consecutive tiles lie in the same segments with
+// all workers in one group (the common case: a workgroup loads them once).  Then, for every worker
+// in order and every segment, the run pieces that meet the tile are added element by element
+// (each element gets at most one value per worker, and the segments of a tile are disjoint).
 constexpr int kAggSegs = 64;
 
 __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t K, const uint32_t* start,
                                                    const float* val, int average, float* out) {
   __shared__ uint32_t s_st[kAggStarts];
   __shared__ uint32_t s_seg[4][kAggSegs];  // o, n, k, P of the pass's segments
-  const uint32_t c = blockIdx.x;
-  const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
-  const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-  float a[kRounds][4];
+  int c_sf = -1, c_sl = -1;                // segments whose starts s_st holds (one pass, one group)
+  const bool pow2 = (W & (W - 1)) == 0;
+  const float inv = 1.0f / (float)W;  // exact when W is a power of two
+  // half tiles: 16 sums per thread keep the register count low, so many workgroups stay
+  // resident and their stores keep HBM busy
+  constexpr int kR = kRounds / 2;
+  constexpr uint32_t kHalf = kTile / 2;
+  for (uint32_t h = blockIdx.x; h < 2u * (uint32_t)T.nchunks; h += gridDim.x) {
+    const uint32_t c = h >> 1;
+    const uint32_t lo = h * kHalf, hi = min((uint32_t)T.d, lo + kHalf);
+    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];  // the tile's segments cover the half
+    if (lo >= hi) continue;
+    float a[kR][4];
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r)
+    for (int r = 0; r < kR; ++r)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
-  for (int l0 = sf; l0 <= sl; l0 += kAggSegs) {
-    const int ns = min(kAggSegs, sl - l0 + 1);
-    const int gw = kAggStarts / ns;  // workers per group
-    for (int w0 = 0; w0 < W; w0 += gw) {
-      const int nw = min(gw, W - w0);
-      if ((int)threadIdx.x < ns) {
-        const int l = l0 + threadIdx.x;
-        s_seg[0][threadIdx.x] = (uint32_t)T.seg_off[l];
-        s_seg[1][threadIdx.x] = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
-        s_seg[2][threadIdx.x] = (uint32_t)T.seg_k[l];
-        s_seg[3][threadIdx.x] = (uint32_t)T.seg_P[l];
-      }
-      for (int x = threadIdx.x; x < nw * ns; x += kNT) {
-        const int w = x / ns, l = l0 + x % ns;
-        const uint32_t n = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
-        s_st[x] = start[(size_t)(w0 + w) * T.L + l] % n;
-      }
-      __syncthreads();
-      for (int w = 0; w < nw; ++w) {
-        const float* v = val + (size_t)(w0 + w) * K;
-        for (int x = 0; x < ns; ++x) {
-          const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], P = s_seg[3][x];
-          const uint32_t s = s_st[w * ns + x];
-          // run piece 1: global [o + s, o + min(s + k, n)), t = i - o - s;
-          // run piece 2: global [o, o + s + k - n), t = i - o + n - s
-          const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + min(s + k, n));
-          const uint32_t a2 = max(lo, o), b2 = s + k > n ? min(hi, o + (s + k - n)) : 0u;
-          if (a1 >= b1 && a2 >= b2) continue;
+      for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
+    for (int l0 = sf; l0 <= sl; l0 += kAggSegs) {
+      const int ns = min(kAggSegs, sl - l0 + 1);
+      const int gw = kAggStarts / ns;  // workers per group
+      const bool one = l0 == sf && sl - sf < kAggSegs && W <= gw;  // whole tile in one pass and group
+      for (int w0 = 0; w0 < W; w0 += gw) {
+        const int nw = min(gw, W - w0);
+        if (!(one && c_sf == sf && c_sl == sl)) {
+          __syncthreads();  // the previous pass is done with s_st / s_seg
+          if ((int)threadIdx.x < ns) {
+            const int l = l0 + threadIdx.x;
+            s_seg[0][threadIdx.x] = (uint32_t)T.seg_off[l];
+            s_seg[1][threadIdx.x] = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
+            s_seg[2][threadIdx.x] = (uint32_t)T.seg_k[l];
+            s_seg[3][threadIdx.x] = (uint32_t)T.seg_P[l];
+          }
+          for (int x = threadIdx.x; x < nw * ns; x += kNT) {
+            const int w = x / ns, l = l0 + x % ns;
+            const uint32_t n = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
+            s_st[x] = start[(size_t)(w0 + w) * T.L + l] % n;
+          }
+          __syncthreads();
+          c_sf = one ? sf : -1;
+          c_sl = one ? sl : -1;
+        }
+        // workers of the group with a run piece in this tile, 64 at a time: each wave finds them
+        // with a ballot (lane j tests worker wb + j) and visits them in ascending order
+        for (int wb = 0; wb < nw; wb += 64) {
+          const int wl = wb + (int)(threadIdx.x & 63);
+          bool hit = false;
+          if (wl < nw) {
+            for (int x = 0; x < ns; ++x) {
+              const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], s = s_st[wl * ns + x];
+              hit = hit || (max(lo, o + s) < min(hi, o + min(s + k, n))) ||
+                    (s + k > n && max(lo, o) < min(hi, o + (s + k - n)));
+            }
+          }
+          uint64_t todo = __ballot(hit);
+          while (todo) {
+            const int w = wb + __ffsll((long long)todo) - 1;
+            todo &= todo - 1;
+            const float* v = val + (size_t)(w0 + w) * K;
+            for (int x = 0; x < ns; ++x) {
+              const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], P = s_seg[3][x];
+              const uint32_t s = s_st[w * ns + x];
+              // run piece 1: global [o + s, o + min(s + k, n)), t = i - o - s;
+              // run piece 2: global [o, o + s + k - n), t = i - o + n - s
+              const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + min(s + k, n));
+              const uint32_t a2 = max(lo, o), b2 = s + k > n ? min(hi, o + (s + k - n)) : 0u;
+              if (a1 >= b1 && a2 >= b2) continue;
 #pragma unroll
-          for (int r = 0; r < kRounds; ++r) {
-            const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+              for (int r = 0; r < kR; ++r) {
+                const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const uint32_t i = i0 + q;
-              if (i >= a1 && i < b1) a[r][q] += v[P + (i - o - s)];
-              else if (i >= a2 && i < b2) a[r][q] += v[P + (i - o + n - s)];
+                for (int q = 0; q < 4; ++q) {
+                  const uint32_t i = i0 + q;
+                  if (i >= a1 && i < b1) a[r][q] += v[P + (i - o - s)];
+                  else if (i >= a2 && i < b2) a[r][q] += v[P + (i - o + n - s)];
+                }
+              }
             }
           }
         }
       }
-      __syncthreads();  // s_st and s_seg are rewritten by the next group
     }
-  }
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float v[4];
+    for (int r = 0; r < kR; ++r) {
+      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+      float v[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = average ? __fdiv_rn(a[r][q], (float)W) : a[r][q];
-    store4(out, i0, nv, v);
+      for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(a[r][q], W, pow2, inv) : a[r][q];
+      store4(out, i0, nv, v);
+    }
   }
 }
 

@@ -280,6 +280,21 @@ bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
     if (_rc != EF_OK) return _rc; \
   } while (0)
 
+// Workgroups that fit on the device at once for a persistent kernel (computed once per kernel;
+// every GPU this library drives is the same part).
+template <typename K>
+unsigned resident_blocks(K kernel) {
+  static const unsigned n = [&] {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, kNT, 0) != hipSuccess || cus < 1 || per < 1)
+      return 1024u;
+    return (unsigned)(cus * per);
+  }();
+  return n;
+}
+
 int check_bound(const ef_layout* L) {
   if (!L || !L->bound) return EF_EINVAL;
   return EF_OK;
@@ -676,12 +691,13 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     const int32_t nt = agg_tiles(L->d);
     EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts);
     EF_TRY(launched());
-    EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), blk, 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average,
-              out);
+    const unsigned g = std::min<unsigned>((unsigned)nt, resident_blocks(k_agg_sparse));
+    EF_LAUNCH(k_agg_sparse, dim3(g), blk, 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average, out);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
-    EF_LAUNCH(k_agg_block, grid, blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
+    const unsigned g = std::min<unsigned>(2u * (unsigned)L->nchunks, resident_blocks(k_agg_block));
+    EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
     return launched();
   }
   return EF_EINVAL;
