@@ -25,7 +25,7 @@ namespace efs {
 
 constexpr int kNT = 256;                      // threads per workgroup of the streaming kernels
 constexpr int kSelNT = 1024;                  // threads per workgroup of the per-segment kernels
-constexpr uint32_t kTile = 8192;              // data elements per chunk
+constexpr uint32_t kTile = 4096;              // data elements per tile (4 float4 groups per thread)
 constexpr int kRounds = kTile / (4 * kNT);    // float4 groups per thread per chunk
 constexpr int kHBins = 2048;                  // LDS histogram bins (11 bits per radix level)
 constexpr int kResWords = 16;                // per-segment selection record (uint32 words)

@@ -459,8 +459,8 @@ __global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_
   }
 }
 
-// Persistent workgroups, each walking half data tiles (blockIdx.x, then every gridDim.x-th), sums
-// held in registers (each thread its kRounds / 2 float4 groups).  Per pass over up to kAggSegs
+// Persistent workgroups, each walking data tiles (blockIdx.x, then every gridDim.x-th), sums held
+// in registers (each thread its kRounds float4 groups; few enough registers for 8 waves per SIMD).  Per pass over up to kAggSegs
 // segments of the tile and a group of workers, the segments' sizes and the workers' block starts
 // come in one round trip, and stay cached while consecutive tiles lie in the same segments with
 // all workers in one group (the common case: a workgroup loads them once).  Then, for every worker
@@ -475,15 +475,10 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
   int c_sf = -1, c_sl = -1;                // segments whose starts s_st holds (one pass, one group)
   const bool pow2 = (W & (W - 1)) == 0;
   const float inv = 1.0f / (float)W;  // exact when W is a power of two
-  // half tiles: 16 sums per thread keep the register count low, so many workgroups stay
-  // resident and their stores keep HBM busy
-  constexpr int kR = kRounds / 2;
-  constexpr uint32_t kHalf = kTile / 2;
-  for (uint32_t h = blockIdx.x; h < 2u * (uint32_t)T.nchunks; h += gridDim.x) {
-    const uint32_t c = h >> 1;
-    const uint32_t lo = h * kHalf, hi = min((uint32_t)T.d, lo + kHalf);
-    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];  // the tile's segments cover the half
-    if (lo >= hi) continue;
+  constexpr int kR = kRounds;
+  for (uint32_t c = blockIdx.x; c < (uint32_t)T.nchunks; c += gridDim.x) {
+    const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
+    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
     float a[kR][4];
 #pragma unroll
     for (int r = 0; r < kR; ++r)

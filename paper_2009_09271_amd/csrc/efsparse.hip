@@ -696,7 +696,7 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
-    const unsigned g = std::min<unsigned>(2u * (unsigned)L->nchunks, resident_blocks(k_agg_block));
+    const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks(k_agg_block));
     EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
     return launched();
   }

@@ -19,6 +19,7 @@ LAYOUTS = [
     [0, 1, 5, 64, 65, 300, 301, 10007, 10008, 40000],
     [0, 3, 8190, 8195, 16384, 16385, 16386, 30000],
     [0, 2, 6, 10, 14, 8200, 8204, 8300, 70000],
+    [0, 4095, 4096, 4097, 8191, 12289, 20000],
 ]
 
 
