@@ -83,8 +83,8 @@ extern "C" {
 /* tuning knobs for ef_layout_tune: they size the candidate sets and change speed only, never
    results (a segment whose candidates cannot contain the answer takes an exact whole-segment
    path) */
-#define EF_TUNE_RANDK_SIGMA 0  /* random-k: candidate bound, standard deviations above k (default 10) */
-#define EF_TUNE_RANDK_EXTRA 1  /* random-k: candidate bound, constant margin (default 64) */
+#define EF_TUNE_RANDK_SIGMA 0  /* random-k: candidate bound, standard deviations above k (default 6) */
+#define EF_TUNE_RANDK_EXTRA 1  /* random-k: candidate bound, constant margin (default 32) */
 #define EF_TUNE_TOPK_SIGMA 2   /* top-k: sampled threshold margin in standard deviations (default 6) */
 #define EF_TUNE_TOPK_EXTRA 3   /* top-k: sampled threshold margin, constant part (default 8) */
 

@@ -70,6 +70,8 @@ struct Tables {
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row
   int32_t d, L, nchunks, nrows, nruns;
+  int32_t rk_direct;           // random-k: k_stream_sel counts the certain winners and lists the
+                               // undecided candidates of every row; k_select gathers the lists
 };
 
 // ---------------------------------------------------------------------------------------------
@@ -163,6 +165,25 @@ __device__ __forceinline__ void store4(float* p, uint32_t i0, int nv, const floa
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (q < nv) p[i0 + q] = v[q];
+  }
+}
+
+// Unconditional variants for groups known to be whole.  Keeping the masked forms (which branch
+// on the group's extent) out of the common path lets every load of a thread be issued before
+// the first wait.
+__device__ __forceinline__ void load4f(const float* p, uint32_t i0, float v[4]) {
+  const f4 x = __builtin_nontemporal_load(reinterpret_cast<const f4*>(p + i0));
+  v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+}
+
+template <int GDT>
+__device__ __forceinline__ void load4gf(const void* g, uint32_t i0, float v[4]) {
+  if constexpr (GDT == 0) {
+    load4f(reinterpret_cast<const float*>(g), i0, v);
+  } else {
+    const u2v x = __builtin_nontemporal_load(reinterpret_cast<const u2v*>(reinterpret_cast<const uint16_t*>(g) + i0));
+    v[0] = bf16_to_f32(x.x & 0xFFFFu); v[1] = bf16_to_f32(x.x >> 16);
+    v[2] = bf16_to_f32(x.y & 0xFFFFu); v[3] = bf16_to_f32(x.y >> 16);
   }
 }
 
@@ -267,6 +288,33 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* lds, u
   __syncthreads();
   total = tot;
   return off + inc - v;
+}
+
+// Exclusive scans of NV counters at once (one pair of barriers); `lds` holds NV * NT/64 words.
+template <int NT, int NV>
+__device__ __forceinline__ void block_excl_scan_n(const uint32_t (&v)[NV], uint32_t* lds, uint32_t (&ex)[NV],
+                                                  uint32_t (&total)[NV]) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  uint32_t inc[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    inc[j] = wave_incl_scan(v[j]);
+    if (lane == 63) lds[j * (NT / 64) + wid] = inc[j];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) {
+      const uint32_t x = lds[j * (NT / 64) + w];
+      off += (w < wid) ? x : 0u;
+      tot += x;
+    }
+    ex[j] = off + inc[j] - v[j];
+    total[j] = tot;
+  }
+  __syncthreads();
 }
 
 // Scanning an LDS histogram from its highest bin down, find the bin in which the running count

@@ -10,14 +10,18 @@
 //   k_sample_select  at most kSampleMax elements, else runs spread over it); per segment either
 //                    the exact winner rule (small segments) or a candidate threshold set so that
 //                    the candidates very likely number at least k_l.
-//   k_randk_init     random-k only: clears the per-segment candidate histograms.
 //   k_stream_sel     per row: fused accumulate (acc = g + e, written to e), candidate test (top-k:
 //                    the rule above; random-k: Philox key < tau_l, a binomial bound on k_l), the
-//                    row's candidates in index order to its slot, and a histogram of them.
-//   k_resolve        per segment: the histogram bin holding the k_l-th best candidate.
-//   k_collect        per row: candidates above that bin are counted, those inside it are listed.
+//                    row's candidates in index order to its slot, and a histogram of them (top-k).
+//                    Random-k on layouts whose rows and key window fit k_select's LDS: also the
+//                    row's certain winners (key < ulo_l) counted and its undecided candidates
+//                    listed, so that k_collect is not needed.
+//   k_resolve        top-k, per segment: the histogram bin holding the k_l-th best candidate.
+//   k_collect        per row: candidates above that bin (random-k: key below ulo_l) are counted,
+//                    the undecided ones are listed.
 //   k_select         per segment: the exact threshold among the listed candidates, then the
-//                    message offset of every row.
+//                    message offset of every row.  Layouts with a very large k_l instead count
+//                    and scan the rows' winners in k_rowcount and k_rowscan.
 //   k_emit           per row: the winners in index order to the message, e = +0 there.
 // A segment with fewer than k_l candidates is resolved exactly over all of its elements by
 // k_select.  Block-random-k is one fused streaming pass (k_randblock_step).  The aggregate
@@ -47,6 +51,13 @@ struct WSel {
 };
 
 __device__ __forceinline__ uint32_t* res_of(const WSel& w, int l) { return w.res + (size_t)l * kResWords; }
+
+// Random-k, direct lists: row r's undecided candidates as (key', index) pairs in the list_idx slot
+// of the row (kTile words hold kRowPairs pairs).
+constexpr uint32_t kRowPairs = kTile / 2;
+__device__ __forceinline__ uint2* row_pairs(const WSel& w, uint32_t row) {
+  return reinterpret_cast<uint2*>(w.list_idx + (size_t)row * kTile);
+}
 constexpr int kLineWords = 32;  // 128-byte L2 line: counters hit by many atomics get a line each
 __device__ __forceinline__ uint32_t* lcnt_of(const WSel& w, int l, uint32_t c) {
   return w.lcnt + ((size_t)l * kSubLists + c) * kLineWords;
@@ -148,54 +159,54 @@ __device__ __forceinline__ uint32_t run_pos(const RunSeg& r, uint32_t i) {
 }
 
 // Fused worker step: acc = g + e; val[P_l + t] = acc on the run; e' = +0 on the run, acc elsewhere.
+// One float4 group per thread (kRbTile elements per workgroup): short-lived workgroups keep the
+// end of the grid short, where a pure streaming pass otherwise loses bandwidth.
+constexpr uint32_t kRbTile = 4u * kNT;
 template <int GDT>
 __global__ __launch_bounds__(kNT) void k_randblock_step(Tables T, const void* g, float* e, uint32_t s0,
                                                         uint32_t s1, uint32_t step, uint32_t* start,
                                                         float* val) {
-  const uint32_t c = blockIdx.x;
-  const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
+  const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)T.d, lo + kRbTile);
+  const uint32_t c = lo / kTile;  // the data tile holding this group: its first and last segment
   const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-  const bool uni = sf == sl;
+  const uint32_t i0 = lo + threadIdx.x * 4u;
+  const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+  float gv[4], ev[4];
+  if (hi - lo == kRbTile) {  // whole group (every workgroup but the last)
+    load4gf<GDT>(g, i0, gv);
+    load4f(e, i0, ev);
+  } else {
+    load4g<GDT>(g, i0, nv, gv);
+    load4(e, i0, nv, ev);
+  }
   RunSeg rs = run_seg(T, sf, step, s0, s1);
   int cur = sf;
-  float gv[kRounds][4], ev[kRounds][4];
+  float out[4];
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    load4g<GDT>(g, i0, nv, gv[r]);
-    load4(e, i0, nv, ev[r]);
-  }
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float out[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float a = gv[r][q] + ev[r][q];
-      out[q] = a;
-      if (q < nv) {
-        const uint32_t i = i0 + q;
-        if (!uni) {
-          const int l = seg_of(i, sf, sl, T.seg_off);
-          if (l != cur) {
-            rs = run_seg(T, l, step, s0, s1);
-            cur = l;
-          }
-        }
-        const uint32_t t = run_pos(rs, i);
-        if (t < rs.k) {
-          val[rs.P + t] = a;
-          out[q] = 0.0f;
+  for (int q = 0; q < 4; ++q) {
+    const float a = gv[q] + ev[q];
+    out[q] = a;
+    if (q < nv) {
+      const uint32_t i = i0 + q;
+      if (sf != sl) {
+        const int l = seg_of(i, sf, sl, T.seg_off);
+        if (l != cur) {
+          rs = run_seg(T, l, step, s0, s1);
+          cur = l;
         }
       }
+      const uint32_t t = run_pos(rs, i);
+      if (t < rs.k) {
+        val[rs.P + t] = a;
+        out[q] = 0.0f;
+      }
     }
-    store4(e, i0, nv, out);
   }
-  // start of every segment that begins in this chunk
+  store4(e, i0, nv, out);
+  // start of every segment that begins in this group
   for (int l = sf + (int)threadIdx.x; l <= sl; l += kNT) {
-    if ((uint32_t)T.seg_off[l] >= lo)
+    const uint32_t ol = (uint32_t)T.seg_off[l];
+    if (ol >= lo && ol < hi)
       start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
   }
 }
@@ -578,6 +589,7 @@ constexpr uint32_t kListLds = 8192;    // listed candidates held in LDS by k_sel
 constexpr uint32_t kRowsLds = 16384;   // rows per segment whose list additions k_select counts in LDS
 constexpr uint32_t kRankList = 256;    // lists up to this size are ranked directly (no radix levels)
 constexpr uint32_t kBigK = 1u << 20;   // layouts with a k_l this large count row winners in parallel
+constexpr uint32_t kSelPer = 8;        // rows per k_select thread held in registers
 constexpr uint32_t kHistDirect = 32;   // rows with more candidates histogram them in LDS first
 constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
 constexpr uint32_t kDiagCount = 4u;    // diagnostics: the row counts of a segment did not add up to k_l
@@ -930,6 +942,9 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
                                                     uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
   __shared__ uint32_t wt[kRounds][kNT / 64];
   __shared__ uint32_t s_hist[KIND == 0 ? kHBins : 1];
+  __shared__ uint32_t s_kk[KIND == 1 ? kTile : 1];  // random-k: the candidates' keys, by element
+  __shared__ uint32_t wc[kNT / 64];  // random-k, direct lists: certain winners per wavefront
+  __shared__ uint32_t s_und;         // random-k, direct lists: undecided candidates listed so far
   const uint32_t row = blockIdx.x;
   const int l = T.row_seg[row];
   const uint32_t o = (uint32_t)T.seg_off[l], e_ = (uint32_t)T.seg_off[l + 1];
@@ -937,8 +952,9 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
   const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   uint32_t* R = res_of(ws, l);
-  uint32_t mode = 1, A = 0, IA = 0, sh = 0;
+  uint32_t mode = 1, A = 0, IA = 0, sh = 0, ulo = 0;
   uint64_t tau = 0;
+  const bool direct = KIND == 1 && T.rk_direct;
   if constexpr (KIND == 0) {
     mode = R[R_MODE];
     A = R[R_A];
@@ -946,21 +962,32 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
     sh = R[R_SH];
   } else {
     tau = T.seg_tau[l];
+    ulo = T.seg_ulo[l];
     // the list counter of k_collect starts from zero (this kernel completes before it runs)
-    if (row == (uint32_t)T.seg_cbase[l] && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
+    if (!direct && row == (uint32_t)T.seg_cbase[l] && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
   }
 
   float v[kRounds][4];
   uint32_t vm[kRounds];
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) vm[r] = group_mask(tb + (uint32_t)(r * kNT + threadIdx.x) * 4u, lo, hi);
+  const bool whole = lo == tb && hi == tb + kTile;  // the row is the whole tile (uniform)
   if constexpr (FUSED) {
     float gv[kRounds][4];
+    if (whole) {
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      load4gm<GDT>(g, i0, vm[r], gv[r]);
-      load4m(src, i0, vm[r], v[r]);
+      for (int r = 0; r < kRounds; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+        load4gf<GDT>(g, i0, gv[r]);
+        load4f(src, i0, v[r]);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+        load4gm<GDT>(g, i0, vm[r], gv[r]);
+        load4m(src, i0, vm[r], v[r]);
+      }
     }
 #pragma unroll
     for (int r = 0; r < kRounds; ++r) {
@@ -971,11 +998,17 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
     }
   } else {
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) load4m(src, tb + (uint32_t)(r * kNT + threadIdx.x) * 4u, vm[r], v[r]);
+    for (int r = 0; r < kRounds; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      if (whole) load4f(src, i0, v[r]);
+      else load4m(src, i0, vm[r], v[r]);
+    }
   }
   // candidate flags; wave-level prefixes through ballots, one barrier for the whole row
   uint32_t mask[kRounds], lpre[kRounds];
   uint32_t kk[kRounds][4];
+  uint32_t ncert = 0;  // random-k, direct lists: certain winners of this wavefront (uniform)
+  uint32_t cbits = 0;  // random-k, direct lists: bit 4r+q marks a certain winner (key below ulo)
 #pragma unroll
   for (int r = 0; r < kRounds; ++r) {
     const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
@@ -992,17 +1025,22 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
         if (vm[r]) x = philox(make_uint4((i0 - o) >> 2, 0u, step, kRandkTag | (uint32_t)l), s0, s1);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          kk[r][q] = ~word(x, q);
-          if (((vm[r] >> q) & 1u) && (uint64_t)word(x, q) < tau) mk |= 1u << q;
+          if (((vm[r] >> q) & 1u) && (uint64_t)word(x, q) < tau) {
+            mk |= 1u << q;
+            s_kk[(r * kNT + threadIdx.x) * 4 + q] = ~word(x, q);
+          }
+          if (((vm[r] >> q) & 1u) && word(x, q) < ulo) cbits |= 1u << (4 * r + q);
         }
       } else {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          kk[r][q] = 0u;
           if ((vm[r] >> q) & 1u) {
             const uint32_t u = randk_key(i0 + q - o, (uint32_t)l, step, s0, s1);
-            kk[r][q] = ~u;
-            if ((uint64_t)u < tau) mk |= 1u << q;
+            if ((uint64_t)u < tau) {
+              mk |= 1u << q;
+              s_kk[(r * kNT + threadIdx.x) * 4 + q] = ~u;
+            }
+            if (u < ulo) cbits |= 1u << (4 * r + q);
           }
         }
       }
@@ -1017,6 +1055,14 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
     }
     lpre[r] = pre;
     if (lane == 0) wt[r][wid] = tot;
+    if (direct) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ncert += (uint32_t)__popcll(__ballot((cbits >> (4 * r + q)) & 1u));
+    }
+  }
+  if (direct) {
+    if (lane == 0) wc[wid] = ncert;
+    if (threadIdx.x == 0) s_und = 0;
   }
   __syncthreads();
   uint32_t base = 0;
@@ -1034,10 +1080,20 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if ((mask[r] >> q) & 1u) {
+          uint32_t key;
+          if constexpr (KIND == 0) key = kk[r][q];
+          else key = s_kk[(r * kNT + threadIdx.x) * 4 + q];
           cidx[pos] = i0 + q;
           cval[pos] = v[r][q];
-          ckey[pos] = kk[r][q];
+          ckey[pos] = key;
           ++pos;
+          if (direct && !((cbits >> (4 * r + q)) & 1u)) {
+            // random-k, direct lists: an undecided candidate ([ulo, tau)) joins the row's list as
+            // a (key', index) pair; a row with more than kRowPairs of them sends the segment down
+            // the exact path (k_select sees the count)
+            const uint32_t p = atomicAdd(&s_und, 1u);
+            if (p < kRowPairs) row_pairs(ws, row)[p] = make_uint2(key, i0 + q);
+          }
         }
       }
     }
@@ -1045,6 +1101,13 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
     for (int w = 0; w < kNT / 64; ++w) base += wt[r][w];
   }
   if (threadIdx.x == 0) ws.counts[row] = base;
+  if (direct && threadIdx.x == 0) {
+    // random-k, direct lists: the row's certain winners (key below ulo)
+    uint32_t c = 0;
+#pragma unroll
+    for (int w = 0; w < kNT / 64; ++w) c += wc[w];
+    ws.rcnt[row] = c;
+  }
   if constexpr (KIND == 0) {
     if (mode == 0 && base) {
       uint32_t* gh = ws.hist + ((size_t)l * kHCopies + (row % kHCopies)) * kHBins;
@@ -1292,9 +1355,9 @@ template <int KIND, bool BIG>
 __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const float* data, float* e_zero,
                                                    uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1,
                                                    uint32_t step) {
-  constexpr uint32_t kPer = 8;  // rows per thread held in registers (more are re-read)
+  constexpr uint32_t kPer = kSelPer;  // rows per thread held in registers (more are re-read)
   __shared__ uint32_t hist[kHBins];
-  __shared__ uint32_t lds[2 * kSelNT / 64];
+  __shared__ uint32_t lds[3 * kSelNT / 64];
   __shared__ uint32_t s_key[kListLds];
   __shared__ uint32_t s_idx[kListLds];
   __shared__ uint32_t s_add[kRowsLds];
@@ -1310,15 +1373,16 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
   const uint32_t* cc = ws.counts + r0;
   // round trip 1: record, sub-list sizes, row counts
   bool slow = false, listed = true;
-  uint32_t need = 0;
+  uint32_t need = 0, mU = 0, exU = 0;
   if constexpr (KIND == 0) {
     slow = R[R_SLOW] != 0;
     listed = R[R_MODE] == 0;
     need = R[R_NEED];
   }
+  const bool direct = KIND == 1 && T.rk_direct;
   uint32_t lc[kSubLists];
 #pragma unroll
-  for (int c = 0; c < kSubLists; ++c) lc[c] = *lcnt_of(ws, l, (uint32_t)c);
+  for (int c = 0; c < kSubLists; ++c) lc[c] = direct ? 0u : *lcnt_of(ws, l, (uint32_t)c);
   uint32_t cr[kPer], cn[kPer];
 #pragma unroll
   for (uint32_t x = 0; x < kPer; ++x) {
@@ -1328,21 +1392,26 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
   if constexpr (KIND == 1) {
     // random-k: the certain winners S (keys below ulo) and the candidates N decide whether the
     // window [ulo, tau) holds the k_l-th smallest key
-    uint32_t sS = 0, sN = 0;
+    // (direct lists: also the rows whose undecided candidates overflowed their pair slot)
+    uint32_t sv[3] = {0u, 0u, 0u};
 #pragma unroll
     for (uint32_t x = 0; x < kPer; ++x) {
-      sS += cr[x];
-      sN += cn[x];
+      sv[0] += cr[x];
+      sv[1] += cn[x];
+      sv[2] += cn[x] - cr[x] > kRowPairs ? 1u : 0u;
     }
     for (uint32_t x = a + kPer; x < b; ++x) {
-      sS += rc[x];
-      sN += cc[x];
+      sv[0] += rc[x];
+      sv[1] += cc[x];
     }
-    uint32_t S, N;
-    (void)block_excl_scan<kSelNT>(sS, lds, S);
-    (void)block_excl_scan<kSelNT>(sN, lds, N);
-    slow = S > kl || N < kl;
+    uint32_t ex[3], tot[3];
+    block_excl_scan_n<kSelNT, 3>(sv, lds, ex, tot);
+    const uint32_t S = tot[0], N = tot[1];
+    // direct lists: the rows' undecided candidates (counts - certain) must fit the LDS list
+    slow = S > kl || N < kl || (direct && (N - S > kListLds || tot[2] != 0));
     need = kl - S;
+    mU = N - S;
+    exU = ex[1] - ex[0];
     if (threadIdx.x == 0) {
       R[R_SLOW] = slow ? 1u : 0u;
       if (slow) atomicOr(ws.diag, kDiagSlowPath);
@@ -1408,9 +1477,41 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
       m += lc[c];
     }
     lk.M[kSubLists] = li.M[kSubLists] = m;
+    if (direct) m = mU;
     const bool in_lds = m <= kListLds;
-    // round trip 2: the listed candidates
-    if (in_lds) {
+    if (direct) {
+      // round trip 2 (direct lists; every row of the segment is one of kPer per thread): each
+      // thread notes (row, slot) of its rows' undecided candidates at their list positions, then
+      // the pairs are fetched, all loads in flight together
+      uint32_t f = exU;
+#pragma unroll
+      for (uint32_t x = 0; x < kPer; ++x) {
+        if (a + x < b)
+          for (uint32_t t = 0; t < cn[x] - cr[x]; ++t) s_key[f++] = ((a + x) << 12) | t;
+      }
+      __syncthreads();
+      for (uint32_t f0 = 0; f0 < m; f0 += (uint32_t)kSelNT * 4u) {
+        uint2 pr[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t fu = f0 + (uint32_t)u * kSelNT + threadIdx.x;
+          pr[u] = make_uint2(0u, 0u);
+          if (fu < m) {
+            const uint32_t rs = s_key[fu];
+            pr[u] = row_pairs(ws, r0 + (rs >> 12))[rs & 0xFFFu];
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const uint32_t fu = f0 + (uint32_t)u * kSelNT + threadIdx.x;
+          if (fu < m) {
+            s_key[fu] = pr[u].x;
+            s_idx[fu] = pr[u].y;
+          }
+        }
+      }
+    } else if (in_lds) {
+      // round trip 2: the listed candidates
       for (uint32_t f0 = 0; f0 < m; f0 += (uint32_t)kSelNT * 4u) {
         uint32_t kx[4], ix[4];
 #pragma unroll
@@ -1565,10 +1666,13 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws) {
   if (threadIdx.x == 0 && total != (uint32_t)T.seg_k[l]) atomicOr(ws.diag, kDiagCount);
 }
 
-// Per row: the winners, in index order, to the message at the row's offset; e = +0 there.
+// Per row, one wavefront each (kNT / 64 rows per workgroup, no workgroup barriers): the winners,
+// in index order, to the message at the row's offset; e = +0 there.
+constexpr uint32_t kEmitRows = kNT / 64;
 __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws, float* e_zero, uint32_t* out_idx, float* out_val) {
-  __shared__ uint32_t s_wt[kNT / 64];
-  const uint32_t row = blockIdx.x;
+  const uint32_t row = blockIdx.x * kEmitRows + (threadIdx.x >> 6);
+  if (row >= (uint32_t)T.nrows) return;
+  const int lane = threadIdx.x & 63;
   const int l = T.row_seg[row];
   const uint32_t* R = res_of(ws, l);
   if (R[R_SLOW]) return;
@@ -1578,9 +1682,8 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws, float* e_zero, 
   const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
   const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
   const float* cv = ws.cand_val + (size_t)row * kTile;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  for (uint32_t j0 = 0; j0 < cnt; j0 += kNT) {
-    const uint32_t j = j0 + threadIdx.x;
+  for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
+    const uint32_t j = j0 + (uint32_t)lane;
     const bool in = j < cnt;
     uint32_t k = 0, i = 0;
     float v = 0.0f;
@@ -1591,23 +1694,13 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws, float* e_zero, 
     }
     const bool win = in && (k > Tk || (k == Tk && i < IT));
     const uint64_t bw = __ballot(win);
-    if (lane == 0) s_wt[wid] = (uint32_t)__popcll(bw);
-    __syncthreads();
-    uint32_t wo = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) {
-      const uint32_t x = s_wt[w];
-      wo += w < wid ? x : 0u;
-      tot += x;
-    }
-    __syncthreads();
-    const uint32_t pos = base + wo + lanes_below(bw);
+    const uint32_t pos = base + lanes_below(bw);
     if (win && pos < pend) {
       out_idx[pos] = i;
       out_val[pos] = v;
       if (e_zero) e_zero[i] = 0.0f;
     }
-    base += tot;
+    base += (uint32_t)__popcll(bw);
   }
 }
 

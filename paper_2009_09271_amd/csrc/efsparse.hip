@@ -51,7 +51,7 @@ struct ef_layout {
   double density = 0;
   int64_t block = 1;
   std::vector<int64_t> off64;
-  double rk_sigma = 10.0, rk_extra = 64.0, tk_sigma = 6.0, tk_extra = 8.0;
+  double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0;
 
   std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg;
   std::vector<uint64_t> tau;
@@ -60,6 +60,7 @@ struct ef_layout {
   int32_t nchunks = 0, nrows = 0, nruns = 0;
   bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
   bool big = false;        // some k_l is large: row winners are counted by many workgroups
+  bool rk_direct = false;  // random-k: every segment's rows and expected window fit k_select's LDS
 
   Blob blob;
   size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
@@ -127,6 +128,16 @@ void ef_layout::build() {
   }
   K = P[n];
   big = *std::max_element(k.begin(), k.end()) >= kBigK;
+  // random-k without k_collect: every row of a segment is held by a k_select thread and the
+  // whole window [ulo, tau) fits k_select's LDS list (a window or a row list that overflows at
+  // run time takes the exact path)
+  rk_direct = !big;
+  for (int l = 0; l < n && rk_direct; ++l) {
+    const double dl = (double)(off64[l + 1] - off64[l]);
+    const double wm = (double)(tau[l] - ulo[l]) / 4294967296.0 * dl;
+    if (cbase[l + 1] - cbase[l] > (int32_t)(kSelNT * kSelPer) || wm + 8.0 * std::sqrt(wm) + 16.0 > (double)kListLds)
+      rk_direct = false;
+  }
   nrows = cbase[n];
   nruns = ro[n];
   rseg.resize(nrows);
@@ -326,6 +337,7 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
   WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
   const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
+  const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
   const dim3 pgrid((unsigned)L->nruns), pblk(kSampleRun);
   if (g) {
     if (g_dtype == EF_F32) {
@@ -366,7 +378,7 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
     EF_LAUNCH((k_select<0, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
   }
   EF_TRY(launched());
-  EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
+  EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();
 }
 
@@ -380,6 +392,7 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
   WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
   const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
+  const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g) {
     if (g_dtype == EF_F32)
@@ -390,8 +403,10 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
     EF_LAUNCH((k_stream_sel<1, 0, false>), rgrid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
   }
   EF_TRY(launched());
-  EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
-  EF_TRY(launched());
+  if (!L->rk_direct) {
+    EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
+    EF_TRY(launched());
+  }
   const float* acc = g ? e_fused : src;
   if (L->big) {
     EF_LAUNCH((k_select<1, true>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
@@ -403,7 +418,7 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
     EF_LAUNCH((k_select<1, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
   }
   EF_TRY(launched());
-  EF_LAUNCH(k_emit, rgrid, blk, 0, st, T, w, e_fused, idx, val);
+  EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, e_fused, idx, val);
   return launched();
 }
 
@@ -563,6 +578,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.nchunks = L->nchunks;
   T.nrows = L->nrows;
   T.nruns = L->nruns;
+  T.rk_direct = L->rk_direct ? 1 : 0;
   L->bound = true;
   return EF_OK;
 }
@@ -643,7 +659,7 @@ int ef_step_randblock(const ef_layout* L, const void* g, int g_dtype, float* e, 
   EF_TRY(check_bound(L));
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !word_ok(start) || !word_ok(val)) return EF_EINVAL;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT);
+  const dim3 grid((unsigned)((L->d + kRbTile - 1) / kRbTile)), blk(kNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g_dtype == EF_F32)
     EF_LAUNCH(k_randblock_step<0>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);

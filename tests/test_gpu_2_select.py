@@ -106,6 +106,18 @@ def test_randk_forced_slow_path():
     assert diag & E.DIAG_SLOW_PATH, "the slow path did not run"
 
 
+@pytest.mark.parametrize("offs", [[0, 4096], [0, 3, 4099, 9000]], ids=["one-row", "ragged"])
+def test_randk_row_list_overflow_takes_exact_path(offs):
+    """A window margin of 2000 around k_l = d_l / 2 makes every element of a 4096-element segment
+    undecided: more than a row's list slot holds, so the segment must take the exact path."""
+    import paper_2009_09271_amd as E
+    announce("randk row list overflow", offs)
+    c = Case(offs, 0.5, tune={E.EF_TUNE_RANDK_EXTRA: 2000.0})
+    g, e = _inputs(c.d, 12)
+    diag = _run_steps(c, "randk", [g, g], e, seed=79)
+    assert diag & E.DIAG_SLOW_PATH, "the exact path did not run"
+
+
 def test_randk_every_element_a_candidate():
     import paper_2009_09271_amd as E
     announce("randk all candidates")
