@@ -470,6 +470,65 @@ __global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_
   }
 }
 
+// Single-segment layouts (flat scope): one workgroup per data tile, no tables to look up.  The
+// starts of up to 64 workers come in one round trip into LDS; each wavefront finds the workers
+// whose run meets the tile with one ballot and visits them in ascending order, as in k_agg_block.
+__global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_t K, const uint32_t* start,
+                                                    const float* val, int average, float* out) {
+  __shared__ uint32_t s_st[64];
+  const uint32_t lo = blockIdx.x * kTile, hi = min((uint32_t)d, lo + kTile);
+  const uint32_t n = (uint32_t)d, k = (uint32_t)K;
+  const bool pow2 = (W & (W - 1)) == 0;
+  const float inv = 1.0f / (float)W;  // exact when W is a power of two
+  const int lane = threadIdx.x & 63;
+  float a[kRounds][4];
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
+  for (int wb = 0; wb < W; wb += 64) {
+    const int nw = min(64, W - wb);
+    if (wb > 0) __syncthreads();  // the previous group is done with s_st
+    if ((int)threadIdx.x < nw) s_st[threadIdx.x] = start[wb + threadIdx.x] % n;
+    __syncthreads();
+    bool hit = false;
+    if (lane < nw) {
+      const uint32_t s = s_st[lane], e1 = min(s + k, n);
+      // run piece 1: [s, e1); piece 2 (wrapped): [0, s + k - e1), empty unless the run wraps
+      hit = max(lo, s) < min(hi, e1) || lo < min(hi, s + k - e1);
+    }
+    uint64_t todo = __ballot(hit);
+    while (todo) {
+      const int j = __ffsll((long long)todo) - 1;
+      todo &= todo - 1;
+      const uint32_t sw = s_st[j];
+      const float* v = val + (size_t)(wb + j) * K;
+      // piece 1 ends at e1 = min(s + k, n); piece 2 ([0, s + k - e1)) is empty unless the run wraps
+      const uint32_t e1 = min(sw + k, n);
+      const uint32_t a1 = max(lo, sw), b1 = min(hi, e1), b2 = min(hi, sw + k - e1);
+#pragma unroll
+      for (int r = 0; r < kRounds; ++r) {
+        const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t i = i0 + q;
+          if (i >= a1 && i < b1) a[r][q] += v[i - sw];
+          else if (i < b2) a[r][q] += v[i + n - sw];
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kRounds; ++r) {
+    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    float v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(a[r][q], W, pow2, inv) : a[r][q];
+    store4(out, i0, nv, v);
+  }
+}
+
 // Persistent workgroups, each walking data tiles (blockIdx.x, then every gridDim.x-th), sums held
 // in registers (each thread its kRounds float4 groups; few enough registers for 8 waves per SIMD).  Per pass over up to kAggSegs
 // segments of the tile and a group of workers, the segments' sizes and the workers' block starts
@@ -527,8 +586,8 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
           if (wl < nw) {
             for (int x = 0; x < ns; ++x) {
               const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], s = s_st[wl * ns + x];
-              hit = hit || (max(lo, o + s) < min(hi, o + min(s + k, n))) ||
-                    (s + k > n && max(lo, o) < min(hi, o + (s + k - n)));
+              const uint32_t e1 = min(s + k, n);  // piece 2 below is empty unless the run wraps
+              hit = hit || (max(lo, o + s) < min(hi, o + e1)) || (max(lo, o) < min(hi, o + (s + k - e1)));
             }
           }
           uint64_t todo = __ballot(hit);
@@ -539,10 +598,12 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
             for (int x = 0; x < ns; ++x) {
               const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], P = s_seg[3][x];
               const uint32_t s = s_st[w * ns + x];
-              // run piece 1: global [o + s, o + min(s + k, n)), t = i - o - s;
-              // run piece 2: global [o, o + s + k - n), t = i - o + n - s
-              const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + min(s + k, n));
-              const uint32_t a2 = max(lo, o), b2 = s + k > n ? min(hi, o + (s + k - n)) : 0u;
+              // run piece 1: global [o + s, o + e1), e1 = min(s + k, n), t = i - o - s;
+              // run piece 2: global [o, o + s + k - e1) (empty unless the run wraps), t = i - o + n - s.
+              // (Written without a conditional: a select of this form was folded away by the compiler.)
+              const uint32_t e1 = min(s + k, n);
+              const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + e1);
+              const uint32_t a2 = max(lo, o), b2 = min(hi, o + (s + k - e1));
               if (a1 >= b1 && a2 >= b2) continue;
 #pragma unroll
               for (int r = 0; r < kR; ++r) {

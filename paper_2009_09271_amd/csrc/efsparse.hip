@@ -712,6 +712,10 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
+    if (L->L == 1) {
+      EF_LAUNCH(k_agg_block1, grid, blk, 0, st, L->T.d, W, (int32_t)L->K, m, val, average, out);
+      return launched();
+    }
     const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks(k_agg_block));
     EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
     return launched();

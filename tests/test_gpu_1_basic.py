@@ -155,6 +155,22 @@ def test_aggregate_block_many_segments_per_tile(W):
         _agg_check(c, "block", msgs, W, average)
 
 
+@pytest.mark.parametrize("W,rho,block", [(70, 0.6, 16), (130, 0.02, 1), (5, 1.0, 1)],
+                         ids=["wrapping-2groups", "3groups", "k=d"])
+def test_aggregate_block_single_segment(W, rho, block):
+    """One segment (flat scope): more than one wavefront's worth of workers, runs that wrap around
+    the end of the vector, and k = d (every worker covers everything)."""
+    announce("aggregate block single segment", W, rho, block)
+    c = Case([0, 10007], rho, block)
+    rng = np.random.default_rng(W + 7)
+    msgs = []
+    for w in range(W):
+        acc = rng.standard_normal(c.d).astype(np.float32)
+        msgs.append(O.compress_randblock(acc, c.offs, c.ks, block, 60 + w, 3))
+    for average in (True, False):
+        _agg_check(c, "block", msgs, W, average)
+
+
 @pytest.mark.parametrize("W,rho", [(4, 0.002), (16, 0.05)], ids=["few-shared", "many-shared"])
 def test_aggregate_sparse_shared_coordinates(W, rho):
     """Random-k with one seed for all workers (every position is hit by every worker): the shared
