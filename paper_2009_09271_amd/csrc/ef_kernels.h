@@ -271,25 +271,65 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 // Aggregate (Algorithm 1): out = (sum over workers in order, from +0) / W.  One workgroup per
 // output tile of kTile elements accumulates in LDS; a barrier separates consecutive workers.
 // ---------------------------------------------------------------------------------------------
-// Output tiles of the sparse aggregate: kAggTile elements, kAggRounds float4 groups per thread.
-constexpr uint32_t kAggTile = 4096;
-constexpr int kAggRounds = (int)kAggTile / (4 * kNT);
+// Output tiles of the sparse aggregate: kAggTile elements, summed by one wavefront (kAggRounds
+// float4 groups per lane).
+constexpr uint32_t kAggTile = 1024;
+constexpr int kAggRounds = (int)kAggTile / (4 * 64);
 
 // tile_start[w][tau] = first entry of message w whose index lies in an aggregate tile >= tau
-// (tau = 0..nt).  Grid: (ceil(K / kNT), W).
+// (tau = 0..nt; an index >= d counts as tile nt).  Grid: (ceil(K / kNT), W), one thread per entry.
+// Entry j starts the tiles after its predecessor's tile, up to its own (past the last entry the
+// tiles up to nt start at K).  A short run of tiles is written by its entry's thread; a longer one
+// (a gap in a message crowded into a few layers) by the whole workgroup as one coalesced run.
+// For ascending messages the entries' runs partition 0..nt.
+constexpr uint32_t kRunOwn = 128;  // runs of at most this many tiles are written by their own thread;
+                                   // longer ones (at most nt / 128 per message) by the workgroup
+
 __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
                                                     uint32_t* tile_start) {
+  __shared__ uint32_t s_nlong;
+  __shared__ uint32_t s_ta[kNT], s_n[kNT], s_j[kNT], s_own[kNT];  // the workgroup's long runs
   const uint32_t j = blockIdx.x * kNT + threadIdx.x;
   const int w = blockIdx.y;
-  if (j >= (uint32_t)K) return;
   const uint32_t* m = idx + (size_t)w * K;
   uint32_t* ts = tile_start + (size_t)w * (nt + 1);
-  auto tile = [&](uint32_t i) -> int { return i < (uint32_t)d ? (int)(i / kAggTile) : nt; };
-  const int tj = tile(m[j]);
-  const int tp = j == 0 ? -1 : tile(m[j - 1]);
-  for (int tau = tp + 1; tau <= tj; ++tau) ts[tau] = j;
-  if (j == (uint32_t)K - 1)
-    for (int tau = tj + 1; tau <= nt; ++tau) ts[tau] = (uint32_t)K;
+  auto tile = [&](uint32_t i) -> uint32_t { return i < (uint32_t)d ? i / kAggTile : (uint32_t)nt; };
+  // tile tau of entry e's run starts at e, except past the last entry's own tile (at K)
+  auto value = [&](uint32_t e, uint32_t tau, uint32_t e_own) -> uint32_t {
+    return e == (uint32_t)K - 1u && tau > e_own ? (uint32_t)K : e;
+  };
+  if (threadIdx.x == 0) s_nlong = 0;
+  __syncthreads();
+  if (j < (uint32_t)K) {
+    const uint32_t own = tile(m[j]);
+    const uint32_t ta = j == 0 ? 0u : tile(m[j - 1]) + 1u;
+    const uint32_t tb = j == (uint32_t)K - 1u ? (uint32_t)nt : own;
+    const uint32_t n = tb + 1u > ta ? tb + 1u - ta : 0u;
+    if (n > kRunOwn) {
+      const uint32_t p = atomicAdd(&s_nlong, 1u);
+      s_ta[p] = ta;
+      s_n[p] = n;
+      s_j[p] = j;
+      s_own[p] = own;
+    } else {
+      for (uint32_t k = 0; k < n; ++k) ts[ta + k] = value(j, ta + k, own);
+    }
+  }
+  __syncthreads();
+  for (uint32_t q = 0; q < s_nlong; ++q) {
+    const uint32_t qa = s_ta[q], qe = qa + s_n[q], qj = s_j[q], qown = s_own[q];
+    // 16-byte stores over the part of the run aligned in memory, single words at its two ends
+    const size_t base = (size_t)w * (nt + 1);
+    const uint32_t a4 = min(qe, qa + (uint32_t)((4u - (base + qa) % 4u) % 4u));
+    const uint32_t b4 = a4 + (qe - a4) / 4u * 4u;
+    if (threadIdx.x < a4 - qa) ts[qa + threadIdx.x] = value(qj, qa + threadIdx.x, qown);
+    if (threadIdx.x < qe - b4) ts[b4 + threadIdx.x] = value(qj, b4 + threadIdx.x, qown);
+    for (uint32_t o = a4 + 4u * threadIdx.x; o < b4; o += 4u * kNT) {
+      const uint4 v = make_uint4(value(qj, o, qown), value(qj, o + 1, qown), value(qj, o + 2, qown),
+                                 value(qj, o + 3, qown));
+      *reinterpret_cast<uint4*>(ts + o) = v;
+    }
+  }
 }
 
 // out = sum / W in IEEE float32.  For W a power of two the quotient is the exact scaling
@@ -299,201 +339,165 @@ __device__ __forceinline__ float agg_scale(float sum, int32_t W, bool pow2, floa
   return pow2 ? sum * inv : __fdiv_rn(sum, (float)W);
 }
 
-constexpr int kAggW = 64;           // workers whose tile ranges are held in LDS at once
-constexpr int kAggStage = 512;      // message entries staged in LDS per pass (2 per thread)
 constexpr int kAggStarts = 1024;    // block starts (workers x segments of the tile) held in LDS
+constexpr int kAggChunk = 4;        // sparse aggregate: entries per lane loaded together past the first 64
+constexpr int kAggClaim = 256;      // sparse aggregate: claim slots (positions hash to x mod 256)
 
-// Worker w of the group (0 <= w < nw) whose staged entries [pre[w], pre[w + 1]) contain f.
-__device__ __forceinline__ int agg_worker_of(const uint32_t* pre, int nw, uint32_t f) {
-  int a = 0, b = nw - 1;
-  while (a < b) {
-    const int mid = (a + b + 1) >> 1;
-    if (pre[mid] <= f) a = mid; else b = mid - 1;
+// Sparse aggregate: one wavefront per workgroup and one output tile of kAggTile elements per
+// workgroup; many small workgroups resident per CU overlap each other's two load round trips
+// (the tile's ranges, then its entries).  Lane j of a group of up to 64 workers holds worker
+// j's entry range in the tile.  A tile no message enters is stored as zeros at once.  Otherwise
+// its sums build up in an LDS tile: the tile's entries, in worker order, are added 64 at a time;
+// lanes whose entries share a position add one after another in lane order (the lowest lane that
+// still has to add claims the position's slot with an LDS atomic minimum; positions sharing a slot
+// only wait for each other), which is worker order.  Entries past the first 64 are loaded
+// kAggChunk per lane at a time.
+struct AggLds {
+  float acc[kAggTile];
+  uint32_t claim[kAggClaim];  // ~0 between adds
+  uint32_t pre[65];           // entry prefix of each worker of the group
+  uint32_t a[64];             // each worker's first entry in the tile
+};
+
+// Staged entry f of a worker group -> message entry: binary search of the prefixes.
+__device__ __forceinline__ size_t agg_entry(const AggLds& S, int nw, int w0, int32_t K, uint32_t f) {
+  int lo = 0, hi = nw - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (S.pre[mid] <= f) lo = mid; else hi = mid - 1;
   }
-  return a;
+  return (size_t)(w0 + lo) * K + S.a[lo] + (f - S.pre[lo]);
 }
 
-// Persistent workgroups, each walking output tiles of kAggTile elements (tile blockIdx.x, then
-// every gridDim.x-th), summed in an LDS tile; the next tile's ranges are loaded while the current
-// one is summed and stored.  Per group of up to
-// kAggW workers: the tile's entry range of every worker in one round trip, then passes of up to
-// kAggStage entries staged in LDS in worker order (loads in flight together).  Within a pass an
-// LDS bitmap finds the positions hit more than once: the others take their value at once (no
-// ordering question), the shared ones are summed in worker order, either by the first entry of
-// each shared position walking the pass's shared entries (few of them) or worker by worker with
-// a barrier after each (many).  Passes, and groups, follow each other in worker order.
-constexpr int kAggScanMax = 64;
+// Prefixes of the worker group [w0, w0 + nw) whose ranges lane j holds (unclamped); returns the
+// group's entry count.  Wave-uniform.
+__device__ __forceinline__ uint32_t agg_group(AggLds& S, int nw, int32_t K, uint32_t ra, uint32_t rb) {
+  const int lane = threadIdx.x;
+  ra = min(ra, (uint32_t)K);
+  rb = min(rb, (uint32_t)K);
+  const uint32_t c = lane < nw && rb > ra ? rb - ra : 0u;
+  const uint32_t inc = wave_incl_scan(c);
+  S.pre[lane] = inc - c;
+  S.a[lane] = ra;
+  if (lane == 63) S.pre[64] = inc;
+  __syncthreads();  // a one-wavefront workgroup: orders the LDS writes above before the reads
+  return __shfl(inc, 63, 64);
+}
 
-__global__ __launch_bounds__(kNT) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
-                                                    const uint32_t* idx, const float* val,
-                                                    const uint32_t* tile_start, int average, float* out) {
-  constexpr int kU = kAggStage / kNT;  // staged entries per thread and pass (2)
-  static_assert(kU == 2, "the shared-entry compaction packs two 16-bit counts");
-  __shared__ float acc[kAggTile];
-  __shared__ uint32_t s_pre[kAggW + 1];
-  __shared__ uint32_t s_a[kAggW];
-  __shared__ uint32_t s_i[kAggStage];
-  __shared__ float s_v[kAggStage];
-  __shared__ uint32_t s_cf[kAggStage];  // staged positions of the shared entries, ascending
-  __shared__ uint32_t s_seen[kAggTile / 32];
-  __shared__ uint32_t s_multi[kAggTile / 32];
-  __shared__ uint32_t lds[kNT / 64];
+// Adds one batch of up to 64 entries (lane order = worker order) into the LDS tile.
+__device__ __forceinline__ void agg_add(AggLds& S, uint32_t lo, uint32_t hi, uint32_t i, float v, bool ok) {
+  const uint32_t lane = threadIdx.x;
+  bool pending = ok && i >= lo && i < hi;
+  const uint32_t x = pending ? i - lo : 0u, c = x % kAggClaim;
+  while (__ballot(pending)) {
+    if (pending) atomicMin(&S.claim[c], lane);
+    __syncthreads();
+    if (pending && S.claim[c] == lane) {
+      S.acc[x] += v;
+      S.claim[c] = ~0u;
+      pending = false;
+    }
+    __syncthreads();
+  }
+}
+
+// Adds entries [f0, E) of the group set up by agg_group, kAggChunk per lane at a time.
+__device__ __forceinline__ void agg_add_rest(AggLds& S, int nw, int w0, int32_t K, const uint32_t* idx,
+                                             const float* val, uint32_t lo, uint32_t hi, uint32_t f0, uint32_t E) {
+  for (; f0 < E; f0 += 64u * kAggChunk) {
+    uint32_t ci[kAggChunk];
+    float cv[kAggChunk];
+#pragma unroll
+    for (int u = 0; u < kAggChunk; ++u) {
+      const uint32_t f = f0 + (uint32_t)u * 64u + threadIdx.x;
+      const size_t j = f < E ? agg_entry(S, nw, w0, K, f) : 0;
+      ci[u] = idx[j];
+      cv[u] = val[j];
+    }
+#pragma unroll
+    for (int u = 0; u < kAggChunk; ++u) agg_add(S, lo, hi, ci[u], cv[u], f0 + (uint32_t)u * 64u + threadIdx.x < E);
+  }
+}
+
+__global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
+                                                   const uint32_t* idx, const float* val,
+                                                   const uint32_t* tile_start, int average, float* out) {
+  __shared__ AggLds S;
+  const int lane = threadIdx.x;
+  const uint32_t t = blockIdx.x;
+  const uint32_t lo = t * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
   const bool pow2 = (W & (W - 1)) == 0;
   const float inv = 1.0f / (float)W;  // exact when W is a power of two
-  // the first worker group's ranges of the next tile are loaded one tile ahead
-  uint32_t pa = 0, pb = 0;
-  auto prefetch = [&](uint32_t t) {
-    if ((int)threadIdx.x < min(W, kAggW) && t < (uint32_t)nt) {
-      const uint32_t* ts = tile_start + (size_t)threadIdx.x * (nt + 1);
-      pa = ts[t];
-      pb = ts[t + 1];
-    }
-  };
-  prefetch(blockIdx.x);
-  for (uint32_t tau = blockIdx.x; tau < (uint32_t)nt; tau += gridDim.x) {
-    const uint32_t lo = tau * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
-    for (uint32_t x = threadIdx.x; x < kAggTile; x += kNT) acc[x] = 0.0f;
-    for (int w0 = 0; w0 < W; w0 += kAggW) {
-      const int nw = min(kAggW, W - w0);
-      uint32_t ra = 0, cnt = 0;
-      if ((int)threadIdx.x < nw) {
-        uint32_t rb;
-        if (w0 == 0) {
-          ra = min(pa, (uint32_t)K);
-          rb = min(pb, (uint32_t)K);
-        } else {
-          const uint32_t* ts = tile_start + (size_t)(w0 + threadIdx.x) * (nt + 1);
-          ra = min(ts[tau], (uint32_t)K);
-          rb = min(ts[tau + 1], (uint32_t)K);
-        }
-        cnt = rb > ra ? rb - ra : 0u;
-      }
-      if (w0 == 0) prefetch(tau + gridDim.x);
-      uint32_t tot;
-      const uint32_t ex = block_excl_scan<kNT>(cnt, lds, tot);
-      if ((int)threadIdx.x < nw) {
-        s_pre[threadIdx.x] = ex;
-        s_a[threadIdx.x] = ra;
-      }
-      if (threadIdx.x == 0) s_pre[nw] = tot;
-      __syncthreads();
-      for (uint32_t f0 = 0; f0 < tot; f0 += kAggStage) {
-        const uint32_t f1 = min(tot, f0 + (uint32_t)kAggStage);
-        uint32_t si[kU];
-        float sv[kU];
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          const uint32_t f = f0 + (uint32_t)(u * kNT) + threadIdx.x;
-          si[u] = 0xFFFFFFFFu;
-          sv[u] = 0.0f;
-          if (f < f1) {
-            const int w = agg_worker_of(s_pre, nw, f);
-            const size_t j = (size_t)(w0 + w) * K + s_a[w] + (f - s_pre[w]);
-            si[u] = idx[j];
-            sv[u] = val[j];
-          }
-          if (si[u] < lo || si[u] >= hi) si[u] = 0xFFFFFFFFu;  // outside the tile: ignored
-        }
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          s_i[u * kNT + threadIdx.x] = si[u];
-          s_v[u * kNT + threadIdx.x] = sv[u];
-        }
-        for (uint32_t x = threadIdx.x; x < kAggTile / 32; x += kNT) {
-          s_seen[x] = 0;
-          s_multi[x] = 0;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          if (si[u] != 0xFFFFFFFFu) {
-            const uint32_t x = si[u] - lo, bit = 1u << (x & 31u);
-            if (atomicOr(&s_seen[x >> 5], bit) & bit) atomicOr(&s_multi[x >> 5], bit);
-          }
-        }
-        __syncthreads();
-        // single entries add at once; shared ones are compacted in staged order
-        uint32_t shared_u = 0;
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          if (si[u] != 0xFFFFFFFFu) {
-            const uint32_t x = si[u] - lo;
-            if ((s_multi[x >> 5] >> (x & 31u)) & 1u) shared_u |= 1u << u;
-            else acc[x] += sv[u];
-          }
-        }
-        uint32_t ctot;
-        const uint32_t cex = block_excl_scan<kNT>((shared_u & 1u) | ((shared_u >> 1) << 16), lds, ctot);
-        const uint32_t n0 = ctot & 0xFFFFu, cn = n0 + (ctot >> 16);
-        if (shared_u & 1u) s_cf[cex & 0xFFFFu] = threadIdx.x;
-        if (shared_u & 2u) s_cf[n0 + (cex >> 16)] = kNT + threadIdx.x;
-        __syncthreads();
-        if (cn > 0 && cn <= (uint32_t)kAggScanMax) {
-          if (threadIdx.x < cn) {
-            const uint32_t i = s_i[s_cf[threadIdx.x]];
-            bool first = true;
-            for (uint32_t e = 0; e < threadIdx.x; ++e) first = first && s_i[s_cf[e]] != i;
-            if (first) {
-              float sum = acc[i - lo];
-              for (uint32_t e = threadIdx.x; e < cn; ++e)
-                if (s_i[s_cf[e]] == i) sum += s_v[s_cf[e]];
-              acc[i - lo] = sum;
-            }
-          }
-        } else if (cn > 0) {
-          const int wa = agg_worker_of(s_pre, nw, f0), wb = agg_worker_of(s_pre, nw, f1 - 1);
-          for (int w = wa; w <= wb; ++w) {
-            const uint32_t ea = lower_bound_u32(s_cf, cn, max(s_pre[w], f0) - f0);
-            const uint32_t eb = lower_bound_u32(s_cf, cn, min(s_pre[w + 1], f1) - f0);
-            if (ea >= eb) continue;
-            for (uint32_t e = ea + threadIdx.x; e < eb; e += kNT) {
-              const uint32_t fe = s_cf[e];
-              acc[s_i[fe] - lo] += s_v[fe];
-            }
-            __syncthreads();
-          }
-        }
-        __syncthreads();  // staging buffers are rewritten by the next pass
-      }
-    }
+  // ranges of the first worker group (lane j: worker j; lanes past W read worker W - 1's)
+  const int nw0 = min(W, 64);
+  const uint32_t* ts = tile_start + (size_t)min(lane, nw0 - 1) * (nt + 1) + t;
+  const uint32_t ra = ts[0], rb = ts[1];
+  for (uint32_t x = lane; x < kAggClaim; x += 64) S.claim[x] = ~0u;
+  const uint32_t E = agg_group(S, nw0, K, ra, rb);
+  if (W <= 64 && E == 0) {
 #pragma unroll
     for (int r = 0; r < kAggRounds; ++r) {
-      const uint32_t x = (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      const uint32_t i0 = lo + x;
-      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-      float v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(acc[x + q], W, pow2, inv) : acc[x + q];
-      store4(out, i0, nv, v);
+      const uint32_t i0 = lo + (uint32_t)(r * 64 + lane) * 4u;
+      const int n = i0 < hi ? (int)min(4u, hi - i0) : 0;
+      const float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      store4(out, i0, n, z);
     }
-    __syncthreads();  // the next tile clears acc
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < kAggRounds; ++r) {
+    const f4 z = {0.0f, 0.0f, 0.0f, 0.0f};
+    *reinterpret_cast<f4*>(&S.acc[(r * 64 + lane) * 4]) = z;
+  }
+  __syncthreads();
+  agg_add_rest(S, nw0, 0, K, idx, val, lo, hi, 0u, E);
+  for (int w0 = 64; w0 < W; w0 += 64) {  // further worker groups
+    const int nw = min(64, W - w0);
+    const uint32_t* tg = tile_start + (size_t)(w0 + min(lane, nw - 1)) * (nt + 1) + t;
+    const uint32_t Eg = agg_group(S, nw, K, tg[0], tg[1]);
+    agg_add_rest(S, nw, w0, K, idx, val, lo, hi, 0u, Eg);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kAggRounds; ++r) {
+    const uint32_t x = (uint32_t)(r * 64 + lane) * 4u;
+    const uint32_t i0 = lo + x;
+    const int n = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    const f4 s4 = *reinterpret_cast<const f4*>(&S.acc[x]);
+    float v[4] = {s4.x, s4.y, s4.z, s4.w};
+    if (average) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = agg_scale(v[q], W, pow2, inv);
+    }
+    store4(out, i0, n, v);
   }
 }
 
-// Single-segment layouts (flat scope): one workgroup per data tile, no tables to look up.  The
-// starts of up to 64 workers come in one round trip into LDS; each wavefront finds the workers
-// whose run meets the tile with one ballot and visits them in ascending order, as in k_agg_block.
+// Single-segment layouts (flat scope): one workgroup per tile of R float4 groups per thread, no
+// tables to look up and no barrier.  Each wavefront loads the starts of 64 workers at a time
+// (lane j: worker wb + j), finds those whose run meets the tile with one ballot and visits them in
+// ascending order, as in k_agg_block.
+template <int R>
 __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_t K, const uint32_t* start,
                                                     const float* val, int average, float* out) {
-  __shared__ uint32_t s_st[64];
-  const uint32_t lo = blockIdx.x * kTile, hi = min((uint32_t)d, lo + kTile);
+  constexpr uint32_t kT = (uint32_t)R * 4u * kNT;
+  const uint32_t lo = blockIdx.x * kT, hi = min((uint32_t)d, lo + kT);
   const uint32_t n = (uint32_t)d, k = (uint32_t)K;
   const bool pow2 = (W & (W - 1)) == 0;
   const float inv = 1.0f / (float)W;  // exact when W is a power of two
   const int lane = threadIdx.x & 63;
-  float a[kRounds][4];
+  float a[R][4];
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r)
+  for (int r = 0; r < R; ++r)
 #pragma unroll
     for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
   for (int wb = 0; wb < W; wb += 64) {
     const int nw = min(64, W - wb);
-    if (wb > 0) __syncthreads();  // the previous group is done with s_st
-    if ((int)threadIdx.x < nw) s_st[threadIdx.x] = start[wb + threadIdx.x] % n;
-    __syncthreads();
+    uint32_t s = 0;
     bool hit = false;
     if (lane < nw) {
-      const uint32_t s = s_st[lane], e1 = min(s + k, n);
+      s = start[wb + lane] % n;
+      const uint32_t e1 = min(s + k, n);
       // run piece 1: [s, e1); piece 2 (wrapped): [0, s + k - e1), empty unless the run wraps
       hit = max(lo, s) < min(hi, e1) || lo < min(hi, s + k - e1);
     }
@@ -501,13 +505,13 @@ __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_
     while (todo) {
       const int j = __ffsll((long long)todo) - 1;
       todo &= todo - 1;
-      const uint32_t sw = s_st[j];
+      const uint32_t sw = __shfl(s, j, 64);
       const float* v = val + (size_t)(wb + j) * K;
       // piece 1 ends at e1 = min(s + k, n); piece 2 ([0, s + k - e1)) is empty unless the run wraps
       const uint32_t e1 = min(sw + k, n);
       const uint32_t a1 = max(lo, sw), b1 = min(hi, e1), b2 = min(hi, sw + k - e1);
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
+      for (int r = 0; r < R; ++r) {
         const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -519,7 +523,7 @@ __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_
     }
   }
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
+  for (int r = 0; r < R; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
     const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
     float v[4];

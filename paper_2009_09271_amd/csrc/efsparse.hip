@@ -291,18 +291,21 @@ bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
     if (_rc != EF_OK) return _rc; \
   } while (0)
 
-// Workgroups that fit on the device at once for a persistent kernel (computed once per kernel;
-// every GPU this library drives is the same part).
-template <typename K>
-unsigned resident_blocks(K kernel) {
-  static const unsigned n = [&] {
-    int dev = 0, cus = 0, per = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, kNT, 0) != hipSuccess || cus < 1 || per < 1)
-      return 1024u;
-    return (unsigned)(cus * per);
-  }();
+// Workgroups of `threads` threads that fit on the device at once for a persistent kernel
+// (computed once per kernel; every GPU this library drives is the same part).
+unsigned resident_blocks(const void* kernel, int threads) {
+  static std::mutex mu;
+  static std::vector<std::pair<const void*, unsigned>> cache;
+  std::lock_guard<std::mutex> lk(mu);
+  for (const auto& c : cache)
+    if (c.first == kernel) return c.second;
+  int dev = 0, cus = 0, per = 0;
+  unsigned n = 1024u;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) == hipSuccess && cus > 0 && per > 0)
+    n = (unsigned)(cus * per);
+  cache.emplace_back(kernel, n);
   return n;
 }
 
@@ -707,16 +710,18 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     const int32_t nt = agg_tiles(L->d);
     EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts);
     EF_TRY(launched());
-    const unsigned g = std::min<unsigned>((unsigned)nt, resident_blocks(k_agg_sparse));
-    EF_LAUNCH(k_agg_sparse, dim3(g), blk, 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average, out);
+    EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), dim3(64), 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average,
+              out);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
     if (L->L == 1) {
-      EF_LAUNCH(k_agg_block1, grid, blk, 0, st, L->T.d, W, (int32_t)L->K, m, val, average, out);
+      constexpr uint32_t kT1 = 4u * kNT;  // one float4 group per thread
+      EF_LAUNCH(k_agg_block1<1>, dim3((unsigned)((L->d + kT1 - 1) / kT1)), blk, 0, st, L->T.d, W, (int32_t)L->K,
+                m, val, average, out);
       return launched();
     }
-    const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks(k_agg_block));
+    const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks((const void*)k_agg_block, kNT));
     EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
     return launched();
   }

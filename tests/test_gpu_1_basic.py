@@ -184,3 +184,27 @@ def test_aggregate_sparse_shared_coordinates(W, rho):
         msgs.append(O.compress_randk(acc, c.offs, c.ks, 1234, 3))
     for average in (True, False):
         _agg_check(c, "sparse", msgs, W, average)
+
+
+@pytest.mark.parametrize("W", [2, 16, 70])
+def test_aggregate_sparse_concentrated(W):
+    """Messages that crowd into a few tiles with long empty gaps (top-k on layers of very
+    different scales): tile boundaries far from every entry (more than one strided pass of the
+    ranges kernel), tiles no message enters, and tiles with thousands of entries."""
+    announce("aggregate concentrated", W)
+    d = 4096 * 700 + 123
+    offs = [0, d]
+    rng = np.random.default_rng(W + 11)
+    msgs = []
+    for w in range(W):
+        hot = rng.choice(np.arange(4096 * 300, 4096 * 303), size=3000, replace=False)
+        far = np.array([5, d - 1], dtype=np.int64)
+        i = np.unique(np.concatenate([hot, far])).astype(np.uint32)
+        v = (rng.standard_normal(i.size) * 10.0 ** rng.integers(-3, 3)).astype(np.float32)
+        msgs.append((i, v))
+    K = msgs[0][0].size
+    assert all(m[0].size == K for m in msgs)
+    c = Case(offs, K / d)
+    assert c.K == K
+    for average in (True, False):
+        _agg_check(c, "sparse", msgs, W, average)
