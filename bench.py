@@ -152,8 +152,13 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="N",
                     help="first launch the library's plain copy kernel N times on d floats (a known "
                          "4d-byte read + 4d-byte write per launch) to calibrate HBM byte counters")
+    ap.add_argument("--schedule", default="fused", choices=["fused", "pipelined"],
+                    help="fused: each top-k / random-k worker step on one of --worker-streams streams; "
+                         "pipelined: its phases split over a streaming stream and two selection streams")
+    ap.add_argument("--worker-streams", type=int, default=3)
     ap.add_argument("--streams", type=int, default=3,
-                    help="HIP streams the simulated workers are spread over (plus one for the aggregates)")
+                    help="workspace slots: top-k / random-k worker steps in flight at once (pipelined: at "
+                         "least 4)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -202,62 +207,125 @@ def main():
         msg[vname(v)] = (torch.empty((W, n_m), dtype=torch.int32, device=dev),
                          torch.empty((W, K), dtype=torch.float32, device=dev))
     out = {vname(v): torch.empty(d, dtype=torch.float32, device=dev) for v in variants}
-    S = max(1, args.streams)
+    # workspace slots of the top-k / random-k steps in flight
+    S = max(4, args.streams) if args.schedule == "pipelined" else max(1, args.streams)
     kinds = {k for k, _ in variants}
     ws_topk = [lay0.workspace(E.EF_OP_TOPK, 1, dev) for _ in range(S)] if "topk" in kinds else None
     ws_randk = [lay0.workspace(E.EF_OP_RANDK, 1, dev) for _ in range(S)] if "randk" in kinds else None
     ws_agg = lay0.workspace(E.EF_OP_AGG_SPARSE, W, dev)
-    # worker streams and one aggregate stream, all at the default priority
-    wstreams = [torch.cuda.Stream(dev) for _ in range(S)]
-    astream = torch.cuda.Stream(dev)
+    # stream A: the streaming passes; streams B0 / B1: the selection phases of even / odd workers;
+    # one stream for the aggregates (all at the default priority)
+    sA, astream = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
+    sB = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
 
-    def worker_step(v, w, t, slot):
-        kind, b = v
-        lay = layouts[b if kind == "randblock" else 1]
+    # events reused every step (a wait takes the event's latest record at the time it is enqueued)
+    evs = {vname(v): [[torch.cuda.Event() for _ in range(W)] for _ in range(3)] for v in variants}
+
+    def phase(v, w, t, p, st):
+        kind, _ = v
         mi, mv = msg[vname(v)]
         ev = e[vname(v)]
         if kind == "topk":
-            E.ef_step_topk(lay, g[w], ev[w], mi[w], mv[w], ws_topk[slot])
-        elif kind == "randk":
-            E.ef_step_randk(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], ws_randk[slot])
+            E.ef_step_topk_phases(lay0, p, g[w], ev[w], mi[w], mv[w], ws_topk[w % S], stream=st)
         else:
-            E.ef_step_randblock(lay, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w])
+            E.ef_step_randk_phases(lay0, p, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], ws_randk[w % S],
+                                   stream=st)
 
-    def aggregate(v):
+    def aggregate(v, st):
         kind, b = v
         lay = layouts[b if kind == "randblock" else 1]
         mi, mv = msg[vname(v)]
         kindm = E.EF_MSG_BLOCK if kind == "randblock" else E.EF_MSG_SPARSE
-        E.decompress_aggregate(lay, kindm, W, mi, mv, out[vname(v)], ws_agg if kindm == E.EF_MSG_SPARSE else None)
+        E.decompress_aggregate(lay, kindm, W, mi, mv, out[vname(v)], ws_agg if kindm == E.EF_MSG_SPARSE else None,
+                               stream=st)
 
-    def run_step(t, vs=None):
-        """One step.  Block-random-k variants run first on one stream (pure streaming kernels gain
-        nothing from overlap, and their launches stay clean to time).  Then the top-k / random-k
-        variants: worker w on stream w % S, so the short selection kernels of one worker overlap
-        the streaming pass of another; each variant's aggregate runs on its own stream once the
-        variant's W messages are written, overlapping the next variant's workers."""
-        vs = vs or variants
+    wstreams = [torch.cuda.Stream(dev) for _ in range(args.worker_streams)]
+
+    def run_step_fused(t, vs):
+        """Top-k / random-k workers run their fused step, worker w on worker stream w % n; each
+        variant's aggregate waits for all of them on its own stream."""
         cur = torch.cuda.current_stream(dev)
-        s0 = wstreams[0]
-        s0.wait_stream(cur)
-        with torch.cuda.stream(s0):
-            for v in vs:
-                if v[0] == "randblock":
-                    for w in range(W):
-                        worker_step(v, w, t, 0)
-                    aggregate(v)
-        conc = [v for v in vs if v[0] != "randblock"]
-        for st in wstreams[1:] + [astream]:
-            st.wait_stream(s0)
-        for v in conc:
+        for st in wstreams + [sA, astream]:
+            st.wait_stream(cur)
+        for v in vs:
+            kind, b = v
+            mi, mv = msg[vname(v)]
+            ev = e[vname(v)]
+            if kind == "randblock":
+                for w in range(W):
+                    E.ef_step_randblock(layouts[b], g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], stream=sA)
+                astream.wait_stream(sA)
+                aggregate(v, astream)
+                continue
+            n = len(wstreams)
             for w in range(W):
-                with torch.cuda.stream(wstreams[w % S]):
-                    worker_step(v, w, t, w % S)
+                st = wstreams[w % n]
+                ws = ws_topk[w % S] if kind == "topk" else ws_randk[w % S]
+                if w >= S and S % n:  # the workspace slot of worker w - S (same stream when n divides S)
+                    st.wait_event(evs[vname(v)][2][w - S])
+                if kind == "topk":
+                    E.ef_step_topk_phases(lay0, E.EF_PHASE_ALL, g[w], ev[w], mi[w], mv[w], ws, stream=st)
+                else:
+                    E.ef_step_randk_phases(lay0, E.EF_PHASE_ALL, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w],
+                                           ws, stream=st)
+                if w + S < W and (S % n):
+                    evs[vname(v)][2][w].record(st)
             for st in wstreams:
                 astream.wait_stream(st)
-            with torch.cuda.stream(astream):
-                aggregate(v)
-        for st in wstreams + [astream]:
+            aggregate(v, astream)
+        for st in wstreams + [sA, astream]:
+            cur.wait_stream(st)
+
+    def run_step(t, vs=None):
+        vs = vs or variants
+        if args.schedule == "fused":
+            return run_step_fused(t, vs)
+        return run_step_pipelined(t, vs)
+
+    def run_step_pipelined(t, vs):
+        """Top-k / random-k workers run their fused step in three phases (ef_step_*_phases): the
+        streaming passes follow each other on stream A, while streams B0 / B1 (even / odd workers)
+        run the selection phases around them, each worker's prepare two workers ahead of its
+        stream pass.  Block-random-k workers are one streaming kernel each on stream A."""
+        cur = torch.cuda.current_stream(dev)
+        for st in [sA, astream] + sB:
+            st.wait_stream(cur)
+        for v in vs:
+            kind, b = v
+            if kind == "randblock":
+                mi, mv = msg[vname(v)]
+                ev = e[vname(v)]
+                for w in range(W):
+                    E.ef_step_randblock(layouts[b], g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], stream=sA)
+                astream.wait_stream(sA)
+                aggregate(v, astream)
+                continue
+            prep = kind == "topk"  # random-k has nothing to prepare
+            ready, done, fin = evs[vname(v)]
+
+            def prepare(w):
+                if prep and w < W:
+                    phase(v, w, t, E.EF_PHASE_PREPARE, sB[w % 2])
+                    ready[w].record(sB[w % 2])
+
+            prepare(0)
+            prepare(1)
+            for w in range(W):
+                sb = sB[w % 2]
+                prepare(w + 2)  # its slot was last used by worker w - 2, finished earlier on sb
+                if prep:
+                    sA.wait_event(ready[w])
+                elif w >= S:  # the workspace slot is free once the step that used it finished
+                    sA.wait_event(fin[w - S])
+                phase(v, w, t, E.EF_PHASE_STREAM, sA)
+                done[w].record(sA)
+                sb.wait_event(done[w])
+                phase(v, w, t, E.EF_PHASE_FINISH, sb)
+                fin[w].record(sb)
+            for sb in sB:
+                astream.wait_stream(sb)
+            aggregate(v, astream)
+        for st in [sA, astream] + sB:
             cur.wait_stream(st)
 
     step_no = 0
@@ -357,7 +425,8 @@ def main():
                          f"+ one aggregate per variant per step"),
             "d": d, "segments": L, "K": K, "W": W, "density": density,
             "variants": [vname(v) for v in variants], "scope": args.scope,
-            "streams": f"{S} worker streams + 1 aggregate stream",
+            "streams": "streaming passes on one stream, selection phases on a second, aggregates on a "
+                       f"third; {S} workspace slots",
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -190,6 +190,33 @@ int ef_step_randk(const ef_layout* layout, const void* g, int g_dtype, float* e,
 int ef_step_randblock(const ef_layout* layout, const void* g, int g_dtype, float* e, uint64_t seed,
                       uint32_t step, uint32_t* start, float* val, void* stream);
 
+/* The fused top-k and random-k steps in phases, for callers that overlap
+ * the steps of several workers (or gradient buckets) on more than one
+ * stream.  Same operation and arguments as ef_step_topk / ef_step_randk,
+ * plus `phases`, a nonzero OR of:
+ *   EF_PHASE_PREPARE  top-k: the threshold sample of acc = g + e and the
+ *                     candidate rule (reads g and e at the sample positions);
+ *                     random-k: nothing (its keys do not depend on the data)
+ *   EF_PHASE_STREAM   the streaming pass: acc = g + e written to e, the
+ *                     candidates listed in the workspace
+ *   EF_PHASE_FINISH   the exact threshold, the message and e = +0 where sent
+ * Calling PREPARE, STREAM and FINISH in that order with the same arguments
+ * and workspace (each call enqueued after the previous one has completed,
+ * on one stream or ordered with events) is bitwise identical to the fused
+ * step; EF_PHASE_ALL is the fused step itself.  Between the first and the
+ * last phase, the workspace belongs to this step and g and e must not be
+ * changed by other work.  Arguments are checked at every call; phases
+ * outside EF_PHASE_ALL are EF_EINVAL. */
+#define EF_PHASE_PREPARE 1u
+#define EF_PHASE_STREAM 2u
+#define EF_PHASE_FINISH 4u
+#define EF_PHASE_ALL 7u
+int ef_step_topk_phases(const ef_layout* layout, unsigned phases, const void* g, int g_dtype, float* e,
+                        uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream);
+int ef_step_randk_phases(const ef_layout* layout, unsigned phases, const void* g, int g_dtype, float* e,
+                         uint64_t seed, uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes,
+                         void* stream);
+
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could
  * not contain the answer and the exact whole-segment path ran instead (a

@@ -24,6 +24,7 @@ EF_F32, EF_BF16 = 0, 1
 EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK = range(5)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
 EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA = range(4)
+EF_PHASE_PREPARE, EF_PHASE_STREAM, EF_PHASE_FINISH, EF_PHASE_ALL = 1, 2, 4, 7
 DIAG_SLOW_PATH = 2
 DIAG_COUNT_MISMATCH = 4
 
@@ -65,6 +66,9 @@ _SIGS = {
     "ef_step_topk": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randblock": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
+    "ef_step_topk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P,
+                                        _c.c_size_t, _P]),
     "ef_timing_enable": (_c.c_int, [_c.c_int]),
     "ef_timing_collect": (_c.c_int, []),
     "ef_timing_count": (_c.c_int, []),
@@ -93,7 +97,11 @@ def _check(code, where):
         raise EfError(code, where)
 
 
-def _stream(t):
+def _stream(t, stream=None):
+    """The HIP stream handle to enqueue on: `stream` (a torch.cuda.Stream) when given, else the
+    current stream of t's device."""
+    if stream is not None:
+        return ctypes.c_void_p(stream.cuda_stream)
     import torch
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
@@ -208,10 +216,10 @@ def ef_update(layout, acc, msg_kind, idx_or_start, e):
            "ef_update")
 
 
-def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, average=True):
+def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, average=True, stream=None):
     n = ws.numel() if ws is not None else 0
     _check(_lib.decompress_aggregate(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
-                                     1 if average else 0, _ptr(out), _ptr(ws), n, _stream(out)),
+                                     1 if average else 0, _ptr(out), _ptr(ws), n, _stream(out, stream)),
            "decompress_aggregate")
 
 
@@ -225,9 +233,20 @@ def ef_step_randk(layout, g, e, seed, step, idx, val, ws):
                               _ptr(ws), ws.numel(), _stream(e)), "ef_step_randk")
 
 
-def ef_step_randblock(layout, g, e, seed, step, start, val):
+def ef_step_topk_phases(layout, phases, g, e, idx, val, ws, stream=None):
+    _check(_lib.ef_step_topk_phases(layout.handle, int(phases), _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val),
+                                    _ptr(ws), ws.numel(), _stream(e, stream)), "ef_step_topk_phases")
+
+
+def ef_step_randk_phases(layout, phases, g, e, seed, step, idx, val, ws, stream=None):
+    _check(_lib.ef_step_randk_phases(layout.handle, int(phases), _ptr(g), _gdt(g), _ptr(e), int(seed), int(step),
+                                     _ptr(idx), _ptr(val), _ptr(ws), ws.numel(), _stream(e, stream)),
+           "ef_step_randk_phases")
+
+
+def ef_step_randblock(layout, g, e, seed, step, start, val, stream=None):
     _check(_lib.ef_step_randblock(layout.handle, _ptr(g), _gdt(g), _ptr(e), int(seed), int(step), _ptr(start),
-                                  _ptr(val), _stream(e)), "ef_step_randblock")
+                                  _ptr(val), _stream(e, stream)), "ef_step_randblock")
 
 
 def lib():

@@ -161,9 +161,10 @@ __device__ __forceinline__ uint32_t run_pos(const RunSeg& r, uint32_t i) {
 // Fused worker step: acc = g + e; val[P_l + t] = acc on the run; e' = +0 on the run, acc elsewhere.
 // One float4 group per thread (kRbTile elements per workgroup): short-lived workgroups keep the
 // end of the grid short, where a pure streaming pass otherwise loses bandwidth.
-constexpr uint32_t kRbTile = 4u * kNT;
+constexpr int kRbNT = 64;  // threads per workgroup (64: 47.2 us per step on ResNet-50 flat; 128: 48.2; 256: 48.6)
+constexpr uint32_t kRbTile = 4u * kRbNT;
 template <int GDT>
-__global__ __launch_bounds__(kNT) void k_randblock_step(Tables T, const void* g, float* e, uint32_t s0,
+__global__ __launch_bounds__(kRbNT) void k_randblock_step(Tables T, const void* g, float* e, uint32_t s0,
                                                         uint32_t s1, uint32_t step, uint32_t* start,
                                                         float* val) {
   const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)T.d, lo + kRbTile);
@@ -204,7 +205,7 @@ __global__ __launch_bounds__(kNT) void k_randblock_step(Tables T, const void* g,
   }
   store4(e, i0, nv, out);
   // start of every segment that begins in this group
-  for (int l = sf + (int)threadIdx.x; l <= sl; l += kNT) {
+  for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
     const uint32_t ol = (uint32_t)T.seg_off[l];
     if (ol >= lo && ol < hi)
       start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
@@ -1000,15 +1001,25 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws) {
 
 // ---------------------------------------------------------------------------------------------
 // Streaming pass: fused accumulate + candidate test + ordered compaction into the row's slot
-// (+ top-k: candidate histogram).  One workgroup per row.
+// (+ top-k: candidate histogram).  One workgroup of kStrNT threads per row, one float4 group per
+// thread (short-lived workgroups keep the end of the grid short, where a streaming pass loses
+// bandwidth).
 // ---------------------------------------------------------------------------------------------
+// Threads per workgroup of the streaming selection pass: two float4 groups per thread (a row of
+// kTile elements per workgroup).  Measured per pass on ResNet-50 flat, top-k / random-k: 256
+// threads (4 groups each) 52.0 / 52.2 us, 512 threads 50.5 / 51.0, 1024 threads 53.1 / 55.8 (one
+// barrier across 16 wavefronts holds the whole row back).
+constexpr int kStrNT = 512;
+constexpr int kStrW = kStrNT / 64;     // its wavefronts
+
 template <int KIND, int GDT, bool FUSED>
-__global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
+__global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
                                                     uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
-  __shared__ uint32_t wt[kRounds][kNT / 64];
+  constexpr int kSR = (int)kTile / (4 * kStrNT);  // float4 groups per thread
+  __shared__ uint32_t wt[kSR][kStrW];
   __shared__ uint32_t s_hist[KIND == 0 ? kHBins : 1];
   __shared__ uint32_t s_kk[KIND == 1 ? kTile : 1];  // random-k: the candidates' keys, by element
-  __shared__ uint32_t wc[kNT / 64];  // random-k, direct lists: certain winners per wavefront
+  __shared__ uint32_t wc[kStrW];  // random-k, direct lists: certain winners per wavefront
   __shared__ uint32_t s_und;         // random-k, direct lists: undecided candidates listed so far
   const uint32_t row = blockIdx.x;
   const int l = T.row_seg[row];
@@ -1032,51 +1043,51 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
     if (!direct && row == (uint32_t)T.seg_cbase[l] && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
   }
 
-  float v[kRounds][4];
-  uint32_t vm[kRounds];
+  float v[kSR][4];
+  uint32_t vm[kSR];
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) vm[r] = group_mask(tb + (uint32_t)(r * kNT + threadIdx.x) * 4u, lo, hi);
+  for (int r = 0; r < kSR; ++r) vm[r] = group_mask(tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u, lo, hi);
   const bool whole = lo == tb && hi == tb + kTile;  // the row is the whole tile (uniform)
   if constexpr (FUSED) {
-    float gv[kRounds][4];
+    float gv[kSR][4];
     if (whole) {
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      for (int r = 0; r < kSR; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
         load4gf<GDT>(g, i0, gv[r]);
         load4f(src, i0, v[r]);
       }
     } else {
 #pragma unroll
-      for (int r = 0; r < kRounds; ++r) {
-        const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      for (int r = 0; r < kSR; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
         load4gm<GDT>(g, i0, vm[r], gv[r]);
         load4m(src, i0, vm[r], v[r]);
       }
     }
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    for (int r = 0; r < kSR; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
       store4m(acc_out, i0, vm[r], v[r]);
     }
   } else {
 #pragma unroll
-    for (int r = 0; r < kRounds; ++r) {
-      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+    for (int r = 0; r < kSR; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
       if (whole) load4f(src, i0, v[r]);
       else load4m(src, i0, vm[r], v[r]);
     }
   }
   // candidate flags; wave-level prefixes through ballots, one barrier for the whole row
-  uint32_t mask[kRounds], lpre[kRounds];
-  uint32_t kk[kRounds][4];
+  uint32_t mask[kSR], lpre[kSR];
+  uint32_t kk[kSR][4];
   uint32_t ncert = 0;  // random-k, direct lists: certain winners of this wavefront (uniform)
   uint32_t cbits = 0;  // random-k, direct lists: bit 4r+q marks a certain winner (key below ulo)
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+  for (int r = 0; r < kSR; ++r) {
+    const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
     uint32_t mk = 0;
     if constexpr (KIND == 0) {
 #pragma unroll
@@ -1092,7 +1103,7 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
         for (int q = 0; q < 4; ++q) {
           if (((vm[r] >> q) & 1u) && (uint64_t)word(x, q) < tau) {
             mk |= 1u << q;
-            s_kk[(r * kNT + threadIdx.x) * 4 + q] = ~word(x, q);
+            s_kk[(r * kStrNT + threadIdx.x) * 4 + q] = ~word(x, q);
           }
           if (((vm[r] >> q) & 1u) && word(x, q) < ulo) cbits |= 1u << (4 * r + q);
         }
@@ -1103,7 +1114,7 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
             const uint32_t u = randk_key(i0 + q - o, (uint32_t)l, step, s0, s1);
             if ((uint64_t)u < tau) {
               mk |= 1u << q;
-              s_kk[(r * kNT + threadIdx.x) * 4 + q] = ~u;
+              s_kk[(r * kStrNT + threadIdx.x) * 4 + q] = ~u;
             }
             if (u < ulo) cbits |= 1u << (4 * r + q);
           }
@@ -1135,19 +1146,19 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
   float* cval = ws.cand_val + (size_t)row * kTile;
   uint32_t* ckey = ws.cand_key + (size_t)row * kTile;
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
+  for (int r = 0; r < kSR; ++r) {
     uint32_t rb = base;
 #pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) rb += w < wid ? wt[r][w] : 0u;
+    for (int w = 0; w < kStrW; ++w) rb += w < wid ? wt[r][w] : 0u;
     if (mask[r]) {
-      const uint32_t i0 = tb + (uint32_t)(r * kNT + threadIdx.x) * 4u;
+      const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
       uint32_t pos = rb + lpre[r];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if ((mask[r] >> q) & 1u) {
           uint32_t key;
           if constexpr (KIND == 0) key = kk[r][q];
-          else key = s_kk[(r * kNT + threadIdx.x) * 4 + q];
+          else key = s_kk[(r * kStrNT + threadIdx.x) * 4 + q];
           cidx[pos] = i0 + q;
           cval[pos] = v[r][q];
           ckey[pos] = key;
@@ -1163,35 +1174,35 @@ __global__ __launch_bounds__(kNT) void k_stream_sel(Tables T, const void* g, con
       }
     }
 #pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) base += wt[r][w];
+    for (int w = 0; w < kStrW; ++w) base += wt[r][w];
   }
   if (threadIdx.x == 0) ws.counts[row] = base;
   if (direct && threadIdx.x == 0) {
     // random-k, direct lists: the row's certain winners (key below ulo)
     uint32_t c = 0;
 #pragma unroll
-    for (int w = 0; w < kNT / 64; ++w) c += wc[w];
+    for (int w = 0; w < kStrW; ++w) c += wc[w];
     ws.rcnt[row] = c;
   }
   if constexpr (KIND == 0) {
     if (mode == 0 && base) {
       uint32_t* gh = ws.hist + ((size_t)l * kHCopies + (row % kHCopies)) * kHBins;
       if (base > kHistDirect) {  // many candidates: count them in LDS, then one atomic per used bin
-        for (int b = threadIdx.x; b < kHBins; b += kNT) s_hist[b] = 0;
+        for (int b = threadIdx.x; b < kHBins; b += kStrNT) s_hist[b] = 0;
         __syncthreads();
 #pragma unroll
-        for (int r = 0; r < kRounds; ++r)
+        for (int r = 0; r < kSR; ++r)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
             if ((mask[r] >> q) & 1u) atomicAdd(&s_hist[cand_bin(kk[r][q], A, sh)], 1u);
         __syncthreads();
-        for (int b = threadIdx.x; b < kHBins; b += kNT) {
+        for (int b = threadIdx.x; b < kHBins; b += kStrNT) {
           const uint32_t c = s_hist[b];
           if (c) atomicAdd(&gh[b], c);
         }
       } else {
 #pragma unroll
-        for (int r = 0; r < kRounds; ++r)
+        for (int r = 0; r < kSR; ++r)
 #pragma unroll
           for (int q = 0; q < 4; ++q)
             if ((mask[r] >> q) & 1u) atomicAdd(&gh[cand_bin(kk[r][q], A, sh)], 1u);

@@ -333,7 +333,7 @@ int check_ws(const ef_layout* L, int op, void* ws, size_t ws_bytes, WsLayout& wl
 // Top-k: sample -> candidate rule -> fused accumulate + candidates -> bin of the k-th ->
 // collect -> exact threshold and row offsets -> emission.
 int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint32_t* idx,
-             float* val, void* ws, size_t ws_bytes, void* stream) {
+             float* val, void* ws, size_t ws_bytes, void* stream, unsigned phases = EF_PHASE_ALL) {
   WsLayout wl;
   EF_TRY(check_ws(L, EF_OP_TOPK, ws, ws_bytes, wl));
   hipStream_t st = S(stream);
@@ -342,28 +342,24 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
   const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
   const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
   const dim3 pgrid((unsigned)L->nruns), pblk(kSampleRun);
-  if (g) {
-    if (g_dtype == EF_F32) {
-      EF_LAUNCH((k_sample_gather<0, true>), pgrid, pblk, 0, st, T, g, src, w);
-      EF_TRY(launched());
-      EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
-      EF_TRY(launched());
-      EF_LAUNCH((k_stream_sel<0, 0, true>), rgrid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
-    } else {
-      EF_LAUNCH((k_sample_gather<1, true>), pgrid, pblk, 0, st, T, g, src, w);
-      EF_TRY(launched());
-      EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
-      EF_TRY(launched());
-      EF_LAUNCH((k_stream_sel<0, 1, true>), rgrid, blk, 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
-    }
-  } else {
-    EF_LAUNCH((k_sample_gather<0, false>), pgrid, pblk, 0, st, T, nullptr, src, w);
+  if (phases & EF_PHASE_PREPARE) {  // the sample and the candidate rule
+    if (!g) EF_LAUNCH((k_sample_gather<0, false>), pgrid, pblk, 0, st, T, nullptr, src, w);
+    else if (g_dtype == EF_F32) EF_LAUNCH((k_sample_gather<0, true>), pgrid, pblk, 0, st, T, g, src, w);
+    else EF_LAUNCH((k_sample_gather<1, true>), pgrid, pblk, 0, st, T, g, src, w);
     EF_TRY(launched());
     EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
     EF_TRY(launched());
-    EF_LAUNCH((k_stream_sel<0, 0, false>), rgrid, blk, 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
   }
-  EF_TRY(launched());
+  if (phases & EF_PHASE_STREAM) {  // the streaming pass
+    if (!g)
+      EF_LAUNCH((k_stream_sel<0, 0, false>), rgrid, dim3(kStrNT), 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
+    else if (g_dtype == EF_F32)
+      EF_LAUNCH((k_stream_sel<0, 0, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+    else
+      EF_LAUNCH((k_stream_sel<0, 1, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
+    EF_TRY(launched());
+  }
+  if (!(phases & EF_PHASE_FINISH)) return EF_OK;
   if (!L->all_exact) {
     EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w);
     EF_TRY(launched());
@@ -388,7 +384,8 @@ int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, f
 // Random-k: fused accumulate + Philox candidates -> collect (certain winners counted, the window
 // [ulo, tau) listed) -> exact threshold and row offsets -> emission.
 int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint64_t seed,
-              uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream) {
+              uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream,
+              unsigned phases = EF_PHASE_ALL) {
   WsLayout wl;
   EF_TRY(check_ws(L, EF_OP_RANDK, ws, ws_bytes, wl));
   hipStream_t st = S(stream);
@@ -397,15 +394,17 @@ int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, 
   const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
   const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
-  if (g) {
-    if (g_dtype == EF_F32)
-      EF_LAUNCH((k_stream_sel<1, 0, true>), rgrid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
+  // (random-k has nothing to prepare: its keys do not depend on the data)
+  if (phases & EF_PHASE_STREAM) {  // the streaming pass
+    if (!g)
+      EF_LAUNCH((k_stream_sel<1, 0, false>), rgrid, dim3(kStrNT), 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
+    else if (g_dtype == EF_F32)
+      EF_LAUNCH((k_stream_sel<1, 0, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, s0, s1, step, w);
     else
-      EF_LAUNCH((k_stream_sel<1, 1, true>), rgrid, blk, 0, st, T, g, src, e_fused, s0, s1, step, w);
-  } else {
-    EF_LAUNCH((k_stream_sel<1, 0, false>), rgrid, blk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
+      EF_LAUNCH((k_stream_sel<1, 1, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, s0, s1, step, w);
+    EF_TRY(launched());
   }
-  EF_TRY(launched());
+  if (!(phases & EF_PHASE_FINISH)) return EF_OK;
   if (!L->rk_direct) {
     EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
     EF_TRY(launched());
@@ -632,6 +631,14 @@ int ef_step_topk(const ef_layout* L, const void* g, int g_dtype, float* e, uint3
   return run_topk(L, g, g_dtype, e, e, idx, val, ws, ws_bytes, stream);
 }
 
+int ef_step_topk_phases(const ef_layout* L, unsigned phases, const void* g, int g_dtype, float* e, uint32_t* idx,
+                        float* val, void* ws, size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  EF_TRY(check_g(g, g_dtype));
+  if (!vec_ok(e) || !word_ok(idx) || !word_ok(val) || phases == 0 || (phases & ~EF_PHASE_ALL)) return EF_EINVAL;
+  return run_topk(L, g, g_dtype, e, e, idx, val, ws, ws_bytes, stream, phases);
+}
+
 int compress_randk(const ef_layout* L, const float* acc, uint64_t seed, uint32_t step, uint32_t* idx, float* val,
                    void* ws, size_t ws_bytes, void* stream) {
   EF_TRY(check_bound(L));
@@ -645,6 +652,14 @@ int ef_step_randk(const ef_layout* L, const void* g, int g_dtype, float* e, uint
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !word_ok(idx) || !word_ok(val)) return EF_EINVAL;
   return run_randk(L, g, g_dtype, e, e, seed, step, idx, val, ws, ws_bytes, stream);
+}
+
+int ef_step_randk_phases(const ef_layout* L, unsigned phases, const void* g, int g_dtype, float* e, uint64_t seed,
+                         uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  EF_TRY(check_g(g, g_dtype));
+  if (!vec_ok(e) || !word_ok(idx) || !word_ok(val) || phases == 0 || (phases & ~EF_PHASE_ALL)) return EF_EINVAL;
+  return run_randk(L, g, g_dtype, e, e, seed, step, idx, val, ws, ws_bytes, stream, phases);
 }
 
 int compress_randblock(const ef_layout* L, const float* acc, uint64_t seed, uint32_t step, uint32_t* start,
@@ -662,7 +677,7 @@ int ef_step_randblock(const ef_layout* L, const void* g, int g_dtype, float* e, 
   EF_TRY(check_bound(L));
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !word_ok(start) || !word_ok(val)) return EF_EINVAL;
-  const dim3 grid((unsigned)((L->d + kRbTile - 1) / kRbTile)), blk(kNT);
+  const dim3 grid((unsigned)((L->d + kRbTile - 1) / kRbTile)), blk(kRbNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g_dtype == EF_F32)
     EF_LAUNCH(k_randblock_step<0>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);

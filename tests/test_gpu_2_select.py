@@ -245,3 +245,51 @@ def test_large_k_row_counting(offs, kind, ties):
     c = Case(offs, 0.6)
     g, e = _inputs(c.d, 31, ties=ties)
     _run_steps(c, kind, [g, g * np.float32(0.5)], e, seed=17, composed=False)
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+@pytest.mark.parametrize("two_streams", [False, True], ids=["one-stream", "two-streams"])
+def test_phased_step_matches_oracle(kind, two_streams):
+    """ef_step_*_phases: PREPARE, STREAM and FINISH as separate calls (the stream pass on a second
+    stream, ordered by events, when two_streams) give the fused step's result bit for bit, over
+    three steps with the residual carried; invalid phase masks are rejected."""
+    import paper_2009_09271_amd as E
+    import torch
+    announce("phased step", kind, two_streams)
+    offs = [0, 3, 8190, 8195, 16384, 16385, 16386, 30000, 100000]
+    c = Case(offs, 0.02)
+    rng = np.random.default_rng(5)
+    g = (rng.standard_normal(c.d) * 0.01).astype(np.float32)
+    e = np.zeros(c.d, np.float32)
+    ws = c.ws(E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK)
+    seed = (9 << 32) | 4
+    side = torch.cuda.Stream() if two_streams else torch.cuda.current_stream()
+    main = torch.cuda.current_stream()
+    gd = dev(g)
+    for step in range(3):
+        ed = dev(e)
+        idx = torch.empty(c.K, dtype=torch.int32, device="cuda")
+        val = torch.empty(c.K, dtype=torch.float32, device="cuda")
+
+        def phase(p):
+            if kind == "topk":
+                E.ef_step_topk_phases(c.L, p, gd, ed, idx, val, ws)
+            else:
+                E.ef_step_randk_phases(c.L, p, gd, ed, seed, step, idx, val, ws)
+
+        phase(E.EF_PHASE_PREPARE)
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            phase(E.EF_PHASE_STREAM)
+        main.wait_stream(side)
+        phase(E.EF_PHASE_FINISH)
+        (wm, wv), we = c.oracle_step(kind, g, e, seed, step)
+        assert_msg_equal(kind, (idx, val), (wm, wv), f"step {step}")
+        assert_f32_equal(ed, we, f"e' step {step}")
+        e = we
+    for bad in (0, 8, 15):
+        with pytest.raises(E.EfError):
+            if kind == "topk":
+                E.ef_step_topk_phases(c.L, bad, gd, ed, idx, val, ws)
+            else:
+                E.ef_step_randk_phases(c.L, bad, gd, ed, seed, 0, idx, val, ws)
