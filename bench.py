@@ -276,9 +276,32 @@ def main():
         for st in wstreams + [sA, astream]:
             cur.wait_stream(st)
 
-    def run_step(t, vs=None):
+    def run_step_serial(t, vs):
+        """Every worker step and aggregate one after another on stream A (per-kernel durations
+        without concurrency)."""
+        cur = torch.cuda.current_stream(dev)
+        sA.wait_stream(cur)
+        for v in vs:
+            kind, b = v
+            mi, mv = msg[vname(v)]
+            ev = e[vname(v)]
+            for w in range(W):
+                if kind == "randblock":
+                    E.ef_step_randblock(layouts[b], g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w], stream=sA)
+                elif kind == "topk":
+                    E.ef_step_topk_phases(lay0, E.EF_PHASE_ALL, g[w], ev[w], mi[w], mv[w], ws_topk[0], stream=sA)
+                else:
+                    E.ef_step_randk_phases(lay0, E.EF_PHASE_ALL, g[w], ev[w], worker_seed(wl, w), t, mi[w], mv[w],
+                                           ws_randk[0], stream=sA)
+            aggregate(v, sA)
+        cur.wait_stream(sA)
+
+    def run_step(t, vs=None, schedule=None):
         vs = vs or variants
-        if args.schedule == "fused":
+        schedule = schedule or args.schedule
+        if schedule == "serial":
+            return run_step_serial(t, vs)
+        if schedule == "fused":
             return run_step_fused(t, vs)
         return run_step_pipelined(t, vs)
 
@@ -366,24 +389,36 @@ def main():
         }
 
     # ---- per-kernel durations from library-recorded HIP events ---------------------------------
-    kernels, roofline = {}, None
-    if not args.no_kernel_timing:
+    # (1) the same schedule as the timed steps (the roofline kernel's launches); (2) every launch
+    # one after another on one stream (each kernel's duration without concurrency)
+    def kernel_table(schedule):
         E.timing_collect(reset=True)
         E.timing_enable(True)
-        for _ in range(args.steps):
-            run_step(step_no)
-            step_no += 1
+        nonlocal_step[0] = run_steps(nonlocal_step[0], args.steps, schedule)
         torch.cuda.synchronize()
         E.timing_enable(False)
         tm = E.timing_collect(reset=True)
+        table = {}
         for name, (tot_ms, n) in sorted(tm.items(), key=lambda kv: -kv[1][0]):
             avg_us = tot_ms * 1e3 / n
             ab = kernel_alg_bytes(name, d, K, L, W)
-            kernels[name] = {"avg_us": round(avg_us, 3), "launches": n, "total_ms": round(tot_ms, 3)}
+            table[name] = {"avg_us": round(avg_us, 3), "launches": n, "total_ms": round(tot_ms, 3)}
             if ab is not None:
-                kernels[name]["alg_bytes"] = ab
-                kernels[name]["alg_GBps"] = round(ab / (avg_us * 1e-6) / 1e9, 1)
-                kernels[name]["frac"] = round(ab / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+                table[name]["alg_bytes"] = ab
+                table[name]["alg_GBps"] = round(ab / (avg_us * 1e-6) / 1e9, 1)
+                table[name]["frac"] = round(ab / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        return table
+
+    def run_steps(t0, n, schedule):
+        for i in range(n):
+            run_step(t0 + i, schedule=schedule)
+        return t0 + n
+
+    nonlocal_step = [step_no]
+    kernels, kernels_serial, roofline = {}, {}, None
+    if not args.no_kernel_timing:
+        kernels = kernel_table(args.schedule)
+        kernels_serial = kernel_table("serial")
         dom = next(iter(kernels))
         ab = kernel_alg_bytes(dom, d, K, L, W)
         if ab is not None:
@@ -432,6 +467,7 @@ def main():
         "cpu_baseline": cpu,
         "per_compressor": per,
         "kernels": kernels,
+        "kernels_serial": kernels_serial,
         "input_generation_s": round(t_gen, 2),
     }
     print(json.dumps(line), flush=True)

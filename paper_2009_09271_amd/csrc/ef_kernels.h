@@ -420,12 +420,22 @@ __device__ __forceinline__ void agg_add_rest(AggLds& S, int nw, int w0, int32_t 
   }
 }
 
+// Workgroup b -> tile: workgroups are dispatched to the 8 XCDs in turn (b mod 8), so XCD x is
+// given the contiguous tiles [x q + min(x, r), ...) (q = n / 8, r = n mod 8; a bijection for any
+// n).  Neighbouring tiles share the cache lines of the range table and of the messages, and now
+// share an L2 as well.
+constexpr uint32_t kXcds = 8;
+__device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
+  const uint32_t x = b % kXcds, j = b / kXcds, q = n / kXcds, r = n % kXcds;
+  return x * q + min(x, r) + j;
+}
+
 __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
                                                    const uint32_t* idx, const float* val,
                                                    const uint32_t* tile_start, int average, float* out) {
   __shared__ AggLds S;
   const int lane = threadIdx.x;
-  const uint32_t t = blockIdx.x;
+  const uint32_t t = xcd_tile(blockIdx.x, (uint32_t)nt);  // the grid has exactly nt workgroups
   const uint32_t lo = t * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
   const bool pow2 = (W & (W - 1)) == 0;
   const float inv = 1.0f / (float)W;  // exact when W is a power of two
