@@ -34,6 +34,12 @@ Readings where the paper is silent (each is listed in the design doc):
 * aggregate: out_i = (sum over workers w = 0..W-1, in that order, of the
   entries present at i, starting from +0.0, in float32) / W, with IEEE
   float32 division; ``average=False`` gives the plain sum of Algorithm 1.
+  With shared coordinates (equal seeds) it is the same sum.
+* parameter update: x' = x - d with d = q (+ wd x) and, with momentum,
+  m' = beta m + d, d = m' (the order of a plain SGD step; the learning rate is
+  inside q), each float32 operation rounded on its own.
+* dense average (the uncompressed baseline): the same ordered sum over dense
+  gradients.
 
 Message formats: sparse messages are (idx uint32[K], val float32[K]) with
 segment l's entries at positions [P_l, P_l + k_l), P_l = sum of earlier k,
@@ -210,6 +216,62 @@ def decompress_aggregate_sparse(d, idx_stack, val_stack, average=True):
 def decompress_aggregate_block(d, seg_offsets, ks, start_stack, val_stack, average=True):
     sup = [block_support(seg_offsets, ks, st) for st in start_stack]
     return decompress_aggregate(d, sup, list(val_stack), average)
+
+
+def decompress_aggregate_shared_sparse(d, idx, val_stack, average=True):
+    """Shared coordinates (Section 3, the allReduce mode: every worker uses the
+    same seed, so every message has the same indices ``idx``): the aggregate is
+    the general one with that index list repeated for each worker."""
+    return decompress_aggregate(d, [idx] * len(val_stack), list(val_stack), average)
+
+
+def decompress_aggregate_shared_block(d, seg_offsets, ks, start, val_stack, average=True):
+    """Shared block starts (the allReduce mode of block-random-k)."""
+    sup = block_support(seg_offsets, ks, start)
+    return decompress_aggregate(d, [sup] * len(val_stack), list(val_stack), average)
+
+
+# ----------------------------------------------------------------------------
+# Algorithm 1, the parameter update x_{t+1} = x_t - q_t, with the momentum and
+# weight decay of the paper's training setup (Section 4, experimental setup) as
+# options.
+# ----------------------------------------------------------------------------
+def apply_update(x, q, m=None, beta=0.0, wd=0.0):
+    """One update of the parameters x by the aggregated step q, in float32 with
+    every operation rounded on its own (no fused multiply-add):
+
+        d = q + (wd * x)              when wd != 0
+        m' = (beta * m) + d, d = m'   when a momentum buffer m is given
+        x' = x - d
+
+    The learning rate is already inside q (the accumulate step scales g), so wd
+    is the learning rate times the weight-decay factor.  Returns (x', m')."""
+    f = np.float32
+    x = np.asarray(x, dtype=f)
+    d = np.asarray(q, dtype=f).copy()
+    if wd != 0.0:
+        d = d + (f(wd) * x).astype(f)
+    m_new = None
+    if m is not None:
+        m_new = (f(beta) * np.asarray(m, dtype=f)).astype(f) + d
+        d = m_new
+    return (x - d).astype(f), m_new
+
+
+# ----------------------------------------------------------------------------
+# Standard SGD's exchange (no compression), the paper's baseline (Section 4,
+# results): the dense average of the W workers' gradients.
+# ----------------------------------------------------------------------------
+def dense_average(G, average=True):
+    """out = (sum over workers w = 0..W-1, in that order, of the dense
+    gradients, from +0.0, in float32) / W."""
+    G = np.asarray(G, dtype=np.float32)
+    out = np.zeros(G.shape[1], dtype=np.float32)
+    for g in G:
+        out = out + g
+    if average:
+        out = out / np.float32(G.shape[0])
+    return out
 
 
 # ----------------------------------------------------------------------------

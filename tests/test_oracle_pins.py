@@ -389,3 +389,103 @@ def test_randblock_segment_not_longer_than_block_uses_unit_alignment():
     # one element more than b: aligned starts 0 and b only
     starts = {O.randblock_start(257, 3, 256, 4242, t) for t in range(200)}
     assert starts == {0, 256}
+
+
+# ----------------------------------------------------------------------------- shared coordinates
+def test_shared_sparse_aggregate_is_dense_sum_of_aligned_values():
+    """With one index list for every worker, the aggregate at idx[j] is the ordered float32 sum of
+    the workers' j-th values (a plain column sum of the [W][K] value matrix, worker by worker),
+    divided by W; zero elsewhere."""
+    rng = np.random.default_rng(3)
+    d, W, K = 500, 5, 37
+    idx = np.sort(rng.choice(d, K, replace=False)).astype(np.uint32)
+    V = (rng.standard_normal((W, K)) * 10.0 ** rng.integers(-3, 3, (W, 1))).astype(np.float32)
+    col = np.zeros(K, np.float32)
+    for w in range(W):
+        col = col + V[w]
+    want = np.zeros(d, np.float32)
+    want[idx.astype(np.int64)] = col / np.float32(W)
+    got = O.decompress_aggregate_shared_sparse(d, idx, V)
+    assert np.array_equal(bits(got), bits(want))
+
+
+def test_shared_block_aggregate_matches_general_with_repeated_starts():
+    offs = [0, 7, 100, 1000]
+    ks = O.segment_ks(offs, 0.1)
+    rng = np.random.default_rng(4)
+    start = np.array([3, 40, 512], dtype=np.uint32)
+    V = rng.standard_normal((3, sum(ks))).astype(np.float32)
+    a = O.decompress_aggregate_shared_block(1000, offs, ks, start, V)
+    b = O.decompress_aggregate_block(1000, offs, ks, [start] * 3, list(V))
+    assert np.array_equal(bits(a), bits(b))
+
+
+# ----------------------------------------------------------------------------- parameter update
+def test_apply_update_plain_is_subtraction():
+    """Algorithm 1's update without momentum or weight decay: x - q (NumPy's float32 subtract)."""
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal(1000).astype(np.float32)
+    q = (rng.standard_normal(1000) * 1e-3).astype(np.float32)
+    x2, m2 = O.apply_update(x, q)
+    assert m2 is None
+    assert np.array_equal(bits(x2), bits(np.subtract(x, q, dtype=np.float32)))
+
+
+def test_apply_update_exact_dyadic():
+    """Small dyadic values with beta = 1/2 and wd = 1/4: every operation is exact, so the result
+    equals the formula evaluated in float64."""
+    rng = np.random.default_rng(6)
+    x = rng.integers(-64, 64, 200).astype(np.float32) / 8
+    q = rng.integers(-64, 64, 200).astype(np.float32) / 16
+    m = rng.integers(-64, 64, 200).astype(np.float32) / 4
+    x2, m2 = O.apply_update(x, q, m, beta=0.5, wd=0.25)
+    d = q.astype(np.float64) + 0.25 * x.astype(np.float64)
+    mm = 0.5 * m.astype(np.float64) + d
+    assert np.array_equal(m2.astype(np.float64), mm)
+    assert np.array_equal(x2.astype(np.float64), x.astype(np.float64) - mm)
+
+
+def test_apply_update_matches_torch_sgd():
+    """Three steps with the buffer carried, against torch.optim.SGD on the CPU (lr = 1, momentum,
+    weight decay, no dampening): the same order of operations, within one float32 rounding of
+    each value (torch may fuse the weight-decay multiply-add)."""
+    import torch
+    rng = np.random.default_rng(7)
+    x = rng.standard_normal(4096).astype(np.float32)
+    p = torch.nn.Parameter(torch.from_numpy(x.copy()))
+    opt = torch.optim.SGD([p], lr=1.0, momentum=0.9, weight_decay=1e-4, dampening=0.0, nesterov=False)
+    m = np.zeros_like(x)
+    for t in range(3):
+        q = (rng.standard_normal(4096) * 1e-2).astype(np.float32)
+        p.grad = torch.from_numpy(q.copy())
+        opt.step()
+        x, m = O.apply_update(x, q, m, beta=0.9, wd=1e-4)
+        ref = p.detach().numpy()
+        assert np.allclose(x, ref, rtol=2 ** -22, atol=1e-7), f"step {t}"
+
+
+# ----------------------------------------------------------------------------- dense average
+def test_dense_average_exact_integers_match_numpy_sum():
+    """Integer-valued gradients: every partial sum is exact, so the ordered sum equals NumPy's sum
+    (any order) and the average its float32 division."""
+    rng = np.random.default_rng(8)
+    G = rng.integers(-1000, 1000, (6, 999)).astype(np.float32)
+    want = (G.astype(np.float64).sum(axis=0).astype(np.float32)) / np.float32(6)
+    assert np.array_equal(bits(O.dense_average(G)), bits(want))
+    assert np.array_equal(bits(O.dense_average(G, average=False)), bits(G.astype(np.float64).sum(axis=0).astype(np.float32)))
+
+
+def test_dense_average_worker_order_and_single_worker():
+    """(1 + 1e8) - 1e8 = 0 in float32 (the spacing at 1e8 is 8), while 1 + (1e8 - 1e8) = 1: the
+    sum runs in worker order.  One worker: the gradient itself (division by 1)."""
+    G = np.array([[1.0], [1e8], [-1e8]], np.float32)
+    assert O.dense_average(G, average=False)[0] == 0.0
+    g = np.random.default_rng(9).standard_normal((1, 50)).astype(np.float32)
+    assert np.array_equal(bits(O.dense_average(g)), bits(g[0]))
+
+
+def test_dense_average_close_to_float64_mean():
+    rng = np.random.default_rng(10)
+    G = rng.standard_normal((16, 5000)).astype(np.float32)
+    ref = G.astype(np.float64).mean(axis=0)
+    assert np.max(np.abs(O.dense_average(G) - ref)) < 16 * 2 ** -23 * np.max(np.abs(G).sum(axis=0))
