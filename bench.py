@@ -86,6 +86,54 @@ def kernel_alg_bytes(name, d, K, L, W):
     return None
 
 
+def measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, args, reps=20):
+    """Average duration and HBM fraction of: the shared-coordinate aggregates (allReduce mode, the
+    coordinates of worker 0's last message shared by all), the block aggregate fused with a
+    momentum update of the parameters, and the dense average of W uncompressed gradients."""
+    res = {}
+
+    def timed(name, fn, alg_bytes):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) * 1e3 / reps
+        res[name] = {"us": round(us, 3), "alg_bytes": int(alg_bytes),
+                     "frac_of_hbm_peak": round(alg_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    out = torch.empty(d, dtype=torch.float32, device=dev)
+    ws_sh = lay0.workspace(E.EF_OP_AGG_SHARED, W, dev)
+    kinds = {vname(v): v for v in variants}
+    if "randk" in kinds:
+        mi, mv = msg["randk"]
+        timed("shared_sparse_aggregate",
+              lambda: E.decompress_aggregate_shared(lay0, E.EF_MSG_SPARSE, W, mi[0], mv, out, ws_sh),
+              4 * d + W * 4 * K + 4 * K)
+    blk = [v for v in variants if v[0] == "randblock"]
+    if blk:
+        v = blk[0]
+        lay = layouts[v[1]]
+        mi, mv = msg[vname(v)]
+        timed(f"shared_block_aggregate_{vname(v)}",
+              lambda: E.decompress_aggregate_shared(lay, E.EF_MSG_BLOCK, W, mi[0], mv, out, ws_sh),
+              4 * d + W * 4 * K + 4 * L)
+        x = torch.zeros(d, dtype=torch.float32, device=dev)
+        m = torch.zeros(d, dtype=torch.float32, device=dev)
+        timed(f"aggregate_apply_momentum_{vname(v)}",
+              lambda: E.decompress_aggregate_apply(lay, E.EF_MSG_BLOCK, W, mi, mv, x, m, 0.9, 1e-5),
+              16 * d + W * (4 * K + 4 * L))
+        del x, m
+    G = torch.randn((W, d), dtype=torch.float32, device=dev)
+    timed("dense_average", lambda: E.ef_dense_average(lay0, W, G, out), (W + 1) * 4 * d)
+    del G
+    return res
+
+
 def cpu_baseline(wl, offs, ks, variants, W, grads, budget_note):
     """Time the CPU oracle on a bounded sample of worker steps plus one aggregate per variant,
     and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
@@ -149,6 +197,8 @@ def main():
     ap.add_argument("--variants", default="topk,randk,randblock")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-next", action="store_true", help="skip the shared-coordinate, fused-update and "
+                    "dense-average measurements")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="N",
                     help="first launch the library's plain copy kernel N times on d floats (a known "
                          "4d-byte read + 4d-byte write per launch) to calibrate HBM byte counters")
@@ -435,6 +485,9 @@ def main():
                         "traffic_source": os.path.relpath(tfile, os.path.dirname(os.path.abspath(__file__)))
                         if traffic is not None else None}
 
+    # ---- the paths next to the hot path, on the same workload (each alone, events on one stream) --
+    nxt = {} if args.no_next else measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, args)
+
     cpu = None
     if not args.no_cpu_baseline:
         ks = [int(k) for k in lay0.segment_k()]
@@ -468,6 +521,7 @@ def main():
         "per_compressor": per,
         "kernels": kernels,
         "kernels_serial": kernels_serial,
+        "next_rows": nxt,
         "input_generation_s": round(t_gen, 2),
     }
     print(json.dumps(line), flush=True)

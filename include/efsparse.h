@@ -75,6 +75,7 @@ extern "C" {
 #define EF_OP_RANDBLOCK 2
 #define EF_OP_AGG_SPARSE 3
 #define EF_OP_AGG_BLOCK 4
+#define EF_OP_AGG_SHARED 5
 
 /* message kinds */
 #define EF_MSG_SPARSE 0
@@ -128,8 +129,10 @@ int ef_layout_bind(ef_layout* layout, void* dev_tables, size_t bytes, void* stre
 
 /* Workspace bytes an entry point needs: EF_OP_TOPK for compress_topk /
  * ef_step_topk, EF_OP_RANDK for compress_randk / ef_step_randk,
- * EF_OP_AGG_SPARSE / EF_OP_AGG_BLOCK for decompress_aggregate with W workers
- * (W is ignored otherwise).  Random-block needs none (returns 0).
+ * EF_OP_AGG_SPARSE / EF_OP_AGG_BLOCK for decompress_aggregate and
+ * decompress_aggregate_apply with W workers, EF_OP_AGG_SHARED for
+ * decompress_aggregate_shared (W is ignored otherwise).  Random-block needs
+ * none (returns 0).
  * Returns 0 for a null layout or unknown op. */
 size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W);
 
@@ -179,6 +182,48 @@ int ef_update(const ef_layout* layout, const float* acc, int msg_kind, const uin
 int decompress_aggregate(const ef_layout* layout, int msg_kind, int32_t W,
                          const uint32_t* idx_or_start, const float* val, int average, float* out,
                          void* ws, size_t ws_bytes, void* stream);
+
+/* Algorithm 1, the aggregate step fused with the parameter update
+ * x_{t+1} = x_t - q_t that follows it, with the momentum and weight decay of
+ * the paper's training setup (Section 4, experimental setup) as options: the
+ * aggregate q of the W messages (as decompress_aggregate computes it) is
+ * applied to the parameters in the same pass over d elements.  Per element:
+ *   d = q + wd * x        (only when wd != 0; wd = learning rate x decay)
+ *   m = beta * m + d, d = m   (only when mom is not null)
+ *   x = x - d
+ * each float32 operation rounded on its own (no fused multiply-add); the
+ * learning rate is already inside q.  This is the order of a plain SGD step
+ * with momentum (no dampening, no Nesterov) at learning rate 1.
+ *   x     f32[d], updated in place;  mom  f32[d] or null (updated in place)
+ *   out   f32[d] or null: also receives q
+ * x, mom and out must be distinct buffers; beta and wd finite.  Workspace as
+ * for decompress_aggregate (EF_OP_AGG_SPARSE for sparse messages). */
+int decompress_aggregate_apply(const ef_layout* layout, int msg_kind, int32_t W,
+                               const uint32_t* idx_or_start, const float* val, int average, float* x,
+                               float* mom, float beta, float wd, float* out, void* ws, size_t ws_bytes,
+                               void* stream);
+
+/* Algorithm 1's aggregate step when the workers share coordinates (Section
+ * 3: equal seeds, the allReduce mode): every message has the same indices
+ * (sparse) or block starts (block), given once:
+ *   idx_or_start  uint32[K] (sparse) or uint32[n_seg] (block), as a message
+ *   val           float32[W][K], the workers' values at those coordinates
+ *   out           float32[d], written in full
+ * The result is bitwise that of decompress_aggregate on the W messages
+ * (coordinates repeated): the values are summed per coordinate in worker
+ * order from +0.0, then placed like one message and divided by W.  Needs
+ * ef_workspace_bytes(layout, EF_OP_AGG_SHARED, W) bytes of workspace. */
+int decompress_aggregate_shared(const ef_layout* layout, int msg_kind, int32_t W,
+                                const uint32_t* idx_or_start, const float* val, int average, float* out,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/* Standard SGD's exchange, the paper's uncompressed baseline (Section 4,
+ * results): out_i = fl32(sum over w = 0..W-1, in order, from +0.0, of
+ * g[w][i]) divided by W in IEEE float32 when average != 0.
+ *   g    float32[W][d] (the layout's d), contiguous
+ *   out  float32[d] */
+int ef_dense_average(const ef_layout* layout, int32_t W, const float* g, int average, float* out,
+                     void* stream);
 
 /* Fused worker steps: accumulate + compress + residual update in one call,
  * bitwise identical to ef_accumulate(g, e -> e), compress_*(e), ef_update(e, e).

@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("EFSPARSE_LIB") or os.path.join(_HERE, "libefsparse.so
 
 EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP = range(5)
 EF_F32, EF_BF16 = 0, 1
-EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK = range(5)
+EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK, EF_OP_AGG_SHARED = range(6)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
 EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA = range(4)
 EF_PHASE_PREPARE, EF_PHASE_STREAM, EF_PHASE_FINISH, EF_PHASE_ALL = 1, 2, 4, 7
@@ -29,7 +29,7 @@ DIAG_SLOW_PATH = 2
 DIAG_COUNT_MISMATCH = 4
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is not built: run `python -m paper_2009_09271_amd.build` "
+    raise ImportError(f"{LIB_PATH} is not built: run `python paper_2009_09271_amd/build.py` "
                       "(or __graft_entry__.build()) first")
 
 # Load PyTorch first so that the library binds to the same HIP runtime that
@@ -63,6 +63,11 @@ _SIGS = {
     "compress_randblock": (_c.c_int, [_P, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
     "ef_update": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P]),
     "decompress_aggregate": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_size_t, _P]),
+    "decompress_aggregate_apply": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_float,
+                                              _c.c_float, _P, _P, _c.c_size_t, _P]),
+    "decompress_aggregate_shared": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_size_t,
+                                               _P]),
+    "ef_dense_average": (_c.c_int, [_P, _c.c_int32, _P, _c.c_int, _P, _P]),
     "ef_step_topk": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randblock": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
@@ -221,6 +226,26 @@ def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, a
     _check(_lib.decompress_aggregate(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
                                      1 if average else 0, _ptr(out), _ptr(ws), n, _stream(out, stream)),
            "decompress_aggregate")
+
+
+def decompress_aggregate_apply(layout, msg_kind, W, idx_or_start, val, x, mom=None, beta=0.0, wd=0.0, out=None,
+                               ws=None, average=True, stream=None):
+    n = ws.numel() if ws is not None else 0
+    _check(_lib.decompress_aggregate_apply(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
+                                           1 if average else 0, _ptr(x), _ptr(mom), float(beta), float(wd),
+                                           _ptr(out), _ptr(ws), n, _stream(x, stream)),
+           "decompress_aggregate_apply")
+
+
+def decompress_aggregate_shared(layout, msg_kind, W, idx_or_start, val, out, ws, average=True, stream=None):
+    _check(_lib.decompress_aggregate_shared(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
+                                            1 if average else 0, _ptr(out), _ptr(ws), ws.numel(),
+                                            _stream(out, stream)), "decompress_aggregate_shared")
+
+
+def ef_dense_average(layout, W, g, out, average=True, stream=None):
+    _check(_lib.ef_dense_average(layout.handle, int(W), _ptr(g), 1 if average else 0, _ptr(out),
+                                 _stream(out, stream)), "ef_dense_average")
 
 
 def ef_step_topk(layout, g, e, idx, val, ws):

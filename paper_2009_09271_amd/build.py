@@ -1,6 +1,6 @@
 """Build libefsparse.so (HIP, gfx950) in-tree with hipcc.
 
-    python -m paper_2009_09271_amd.build      # or: python paper_2009_09271_amd/build.py
+    python paper_2009_09271_amd/build.py      # by path: importing the package needs a built library
 """
 
 import os

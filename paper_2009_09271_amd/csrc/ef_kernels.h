@@ -277,8 +277,26 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 constexpr uint32_t kAggTile = 1024;
 constexpr int kAggRounds = (int)kAggTile / (4 * 64);
 
+// Column sum over W rows of K values (shared coordinates): sum_u v[u K + j] in row order from +0.0,
+// loads of kSumBatch rows in flight together.
+constexpr int kSumBatch = 8;
+__device__ __forceinline__ float column_sum(const float* v, int32_t W, int32_t K, uint32_t j) {
+  float s = 0.0f;
+  for (int u0 = 0; u0 < W; u0 += kSumBatch) {
+    float t[kSumBatch];
+#pragma unroll
+    for (int u = 0; u < kSumBatch; ++u) t[u] = u0 + u < W ? v[(size_t)(u0 + u) * K + j] : 0.0f;
+#pragma unroll
+    for (int u = 0; u < kSumBatch; ++u)
+      if (u0 + u < W) s += t[u];
+  }
+  return s;
+}
+
 // tile_start[w][tau] = first entry of message w whose index lies in an aggregate tile >= tau
 // (tau = 0..nt; an index >= d counts as tile nt).  Grid: (ceil(K / kNT), W), one thread per entry.
+// With `sums` (shared coordinates: W = 1 message whose values are vW workers' rows `vals`), entry
+// j's thread also writes sums[j], the column sum of the rows in worker order.
 // Entry j starts the tiles after its predecessor's tile, up to its own (past the last entry the
 // tiles up to nt start at K).  A short run of tiles is written by its entry's thread; a longer one
 // (a gap in a message crowded into a few layers) by the whole workgroup as one coalesced run.
@@ -287,7 +305,8 @@ constexpr uint32_t kRunOwn = 128;  // runs of at most this many tiles are writte
                                    // longer ones (at most nt / 128 per message) by the workgroup
 
 __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
-                                                    uint32_t* tile_start) {
+                                                    uint32_t* tile_start, const float* vals, int32_t vW,
+                                                    float* sums) {
   __shared__ uint32_t s_nlong;
   __shared__ uint32_t s_ta[kNT], s_n[kNT], s_j[kNT], s_own[kNT];  // the workgroup's long runs
   const uint32_t j = blockIdx.x * kNT + threadIdx.x;
@@ -300,6 +319,8 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
     return e == (uint32_t)K - 1u && tau > e_own ? (uint32_t)K : e;
   };
   if (threadIdx.x == 0) s_nlong = 0;
+  // shared coordinates (one message for vW workers): also the column sums of their values
+  if (sums && w == 0 && j < (uint32_t)K) sums[j] = column_sum(vals, vW, K, j);
   __syncthreads();
   if (j < (uint32_t)K) {
     const uint32_t own = tile(m[j]);
@@ -338,6 +359,45 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
 // real number), and a multiply costs one instruction instead of a division sequence.
 __device__ __forceinline__ float agg_scale(float sum, int32_t W, bool pow2, float inv) {
   return pow2 ? sum * inv : __fdiv_rn(sum, (float)W);
+}
+
+// Output stage of the aggregates.  q = the worker sum, divided by wdiv when averaging.  q goes to
+// `out` when given; when `x` is given, Algorithm 1's parameter update is applied in the same pass:
+// d = q (+ wd x when wd != 0); with a momentum buffer m: m = beta m + d, d = m; then x = x - d
+// (each float32 operation rounded on its own).
+struct AggOut {
+  float* out;     // the aggregate, or nullptr
+  float* x;       // parameters to update, or nullptr
+  float* m;       // momentum buffer, or nullptr
+  float beta, wd;
+  int32_t wdiv;   // divisor of the average: the number of workers
+  int32_t average;
+};
+
+__device__ __forceinline__ void agg_emit4(const AggOut& O, uint32_t i0, int nv, const float sum[4]) {
+  const bool pow2 = (O.wdiv & (O.wdiv - 1)) == 0;
+  const float inv = 1.0f / (float)O.wdiv;  // exact when wdiv is a power of two
+  float q[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) q[j] = O.average ? agg_scale(sum[j], O.wdiv, pow2, inv) : sum[j];
+  if (O.out) store4(O.out, i0, nv, q);
+  if (O.x) {
+    float x[4], m[4];
+    load4(O.x, i0, nv, x);
+    if (O.m) load4(O.m, i0, nv, m);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float dj = q[j];
+      if (O.wd != 0.0f) dj = dj + O.wd * x[j];
+      if (O.m) {
+        m[j] = O.beta * m[j] + dj;
+        dj = m[j];
+      }
+      x[j] = x[j] - dj;
+    }
+    store4(O.x, i0, nv, x);
+    if (O.m) store4(O.m, i0, nv, m);
+  }
 }
 
 constexpr int kAggStarts = 1024;    // block starts (workers x segments of the tile) held in LDS
@@ -432,13 +492,11 @@ __device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
 
 __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
                                                    const uint32_t* idx, const float* val,
-                                                   const uint32_t* tile_start, int average, float* out) {
+                                                   const uint32_t* tile_start, AggOut O) {
   __shared__ AggLds S;
   const int lane = threadIdx.x;
   const uint32_t t = xcd_tile(blockIdx.x, (uint32_t)nt);  // the grid has exactly nt workgroups
   const uint32_t lo = t * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
-  const bool pow2 = (W & (W - 1)) == 0;
-  const float inv = 1.0f / (float)W;  // exact when W is a power of two
   // ranges of the first worker group (lane j: worker j; lanes past W read worker W - 1's)
   const int nw0 = min(W, 64);
   const uint32_t* ts = tile_start + (size_t)min(lane, nw0 - 1) * (nt + 1) + t;
@@ -451,7 +509,7 @@ __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t
       const uint32_t i0 = lo + (uint32_t)(r * 64 + lane) * 4u;
       const int n = i0 < hi ? (int)min(4u, hi - i0) : 0;
       const float z[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-      store4(out, i0, n, z);
+      agg_emit4(O, i0, n, z);
     }
     return;
   }
@@ -475,12 +533,8 @@ __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t
     const uint32_t i0 = lo + x;
     const int n = i0 < hi ? (int)min(4u, hi - i0) : 0;
     const f4 s4 = *reinterpret_cast<const f4*>(&S.acc[x]);
-    float v[4] = {s4.x, s4.y, s4.z, s4.w};
-    if (average) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = agg_scale(v[q], W, pow2, inv);
-    }
-    store4(out, i0, n, v);
+    const float v[4] = {s4.x, s4.y, s4.z, s4.w};
+    agg_emit4(O, i0, n, v);
   }
 }
 
@@ -490,12 +544,10 @@ __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t
 // ascending order, as in k_agg_block.
 template <int R>
 __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_t K, const uint32_t* start,
-                                                    const float* val, int average, float* out) {
+                                                    const float* val, AggOut O) {
   constexpr uint32_t kT = (uint32_t)R * 4u * kNT;
   const uint32_t lo = blockIdx.x * kT, hi = min((uint32_t)d, lo + kT);
   const uint32_t n = (uint32_t)d, k = (uint32_t)K;
-  const bool pow2 = (W & (W - 1)) == 0;
-  const float inv = 1.0f / (float)W;  // exact when W is a power of two
   const int lane = threadIdx.x & 63;
   float a[R][4];
 #pragma unroll
@@ -537,10 +589,7 @@ __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_
   for (int r = 0; r < R; ++r) {
     const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
     const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float v[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(a[r][q], W, pow2, inv) : a[r][q];
-    store4(out, i0, nv, v);
+    agg_emit4(O, i0, nv, a[r]);
   }
 }
 
@@ -554,12 +603,10 @@ __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_
 constexpr int kAggSegs = 64;
 
 __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t K, const uint32_t* start,
-                                                   const float* val, int average, float* out) {
+                                                   const float* val, AggOut O) {
   __shared__ uint32_t s_st[kAggStarts];
   __shared__ uint32_t s_seg[4][kAggSegs];  // o, n, k, P of the pass's segments
   int c_sf = -1, c_sl = -1;                // segments whose starts s_st holds (one pass, one group)
-  const bool pow2 = (W & (W - 1)) == 0;
-  const float inv = 1.0f / (float)W;  // exact when W is a power of two
   constexpr int kR = kRounds;
   for (uint32_t c = blockIdx.x; c < (uint32_t)T.nchunks; c += gridDim.x) {
     const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
@@ -639,12 +686,44 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
     for (int r = 0; r < kR; ++r) {
       const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
       const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-      float v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = average ? agg_scale(a[r][q], W, pow2, inv) : a[r][q];
-      store4(out, i0, nv, v);
+      agg_emit4(O, i0, nv, a[r]);
     }
   }
+}
+
+// Shared block starts: the column sums of the W workers' values (worker order, from +0.0).
+__global__ __launch_bounds__(kNT) void k_shared_sum(int32_t W, int32_t K, const float* val, float* sum) {
+  const uint32_t j = blockIdx.x * kNT + threadIdx.x;
+  if (j < (uint32_t)K) sum[j] = column_sum(val, W, K, j);
+}
+
+// Standard SGD's exchange (no compression): out = (sum over workers in order, from +0.0) / W of
+// the dense gradients g[W][d].  One float4 group per thread; the loads of kDenseBatch workers are
+// in flight together.
+constexpr int kDenseBatch = 8;
+__global__ __launch_bounds__(kNT) void k_dense_average(int32_t d, int32_t W, const float* g, int average,
+                                                       float* out) {
+  const uint32_t i0 = (blockIdx.x * kNT + threadIdx.x) * 4u;
+  if (i0 >= (uint32_t)d) return;
+  const int nv = (int)min(4u, (uint32_t)d - i0);
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int w0 = 0; w0 < W; w0 += kDenseBatch) {
+    float v[kDenseBatch][4];
+#pragma unroll
+    for (int u = 0; u < kDenseBatch; ++u)
+      if (w0 + u < W) load4(g + (size_t)(w0 + u) * d, i0, nv, v[u]);
+#pragma unroll
+    for (int u = 0; u < kDenseBatch; ++u)
+      if (w0 + u < W)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s[q] += v[u][q];
+  }
+  const bool pow2 = (W & (W - 1)) == 0;
+  const float inv = 1.0f / (float)W;
+  float o[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) o[q] = average ? agg_scale(s[q], W, pow2, inv) : s[q];
+  store4(out, i0, nv, o);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -595,6 +595,10 @@ size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W) {
       if (W < 1) return 0;
       return align_up((size_t)W * ((size_t)agg_tiles(layout->d) + 1) * 4, kAlign);
     case EF_OP_AGG_BLOCK: return 0;
+    case EF_OP_AGG_SHARED:
+      if (W < 1) return 0;
+      // the column sums and one message's tile ranges
+      return align_up((size_t)layout->K * 4, kAlign) + align_up(((size_t)agg_tiles(layout->d) + 1) * 4, kAlign);
     default: return 0;
   }
 }
@@ -709,13 +713,16 @@ int ef_update(const ef_layout* L, const float* acc, int msg_kind, const uint32_t
   return EF_EINVAL;
 }
 
-int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
-                         int average, float* out, void* ws, size_t ws_bytes, void* stream) {
-  EF_TRY(check_bound(L));
-  if (W < 1 || W > 65535) return EF_ERANGE;
-  if (!word_ok(m) || !word_ok(val) || !vec_ok(out)) return EF_EINVAL;
-  hipStream_t st = S(stream);
-  const dim3 grid((unsigned)L->nchunks), blk(kNT);
+}  // extern "C"
+
+namespace {
+
+// The aggregate of W messages through the output stage O (see AggOut).  With `sums` (shared
+// coordinates: W = 1 and val holds vW workers' rows), the ranges pass first writes the rows'
+// column sums there and the aggregate reads those.
+int run_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val, const AggOut& O,
+                  void* ws, size_t ws_bytes, hipStream_t st, int32_t vW = 0, float* sums = nullptr) {
+  const dim3 blk(kNT);
   if (msg_kind == EF_MSG_SPARSE) {
     const size_t need = ef_workspace_bytes(L, EF_OP_AGG_SPARSE, W);
     if (!ws || !aligned(ws, kAlign)) return EF_EINVAL;
@@ -723,24 +730,83 @@ int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint
     const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
     uint32_t* ts = reinterpret_cast<uint32_t*>(ws);
     const int32_t nt = agg_tiles(L->d);
-    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts);
+    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts,
+              val, vW, sums);
     EF_TRY(launched());
-    EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), dim3(64), 0, st, L->T.d, W, (int32_t)L->K, nt, m, val, ts, average,
-              out);
+    EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), dim3(64), 0, st, L->T.d, W, (int32_t)L->K, nt, m,
+              sums ? sums : val, ts, O);
     return launched();
   }
   if (msg_kind == EF_MSG_BLOCK) {
     if (L->L == 1) {
       constexpr uint32_t kT1 = 4u * kNT;  // one float4 group per thread
       EF_LAUNCH(k_agg_block1<1>, dim3((unsigned)((L->d + kT1 - 1) / kT1)), blk, 0, st, L->T.d, W, (int32_t)L->K,
-                m, val, average, out);
+                m, val, O);
       return launched();
     }
     const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks((const void*)k_agg_block, kNT));
-    EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, average, out);
+    EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, O);
     return launched();
   }
   return EF_EINVAL;
+}
+
+}  // namespace
+
+extern "C" {
+
+int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
+                         int average, float* out, void* ws, size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!word_ok(m) || !word_ok(val) || !vec_ok(out)) return EF_EINVAL;
+  const AggOut O{out, nullptr, nullptr, 0.0f, 0.0f, W, average ? 1 : 0};
+  return run_aggregate(L, msg_kind, W, m, val, O, ws, ws_bytes, S(stream));
+}
+
+int decompress_aggregate_apply(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
+                               int average, float* x, float* mom, float beta, float wd, float* out, void* ws,
+                               size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!word_ok(m) || !word_ok(val) || !vec_ok(x) || (mom && !vec_ok(mom)) || (out && !vec_ok(out)))
+    return EF_EINVAL;
+  if (!std::isfinite(beta) || !std::isfinite(wd)) return EF_EINVAL;
+  if (mom == x || (out && (out == x || out == mom))) return EF_EINVAL;
+  const AggOut O{out, x, mom, beta, wd, W, average ? 1 : 0};
+  return run_aggregate(L, msg_kind, W, m, val, O, ws, ws_bytes, S(stream));
+}
+
+int decompress_aggregate_shared(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
+                                int average, float* out, void* ws, size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!word_ok(m) || !word_ok(val) || !vec_ok(out)) return EF_EINVAL;
+  if (msg_kind != EF_MSG_SPARSE && msg_kind != EF_MSG_BLOCK) return EF_EINVAL;
+  if (!ws || !aligned(ws, kAlign)) return EF_EINVAL;
+  if (ws_bytes < ef_workspace_bytes(L, EF_OP_AGG_SHARED, W)) return EF_EWORKSPACE;
+  // one message (the shared coordinates) whose values are the column sums of the W workers'
+  // values in worker order, divided by W
+  hipStream_t st = S(stream);
+  float* sum = reinterpret_cast<float*>(ws);
+  void* ws1 = reinterpret_cast<uint8_t*>(ws) + align_up((size_t)L->K * 4, kAlign);
+  const size_t ws1_bytes = ws_bytes - align_up((size_t)L->K * 4, kAlign);
+  const AggOut O{out, nullptr, nullptr, 0.0f, 0.0f, W, average ? 1 : 0};
+  if (msg_kind == EF_MSG_SPARSE) return run_aggregate(L, msg_kind, 1, m, val, O, ws1, ws1_bytes, st, W, sum);
+  EF_LAUNCH(k_shared_sum, dim3((unsigned)(((size_t)L->K + kNT - 1) / kNT)), dim3(kNT), 0, st, W, (int32_t)L->K, val,
+            sum);
+  EF_TRY(launched());
+  return run_aggregate(L, msg_kind, 1, m, sum, O, ws1, ws1_bytes, st);
+}
+
+int ef_dense_average(const ef_layout* L, int32_t W, const float* g, int average, float* out, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!vec_ok(g) || !vec_ok(out)) return EF_EINVAL;
+  const size_t groups = ((size_t)L->d + 3) / 4;
+  EF_LAUNCH(k_dense_average, dim3((unsigned)((groups + kNT - 1) / kNT)), dim3(kNT), 0, S(stream), L->T.d, W, g,
+            average ? 1 : 0, out);
+  return launched();
 }
 
 }  // extern "C"
