@@ -202,8 +202,9 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="N",
                     help="first launch the library's plain copy kernel N times on d floats (a known "
                          "4d-byte read + 4d-byte write per launch) to calibrate HBM byte counters")
-    ap.add_argument("--schedule", default="fused", choices=["fused", "pipelined"],
-                    help="fused: each top-k / random-k worker step on one of --worker-streams streams; "
+    ap.add_argument("--schedule", default="batch", choices=["batch", "fused", "pipelined"],
+                    help="batch: each variant's W top-k / random-k steps in one ef_step_*_batch call; "
+                         "fused: each top-k / random-k worker step on one of --worker-streams streams; "
                          "pipelined: its phases split over a streaming stream and two selection streams")
     ap.add_argument("--worker-streams", type=int, default=3)
     ap.add_argument("--streams", type=int, default=3,
@@ -241,7 +242,7 @@ def main():
     lay0 = next(iter(layouts.values()))
     K, L = lay0.K, lay0.n_seg
 
-    g = [torch.from_numpy(x).to(dev) for x in grads]
+    g = [torch.from_numpy(x).to(dev) for x in grads]  # separate allocations
     if args.calibrate_copy:
         src_c = torch.randn(d, device=dev)
         dst_c = torch.empty(d, device=dev)
@@ -251,11 +252,14 @@ def main():
         torch.cuda.synchronize()
         del src_c, dst_c, none
     e = {vname(v): [torch.zeros(d, dtype=torch.float32, device=dev) for _ in range(W)] for v in variants}
-    msg = {}
+    # two message buffers per variant, alternating by step, so that a step's aggregate can run while
+    # the next step's workers write their messages
+    msg_bufs = {}
     for v in variants:
         n_m = L if v[0] == "randblock" else K
-        msg[vname(v)] = (torch.empty((W, n_m), dtype=torch.int32, device=dev),
-                         torch.empty((W, K), dtype=torch.float32, device=dev))
+        msg_bufs[vname(v)] = [(torch.empty((W, n_m), dtype=torch.int32, device=dev),
+                               torch.empty((W, K), dtype=torch.float32, device=dev)) for _ in range(2)]
+    msg = {k: b[0] for k, b in msg_bufs.items()}  # the current step's buffers (set by run_step)
     out = {vname(v): torch.empty(d, dtype=torch.float32, device=dev) for v in variants}
     # workspace slots of the top-k / random-k steps in flight
     S = max(4, args.streams) if args.schedule == "pipelined" else max(1, args.streams)
@@ -263,6 +267,11 @@ def main():
     ws_topk = [lay0.workspace(E.EF_OP_TOPK, 1, dev) for _ in range(S)] if "topk" in kinds else None
     ws_randk = [lay0.workspace(E.EF_OP_RANDK, 1, dev) for _ in range(S)] if "randk" in kinds else None
     ws_agg = lay0.workspace(E.EF_OP_AGG_SPARSE, W, dev)
+    wsb = {}
+    if args.schedule == "batch":
+        for k, op in (("topk", E.EF_OP_TOPK), ("randk", E.EF_OP_RANDK)):
+            if k in kinds:
+                wsb[k] = E.batch_workspace(lay0, op, W, dev)
     # stream A: the streaming passes; streams B0 / B1: the selection phases of even / odd workers;
     # one stream for the aggregates (all at the default priority)
     sA, astream = torch.cuda.Stream(dev), torch.cuda.Stream(dev)
@@ -346,11 +355,55 @@ def main():
             aggregate(v, sA)
         cur.wait_stream(sA)
 
+    seeds = [worker_seed(wl, w) for w in range(W)]
+
+    agg_done = [torch.cuda.Event(), torch.cuda.Event()]
+
+    def run_step_batch(t, vs):
+        """Each variant's W worker steps on stream A, one after another (block-random-k: W one-kernel
+        steps; top-k / random-k: one ef_step_*_batch call, whose streaming passes run back to back and
+        whose selection kernels run once for all W workers).  Each variant's aggregate runs on a
+        second stream, overlapping the next variant's workers; message buffers alternate by step, and
+        a step's workers only wait for the aggregates of two steps before."""
+        sA.wait_event(agg_done[t % 2])
+        for v in vs:
+            kind, b = v
+            mi, mv = msg[vname(v)]
+            ev = e[vname(v)]
+            if kind == "randblock":
+                for w in range(W):
+                    E.ef_step_randblock(layouts[b], g[w], ev[w], seeds[w], t, mi[w], mv[w], stream=sA)
+            elif kind == "topk":
+                E.ef_step_topk_batch(lay0, g, ev, mi, mv, wsb["topk"][0], wsb["topk"][1], stream=sA)
+            else:
+                E.ef_step_randk_batch(lay0, g, ev, seeds, t, mi, mv, wsb["randk"][0], wsb["randk"][1], stream=sA)
+            astream.wait_stream(sA)
+            aggregate(v, astream)
+        agg_done[t % 2].record(astream)
+
+    def run_variant_alone(t, v):
+        """One variant by itself: its W worker steps and its aggregate, all on stream A."""
+        kind, b = v
+        mi, mv = msg[vname(v)]
+        ev = e[vname(v)]
+        if kind == "randblock":
+            for w in range(W):
+                E.ef_step_randblock(layouts[b], g[w], ev[w], seeds[w], t, mi[w], mv[w], stream=sA)
+        elif kind == "topk":
+            E.ef_step_topk_batch(lay0, g, ev, mi, mv, wsb["topk"][0], wsb["topk"][1], stream=sA)
+        else:
+            E.ef_step_randk_batch(lay0, g, ev, seeds, t, mi, mv, wsb["randk"][0], wsb["randk"][1], stream=sA)
+        aggregate(v, sA)
+
     def run_step(t, vs=None, schedule=None):
         vs = vs or variants
         schedule = schedule or args.schedule
+        for k, bufs in msg_bufs.items():
+            msg[k] = bufs[t % 2]
         if schedule == "serial":
             return run_step_serial(t, vs)
+        if schedule == "batch":
+            return run_step_batch(t, vs)
         if schedule == "fused":
             return run_step_fused(t, vs)
         return run_step_pipelined(t, vs)
@@ -402,31 +455,40 @@ def main():
             cur.wait_stream(st)
 
     step_no = 0
-    for _ in range(args.warmup):
-        run_step(step_no)
-        step_no += 1
+    with torch.cuda.stream(sA):
+        for _ in range(args.warmup):
+            run_step(step_no)
+            step_no += 1
     torch.cuda.synchronize()
 
     # ---- timed region: exactly `steps` steps --------------------------------------------------
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run_step(step_no)
-        step_no += 1
+    with torch.cuda.stream(sA):
+        for _ in range(args.steps):
+            run_step(step_no)
+            step_no += 1
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed * 1e3 / args.steps
     elems_per_step = len(variants) * W * d
     value = elems_per_step / (ms_per_step / 1e3)
 
-    # ---- per-variant breakdown: the same schedule with one variant at a time ----------------
+    # ---- per-variant breakdown: each variant alone (batch schedule: its W steps and aggregate on
+    # one stream; other schedules: their own schedule with one variant) -------------------------
     per = {}
     for v in variants:
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        for _ in range(args.steps):
-            run_step(step_no, [v])
-            step_no += 1
+        with torch.cuda.stream(sA):
+            for _ in range(args.steps):
+                if args.schedule == "batch":
+                    for k, bufs in msg_bufs.items():
+                        msg[k] = bufs[step_no % 2]
+                    run_variant_alone(step_no, v)
+                else:
+                    run_step(step_no, [v])
+                step_no += 1
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t1) * 1e3 / args.steps
         step_b, agg_b = alg_bytes_op(v[0], d, K, L, W)
@@ -460,8 +522,9 @@ def main():
         return table
 
     def run_steps(t0, n, schedule):
-        for i in range(n):
-            run_step(t0 + i, schedule=schedule)
+        with torch.cuda.stream(sA):
+            for i in range(n):
+                run_step(t0 + i, schedule=schedule)
         return t0 + n
 
     nonlocal_step = [step_no]
@@ -513,8 +576,12 @@ def main():
                          f"+ one aggregate per variant per step"),
             "d": d, "segments": L, "K": K, "W": W, "density": density,
             "variants": [vname(v) for v in variants], "scope": args.scope,
-            "streams": "streaming passes on one stream, selection phases on a second, aggregates on a "
-                       f"third; {S} workspace slots",
+            "schedule": {"batch": "each variant's W steps on one stream (top-k / random-k: one ef_step_*_batch "
+                                  "call); aggregates on a second stream",
+                         "fused": f"top-k / random-k worker steps on {args.worker_streams} streams; aggregates "
+                                  "on another",
+                         "pipelined": "streaming phases on one stream, selection phases on two more, aggregates "
+                                      "on another"}[args.schedule],
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -262,6 +262,31 @@ int ef_step_randk_phases(const ef_layout* layout, unsigned phases, const void* g
                          uint64_t seed, uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes,
                          void* stream);
 
+/* The fused top-k / random-k steps of W workers (or W gradient buckets of
+ * one layout) in one call: with phases = EF_PHASE_ALL, bitwise W calls of
+ * ef_step_topk / ef_step_randk.  The workers' streaming passes run back to
+ * back and every selection kernel runs once for up to 64 workers (the worker
+ * is the grid's second dimension), so the short latency-bound selection
+ * steps are paid once per batch rather than once per worker.
+ *   phases as for ef_step_*_phases, applied to all W workers: the phases of
+ *         one batch called in order (ordered as there) give the same result
+ *   g     host array of W device pointers: worker w's gradient, f32 or bf16[d]
+ *   e     host array of W device pointers: worker w's residual f32[d], e_t on
+ *         entry and e_{t+1} on return
+ *   seeds random-k: host array of W seeds (worker w's seed); step as above
+ *   idx   uint32[W][K], val float32[W][K]: worker w's message is row w
+ *   ws    W workspaces, worker w's at ws + w * ws_stride; ws_stride a
+ *         multiple of 256 and >= ef_workspace_bytes(layout, op, 1)
+ * The host arrays are read during the call only.  (Each worker's g and e are
+ * separate pointers: streaming over rows of two very large allocations
+ * measured about 13 % slower here than over separate allocations.) */
+int ef_step_topk_batch(const ef_layout* layout, unsigned phases, int32_t W, const void* const* g,
+                       int g_dtype, float* const* e, uint32_t* idx, float* val, void* ws,
+                       size_t ws_stride, void* stream);
+int ef_step_randk_batch(const ef_layout* layout, unsigned phases, int32_t W, const void* const* g,
+                        int g_dtype, float* const* e, const uint64_t* seeds, uint32_t step, uint32_t* idx,
+                        float* val, void* ws, size_t ws_stride, void* stream);
+
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could
  * not contain the answer and the exact whole-segment path ran instead (a

@@ -71,6 +71,9 @@ _SIGS = {
     "ef_step_topk": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randblock": (_c.c_int, [_P, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P]),
+    "ef_step_topk_batch": (_c.c_int, [_P, _c.c_uint, _c.c_int32, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randk_batch": (_c.c_int, [_P, _c.c_uint, _c.c_int32, _P, _c.c_int, _P, _P, _c.c_uint32, _P, _P, _P,
+                                       _c.c_size_t, _P]),
     "ef_step_topk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P,
                                         _c.c_size_t, _P]),
@@ -267,6 +270,37 @@ def ef_step_randk_phases(layout, phases, g, e, seed, step, idx, val, ws, stream=
     _check(_lib.ef_step_randk_phases(layout.handle, int(phases), _ptr(g), _gdt(g), _ptr(e), int(seed), int(step),
                                      _ptr(idx), _ptr(val), _ptr(ws), ws.numel(), _stream(e, stream)),
            "ef_step_randk_phases")
+
+
+def batch_workspace(layout, op, W, device="cuda"):
+    """W zero-filled workspaces for ef_step_*_batch, one row of `stride` bytes each: (tensor, stride)."""
+    import torch
+    stride = (max(layout.workspace_bytes(op, 1), 256) + 255) // 256 * 256
+    return torch.zeros((W, stride), dtype=torch.uint8, device=device), stride
+
+
+def _ptr_table(tensors):
+    return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+
+
+def ef_step_topk_batch(layout, g, e, idx, val, ws, ws_stride, phases=EF_PHASE_ALL, stream=None):
+    """W workers' fused top-k steps: g, e lists of W tensors; idx, val [W][K] (rows of the batch); ws rows
+    from batch_workspace."""
+    if len(g) != len(e):
+        raise ValueError("one gradient and one residual per worker")
+    _check(_lib.ef_step_topk_batch(layout.handle, int(phases), len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
+                                   _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride), _stream(e[0], stream)),
+           "ef_step_topk_batch")
+
+
+def ef_step_randk_batch(layout, g, e, seeds, step, idx, val, ws, ws_stride, phases=EF_PHASE_ALL, stream=None):
+    """W workers' fused random-k steps; seeds: W integers (host)."""
+    sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64))
+    if len(g) != len(e) or sd.shape != (len(e),):
+        raise ValueError("one gradient, one residual and one seed per worker")
+    _check(_lib.ef_step_randk_batch(layout.handle, int(phases), len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
+                                    sd.ctypes.data, int(step), _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride),
+                                    _stream(e[0], stream)), "ef_step_randk_batch")
 
 
 def ef_step_randblock(layout, g, e, seed, step, start, val, stream=None):

@@ -52,6 +52,44 @@ struct WSel {
 
 __device__ __forceinline__ uint32_t* res_of(const WSel& w, int l) { return w.res + (size_t)l * kResWords; }
 
+// Several workers' steps in one launch of a selection kernel: worker blockIdx.y's buffers.  The
+// gradient and residual of each worker are separate allocations (pointer tables); workspaces and
+// messages lie at fixed strides from worker 0's.
+constexpr int kBatchMax = 64;  // workers per launch of the selection kernels
+struct Batch {
+  uint64_t ws;                   // bytes between the workers' workspaces
+  uint32_t msg;                  // entries between the workers' messages
+  const void* g[kBatchMax];      // each worker's gradient (null: compress only)
+  const float* src[kBatchMax];   // each worker's input: the residual e (fused steps) or acc
+  float* e[kBatchMax];           // each worker's residual to update (null: compress only)
+  uint32_t seed_lo[kBatchMax], seed_hi[kBatchMax];  // random-k: each worker's seed
+};
+
+template <typename P>
+__device__ __forceinline__ P* shifted(P* p, uint64_t bytes) {
+  return p ? reinterpret_cast<P*>(reinterpret_cast<uint8_t*>(const_cast<void*>(static_cast<const void*>(p))) + bytes)
+           : p;
+}
+
+__device__ __forceinline__ WSel ws_at(WSel w, uint64_t off) {
+  if (off == 0) return w;
+  w.diag = shifted(w.diag, off);
+  w.res = shifted(w.res, off);
+  w.hist = shifted(w.hist, off);
+  w.samp = shifted(w.samp, off);
+  w.counts = shifted(w.counts, off);
+  w.rcnt = shifted(w.rcnt, off);
+  w.roff = shifted(w.roff, off);
+  w.rtie = shifted(w.rtie, off);
+  w.lcnt = shifted(w.lcnt, off);
+  w.cand_idx = shifted(w.cand_idx, off);
+  w.cand_val = shifted(w.cand_val, off);
+  w.cand_key = shifted(w.cand_key, off);
+  w.list_idx = shifted(w.list_idx, off);
+  w.list_key = shifted(w.list_key, off);
+  return w;
+}
+
 // Random-k, direct lists: row r's undecided candidates as (key', index) pairs in the list_idx slot
 // of the row (kTile words hold kRowPairs pairs).
 constexpr uint32_t kRowPairs = kTile / 2;
@@ -978,7 +1016,10 @@ __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t 
 // its candidate histogram (kHCopies * kHBins = kSampleMax words, one slice per run).
 static_assert(kHCopies * kHBins == kSampleMax, "one histogram slice per sample run");
 template <int GDT, bool FUSED>
-__global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, const void* g, const float* src, WSel ws) {
+__global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
+  const void* g = BT.g[blockIdx.y];
+  const float* src = BT.src[blockIdx.y];
   const uint32_t r = blockIdx.x;
   const int l = seg_of(r, 0, T.L - 1, T.seg_ro);
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
@@ -1014,7 +1055,8 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, const vo
 //    keys above A, sh chosen so that the range up to the urank-th sampled key (the expected rank
 //    minus the margin) spans about 1024 bins: the k_l-th key very likely falls inside it, and the
 //    bins there are as narrow as the sample allows (mode 0).
-__global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws) {
+__global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[kHBins];
   __shared__ uint32_t hist2[kHBins];
@@ -1302,7 +1344,8 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
 
 // Top-k, per segment: the histogram bin B holding the k_l-th best candidate and how many winners
 // it still has to give; fewer than k_l candidates in all marks the segment for the exact path.
-__global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws) {
+__global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t hist[kHBins];
   __shared__ uint32_t lds[2 * kSelNT / 64];
   const int l = blockIdx.x;
@@ -1339,7 +1382,8 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws) {
 // r % kSubLists, which spreads the atomics on the list counters).  Top-k: above / inside bin B of
 // a histogrammed segment.  Random-k: Philox key below ulo_l / in [ulo_l, tau_l).
 template <int KIND>
-__global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws) {
+__global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t lds[kNT / 64];
   __shared__ uint32_t s_base;
   const uint32_t row = blockIdx.x;
@@ -1517,9 +1561,14 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
 // winners are then counted by k_rowcount and scanned by k_rowscan, both spread over many
 // workgroups, instead of one workgroup adding the list's winners to their rows.
 template <int KIND, bool BIG>
-__global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const float* data, float* e_zero,
-                                                   uint32_t* out_idx, float* out_val, uint32_t s0, uint32_t s1,
-                                                   uint32_t step) {
+__global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t* out_idx, float* out_val,
+                                                   uint32_t step, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
+  float* e_zero = BT.e[blockIdx.y];
+  const float* data = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];  // acc
+  out_idx = shifted(out_idx, (uint64_t)blockIdx.y * BT.msg * 4u);
+  out_val = shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u);
+  const uint32_t s0 = BT.seed_lo[blockIdx.y], s1 = BT.seed_hi[blockIdx.y];
   constexpr uint32_t kPer = kSelPer;  // rows per thread held in registers (more are re-read)
   __shared__ uint32_t hist[kHBins];
   __shared__ uint32_t lds[3 * kSelNT / 64];
@@ -1756,7 +1805,8 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws, const floa
 
 // Large layouts, per row: how many of the row's candidates win (all of them in mode 1).
 template <int KIND>
-__global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws) {
+__global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t lds[kNT / 64];
   const uint32_t row = blockIdx.x;
   const int l = T.row_seg[row];
@@ -1783,7 +1833,8 @@ __global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws) {
 // Large layouts, per segment: message offset of every row (exclusive scan of the winner counts),
 // in tiles of kSelNT * 8 rows: coalesced loads into LDS, eight consecutive rows per thread, a
 // workgroup scan, coalesced stores.
-__global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws) {
+__global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   constexpr uint32_t kU = 8, kTl = kSelNT * kU;
   __shared__ uint32_t lds[2 * kSelNT / 64];
   __shared__ uint32_t s_c[kTl + kTl / 32];
@@ -1834,7 +1885,11 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws) {
 // Per row, one wavefront each (kNT / 64 rows per workgroup, no workgroup barriers): the winners,
 // in index order, to the message at the row's offset; e = +0 there.
 constexpr uint32_t kEmitRows = kNT / 64;
-__global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws, float* e_zero, uint32_t* out_idx, float* out_val) {
+__global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT) {
+  const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
+  float* e_zero = BT.e[blockIdx.y];
+  out_idx = shifted(out_idx, (uint64_t)blockIdx.y * BT.msg * 4u);
+  out_val = shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u);
   const uint32_t row = blockIdx.x * kEmitRows + (threadIdx.x >> 6);
   if (row >= (uint32_t)T.nrows) return;
   const int lane = threadIdx.x & 63;

@@ -330,98 +330,150 @@ int check_ws(const ef_layout* L, int op, void* ws, size_t ws_bytes, WsLayout& wl
   return EF_OK;
 }
 
-// Top-k: sample -> candidate rule -> fused accumulate + candidates -> bin of the k-th ->
+// The steps of W workers (one for the single-worker entry points): each worker's gradient and
+// residual by pointer (host tables), messages of K entries and workspaces ws_stride bytes apart.
+struct Steps {
+  int32_t W = 1;
+  const void* const* g = nullptr;  // [W]; null table: compress only (acc = src)
+  int g_dtype = EF_F32;
+  const float* const* src = nullptr;  // [W]: acc (compress) or e (fused step)
+  float* const* e = nullptr;          // [W] or null table (compress)
+  uint32_t* idx = nullptr;
+  float* val = nullptr;
+  uint8_t* ws = nullptr;
+  size_t ws_bytes = 0;  // per worker
+  size_t ws_stride = 0;
+  const uint64_t* seeds = nullptr;  // random-k, host array [W]
+  uint32_t step = 0;
+};
+
+// Top-k (KIND 0): sample -> candidate rule -> fused accumulate + candidates -> bin of the k-th ->
 // collect -> exact threshold and row offsets -> emission.
-int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint32_t* idx,
-             float* val, void* ws, size_t ws_bytes, void* stream, unsigned phases = EF_PHASE_ALL) {
+// Random-k (KIND 1): fused accumulate + Philox candidates -> collect (certain winners counted, the
+// window [ulo, tau) listed; on direct layouts by the streaming pass itself) -> exact threshold and
+// row offsets -> emission.
+// Each phase runs for all W workers before the next: the streaming passes one launch per worker,
+// every other kernel once per kBatchMax workers (the worker is the grid's second dimension), so
+// the short latency-bound selection kernels are paid once for the batch.
+template <int KIND>
+int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream) {
   WsLayout wl;
-  EF_TRY(check_ws(L, EF_OP_TOPK, ws, ws_bytes, wl));
+  EF_TRY(check_ws(L, KIND == 0 ? EF_OP_TOPK : EF_OP_RANDK, P.ws, P.ws_bytes, wl));
   hipStream_t st = S(stream);
-  WSel w = make_ws(wl, ws);
   const Tables& T = L->T;
-  const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
-  const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
-  const dim3 pgrid((unsigned)L->nruns), pblk(kSampleRun);
-  if (phases & EF_PHASE_PREPARE) {  // the sample and the candidate rule
-    if (!g) EF_LAUNCH((k_sample_gather<0, false>), pgrid, pblk, 0, st, T, nullptr, src, w);
-    else if (g_dtype == EF_F32) EF_LAUNCH((k_sample_gather<0, true>), pgrid, pblk, 0, st, T, g, src, w);
-    else EF_LAUNCH((k_sample_gather<1, true>), pgrid, pblk, 0, st, T, g, src, w);
-    EF_TRY(launched());
-    EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w);
-    EF_TRY(launched());
+  const uint64_t K = (uint64_t)L->K;
+  const dim3 blk(kNT), sblk(kSelNT), pblk(kSampleRun);
+  auto g_at = [&](int w) -> const void* { return P.g ? P.g[w] : nullptr; };
+  auto e_at = [&](int w) -> float* { return P.e ? P.e[w] : nullptr; };
+  auto ws_of = [&](int w) { return make_ws(wl, P.ws + (uint64_t)w * P.ws_stride); };
+  // the kernel-argument table of workers [c0, c0 + nw)
+  auto batch_of = [&](int c0, int nw) {
+    Batch b{};
+    b.ws = P.ws_stride;
+    b.msg = (uint32_t)K;
+    for (int j = 0; j < nw; ++j) {
+      b.g[j] = g_at(c0 + j);
+      b.src[j] = P.src[c0 + j];
+      b.e[j] = e_at(c0 + j);
+      const uint64_t s = KIND == 1 && P.seeds ? P.seeds[c0 + j] : 0u;
+      b.seed_lo[j] = (uint32_t)s;
+      b.seed_hi[j] = (uint32_t)(s >> 32);
+    }
+    return b;
+  };
+
+  if (KIND == 0 && (phases & EF_PHASE_PREPARE)) {  // the sample and the candidate rule
+    for (int c0 = 0; c0 < P.W; c0 += kBatchMax) {
+      const unsigned nw = (unsigned)std::min(kBatchMax, P.W - c0);
+      const WSel w = ws_of(c0);
+      const Batch bt = batch_of(c0, (int)nw);
+      const dim3 pgrid((unsigned)L->nruns, nw), sgrid((unsigned)L->L, nw);
+      if (!P.g) EF_LAUNCH((k_sample_gather<0, false>), pgrid, pblk, 0, st, T, w, bt);
+      else if (P.g_dtype == EF_F32) EF_LAUNCH((k_sample_gather<0, true>), pgrid, pblk, 0, st, T, w, bt);
+      else EF_LAUNCH((k_sample_gather<1, true>), pgrid, pblk, 0, st, T, w, bt);
+      EF_TRY(launched());
+      EF_LAUNCH(k_sample_select, sgrid, sblk, 0, st, T, w, bt);
+      EF_TRY(launched());
+    }
   }
-  if (phases & EF_PHASE_STREAM) {  // the streaming pass
-    if (!g)
-      EF_LAUNCH((k_stream_sel<0, 0, false>), rgrid, dim3(kStrNT), 0, st, T, nullptr, src, nullptr, 0u, 0u, 0u, w);
-    else if (g_dtype == EF_F32)
-      EF_LAUNCH((k_stream_sel<0, 0, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
-    else
-      EF_LAUNCH((k_stream_sel<0, 1, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, 0u, 0u, 0u, w);
-    EF_TRY(launched());
+  if (phases & EF_PHASE_STREAM) {  // the streaming passes
+    const dim3 rgrid((unsigned)L->nrows), rblk(kStrNT);
+    for (int wk = 0; wk < P.W; ++wk) {
+      const WSel w = ws_of(wk);
+      const float* src = P.src[wk];
+      const uint64_t seed = KIND == 1 && P.seeds ? P.seeds[wk] : 0u;
+      const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32), step = KIND == 1 ? P.step : 0u;
+      if (!P.g)
+        EF_LAUNCH((k_stream_sel<KIND, 0, false>), rgrid, rblk, 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
+      else if (P.g_dtype == EF_F32)
+        EF_LAUNCH((k_stream_sel<KIND, 0, true>), rgrid, rblk, 0, st, T, g_at(wk), src, e_at(wk), s0, s1, step, w);
+      else
+        EF_LAUNCH((k_stream_sel<KIND, 1, true>), rgrid, rblk, 0, st, T, g_at(wk), src, e_at(wk), s0, s1, step, w);
+      EF_TRY(launched());
+    }
   }
   if (!(phases & EF_PHASE_FINISH)) return EF_OK;
-  if (!L->all_exact) {
-    EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w);
+  for (int c0 = 0; c0 < P.W; c0 += kBatchMax) {
+    const unsigned nw = (unsigned)std::min(kBatchMax, P.W - c0);
+    const WSel w = ws_of(c0);
+    const Batch bt = batch_of(c0, (int)nw);
+    const dim3 rgrid((unsigned)L->nrows, nw), sgrid((unsigned)L->L, nw);
+    const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows), nw);
+    uint32_t* idx = P.idx + (uint64_t)c0 * K;
+    float* val = P.val + (uint64_t)c0 * K;
+    if (KIND == 0 ? !L->all_exact : !L->rk_direct) {
+      if (KIND == 0) {
+        EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w, bt);
+        EF_TRY(launched());
+      }
+      EF_LAUNCH(k_collect<KIND>, rgrid, blk, 0, st, T, w, bt);
+      EF_TRY(launched());
+    }
+    if (L->big) {
+      EF_LAUNCH((k_select<KIND, true>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
+      EF_TRY(launched());
+      EF_LAUNCH(k_rowcount<KIND>, rgrid, blk, 0, st, T, w, bt);
+      EF_TRY(launched());
+      EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w, bt);
+    } else {
+      EF_LAUNCH((k_select<KIND, false>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
+    }
     EF_TRY(launched());
-    EF_LAUNCH(k_collect<0>, rgrid, blk, 0, st, T, w);
+    EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, idx, val, bt);
     EF_TRY(launched());
   }
-  const float* acc = g ? e_fused : src;
-  if (L->big) {
-    EF_LAUNCH((k_select<0, true>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
-    EF_TRY(launched());
-    EF_LAUNCH(k_rowcount<0>, rgrid, blk, 0, st, T, w);
-    EF_TRY(launched());
-    EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w);
-  } else {
-    EF_LAUNCH((k_select<0, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, 0u, 0u, 0u);
-  }
-  EF_TRY(launched());
-  EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, e_fused, idx, val);
-  return launched();
+  return EF_OK;
 }
 
-// Random-k: fused accumulate + Philox candidates -> collect (certain winners counted, the window
-// [ulo, tau) listed) -> exact threshold and row offsets -> emission.
+// One worker's step (the single-worker entry points): pointer tables of one entry.
+int run_one(int kind, const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint64_t seed,
+            uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream, unsigned phases) {
+  const void* gt[1] = {g};
+  const float* st[1] = {src};
+  float* et[1] = {e_fused};
+  Steps P;
+  P.g = g ? gt : nullptr;
+  P.g_dtype = g_dtype;
+  P.src = st;
+  P.e = e_fused ? et : nullptr;
+  P.idx = idx;
+  P.val = val;
+  P.ws = static_cast<uint8_t*>(ws);
+  P.ws_bytes = ws_bytes;
+  P.seeds = &seed;
+  P.step = step;
+  return kind == 0 ? run_select<0>(L, P, phases, stream) : run_select<1>(L, P, phases, stream);
+}
+
+int run_topk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint32_t* idx,
+             float* val, void* ws, size_t ws_bytes, void* stream, unsigned phases = EF_PHASE_ALL) {
+  return run_one(0, L, g, g_dtype, src, e_fused, 0u, 0u, idx, val, ws, ws_bytes, stream, phases);
+}
+
 int run_randk(const ef_layout* L, const void* g, int g_dtype, const float* src, float* e_fused, uint64_t seed,
               uint32_t step, uint32_t* idx, float* val, void* ws, size_t ws_bytes, void* stream,
               unsigned phases = EF_PHASE_ALL) {
-  WsLayout wl;
-  EF_TRY(check_ws(L, EF_OP_RANDK, ws, ws_bytes, wl));
-  hipStream_t st = S(stream);
-  WSel w = make_ws(wl, ws);
-  const Tables& T = L->T;
-  const dim3 rgrid((unsigned)L->nrows), blk(kNT), sgrid((unsigned)L->L), sblk(kSelNT);
-  const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows));
-  const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
-  // (random-k has nothing to prepare: its keys do not depend on the data)
-  if (phases & EF_PHASE_STREAM) {  // the streaming pass
-    if (!g)
-      EF_LAUNCH((k_stream_sel<1, 0, false>), rgrid, dim3(kStrNT), 0, st, T, nullptr, src, nullptr, s0, s1, step, w);
-    else if (g_dtype == EF_F32)
-      EF_LAUNCH((k_stream_sel<1, 0, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, s0, s1, step, w);
-    else
-      EF_LAUNCH((k_stream_sel<1, 1, true>), rgrid, dim3(kStrNT), 0, st, T, g, src, e_fused, s0, s1, step, w);
-    EF_TRY(launched());
-  }
-  if (!(phases & EF_PHASE_FINISH)) return EF_OK;
-  if (!L->rk_direct) {
-    EF_LAUNCH(k_collect<1>, rgrid, blk, 0, st, T, w);
-    EF_TRY(launched());
-  }
-  const float* acc = g ? e_fused : src;
-  if (L->big) {
-    EF_LAUNCH((k_select<1, true>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
-    EF_TRY(launched());
-    EF_LAUNCH(k_rowcount<1>, rgrid, blk, 0, st, T, w);
-    EF_TRY(launched());
-    EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w);
-  } else {
-    EF_LAUNCH((k_select<1, false>), sgrid, sblk, 0, st, T, w, acc, e_fused, idx, val, s0, s1, step);
-  }
-  EF_TRY(launched());
-  EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, e_fused, idx, val);
-  return launched();
+  return run_one(1, L, g, g_dtype, src, e_fused, seed, step, idx, val, ws, ws_bytes, stream, phases);
 }
 
 }  // namespace
@@ -641,6 +693,48 @@ int ef_step_topk_phases(const ef_layout* L, unsigned phases, const void* g, int 
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !word_ok(idx) || !word_ok(val) || phases == 0 || (phases & ~EF_PHASE_ALL)) return EF_EINVAL;
   return run_topk(L, g, g_dtype, e, e, idx, val, ws, ws_bytes, stream, phases);
+}
+
+// W workers' fused steps in one call (see the header).
+int step_batch(int kind, const ef_layout* L, unsigned phases, int32_t W, const void* const* g, int g_dtype,
+               float* const* e, const uint64_t* seeds, uint32_t step, uint32_t* idx, float* val, void* ws,
+               size_t ws_stride, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (phases == 0 || (phases & ~EF_PHASE_ALL)) return EF_EINVAL;
+  if (!g || !e || !word_ok(idx) || !word_ok(val)) return EF_EINVAL;
+  if (kind == 1 && !seeds) return EF_EINVAL;
+  for (int32_t w = 0; w < W; ++w) {
+    EF_TRY(check_g(g[w], g_dtype));
+    if (!vec_ok(e[w])) return EF_EINVAL;
+  }
+  if (!ws || !aligned(ws, kAlign) || ws_stride % kAlign) return EF_EINVAL;
+  if (ws_stride < ef_workspace_bytes(L, kind == 0 ? EF_OP_TOPK : EF_OP_RANDK, 1)) return EF_EWORKSPACE;
+  Steps P;
+  P.W = W;
+  P.g = g;
+  P.g_dtype = g_dtype;
+  P.src = const_cast<const float* const*>(e);
+  P.e = e;
+  P.idx = idx;
+  P.val = val;
+  P.ws = static_cast<uint8_t*>(ws);
+  P.ws_bytes = ws_stride;
+  P.ws_stride = ws_stride;
+  P.seeds = seeds;
+  P.step = step;
+  return kind == 0 ? run_select<0>(L, P, phases, stream) : run_select<1>(L, P, phases, stream);
+}
+
+int ef_step_topk_batch(const ef_layout* L, unsigned phases, int32_t W, const void* const* g, int g_dtype,
+                       float* const* e, uint32_t* idx, float* val, void* ws, size_t ws_stride, void* stream) {
+  return step_batch(0, L, phases, W, g, g_dtype, e, nullptr, 0u, idx, val, ws, ws_stride, stream);
+}
+
+int ef_step_randk_batch(const ef_layout* L, unsigned phases, int32_t W, const void* const* g, int g_dtype,
+                        float* const* e, const uint64_t* seeds, uint32_t step, uint32_t* idx, float* val, void* ws,
+                        size_t ws_stride, void* stream) {
+  return step_batch(1, L, phases, W, g, g_dtype, e, seeds, step, idx, val, ws, ws_stride, stream);
 }
 
 int compress_randk(const ef_layout* L, const float* acc, uint64_t seed, uint32_t step, uint32_t* idx, float* val,

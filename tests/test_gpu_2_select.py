@@ -293,3 +293,59 @@ def test_phased_step_matches_oracle(kind, two_streams):
                 E.ef_step_topk_phases(c.L, bad, gd, ed, idx, val, ws)
             else:
                 E.ef_step_randk_phases(c.L, bad, gd, ed, seed, 0, idx, val, ws)
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+@pytest.mark.parametrize("offs,rho,W,bf16", [
+    ([0, 3, 8192, 8196, 16384, 16388, 16392, 30000, 100000], 0.02, 3, False),
+    ([0, 1, 5, 64, 68, 300, 304, 10008, 10012, 40000], 0.1, 70, False),
+    ([0, 100000], 0.01, 1, True),
+    ([0, 2200000], 0.5, 2, False),
+], ids=["ragged-W3", "small-segments-W70", "flat-W1-bf16", "big-k-W2"])
+@pytest.mark.parametrize("split", [False, True], ids=["fused", "split-phases"])
+def test_batched_steps_match_oracle(kind, offs, rho, W, bf16, split):
+    """ef_step_*_batch: W workers' fused steps in one call (selection kernels with the worker in
+    the grid, in chunks of 64) equal the oracle's steps worker by worker, over two steps with the
+    residual carried."""
+    import paper_2009_09271_amd as E
+    import torch
+    from workloads import to_bf16_bits
+    announce("batched steps", kind, offs[-1], len(offs) - 1, W, bf16)
+    c = Case(offs, rho)
+    rng = np.random.default_rng(W + len(offs))
+    G = (rng.standard_normal((W, c.d)) * 10.0 ** rng.integers(-3, 1, (W, 1))).astype(np.float32)
+    if bf16:
+        G = np.stack([to_bf16_bits(x) for x in G])
+    gd = [dev(x) for x in G]
+    if bf16:
+        gd = [x.view(torch.bfloat16) for x in gd]
+    e = np.zeros((W, c.d), np.float32)
+    ed = [dev(x) for x in e]
+    ws, stride = E.batch_workspace(c.L, E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK, W)
+    seeds = [(11 << 32) | w for w in range(W)]
+    for step in range(2):
+        idx = torch.empty((W, c.K), dtype=torch.int32, device="cuda")
+        val = torch.empty((W, c.K), dtype=torch.float32, device="cuda")
+        def call(p, st=None):
+            if kind == "topk":
+                E.ef_step_topk_batch(c.L, gd, ed, idx, val, ws, stride, phases=p, stream=st)
+            else:
+                E.ef_step_randk_batch(c.L, gd, ed, seeds, step, idx, val, ws, stride, phases=p, stream=st)
+
+        if split:  # prepare + stream on one stream, finish on another after an event
+            side = torch.cuda.Stream()
+            call(E.EF_PHASE_PREPARE | E.EF_PHASE_STREAM)
+            side.wait_stream(torch.cuda.current_stream())
+            call(E.EF_PHASE_FINISH, side)
+            torch.cuda.current_stream().wait_stream(side)
+        else:
+            call(E.EF_PHASE_ALL)
+        hi, hv, he = host(idx).view(np.uint32), host(val), np.stack([host(x) for x in ed])
+        for w in range(W):
+            (wm, wv), we = c.oracle_step(kind, G[w], e[w], seeds[w], step)
+            assert_msg_equal(kind, (hi[w], hv[w]), (wm, wv), f"step {step} worker {w}")
+            assert np.array_equal(bits(he[w]), bits(we)), f"e' step {step} worker {w}"
+            e[w] = we
+        op = E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK
+        for w in range(min(W, 3)):
+            assert not (c.L.diag(ws[w], op) & E.DIAG_COUNT_MISMATCH), f"worker {w}: row counts do not add up"
