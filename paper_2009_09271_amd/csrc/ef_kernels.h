@@ -1201,7 +1201,8 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
-      store4m(acc_out, i0, vm[r], v[r]);
+      // random-k, direct lists: stored below, once the certain winners are known
+      if (!(KIND == 1 && direct)) store4m(acc_out, i0, vm[r], v[r]);
     }
   } else {
 #pragma unroll
@@ -1270,6 +1271,21 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
   if (direct) {
     if (lane == 0) wc[wid] = ncert;
     if (threadIdx.x == 0) s_und = 0;
+  }
+  if constexpr (FUSED && KIND == 1) {
+    // random-k, direct lists: the residual is +0 at the certain winners (every one of them is sent
+    // unless the segment takes the exact path, which puts their values back first), so the emit
+    // kernel only zeroes the winners from the undecided window
+    if (direct) {
+#pragma unroll
+      for (int r = 0; r < kSR; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = ((cbits >> (4 * r + q)) & 1u) ? 0.0f : v[r][q];
+        store4m(acc_out, i0, vm[r], o);
+      }
+    }
   }
   __syncthreads();
   uint32_t base = 0;
@@ -1381,67 +1397,76 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 // any order: the selection over the list does not depend on it; row r appends to sub-list
 // r % kSubLists, which spreads the atomics on the list counters).  Top-k: above / inside bin B of
 // a histogrammed segment.  Random-k: Philox key below ulo_l / in [ulo_l, tau_l).
+// One wavefront per kCollectRows consecutive rows: the rows' segments, candidate counts and first
+// 64 candidate keys are loaded together; counts and list positions come from ballots, and each
+// chunk of 64 candidates reserves its list space with one atomic.
+constexpr uint32_t kCollectRows = 4;                          // rows per wavefront
+constexpr uint32_t kCollectRowsWG = (kNT / 64) * kCollectRows;  // rows per workgroup
 template <int KIND>
 __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
-  __shared__ uint32_t lds[kNT / 64];
-  __shared__ uint32_t s_base;
-  const uint32_t row = blockIdx.x;
-  const int l = T.row_seg[row];
-  uint32_t* R = res_of(ws, l);
-  uint32_t A = 0, sh = 0, B = 0, ulo = 0;
-  if constexpr (KIND == 0) {
-    if (R[R_SLOW] || R[R_MODE]) return;
-    A = R[R_A];
-    sh = R[R_SH];
-    B = R[R_B];
-  } else {
-    ulo = T.seg_ulo[l];
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * kCollectRows;
+  int ls[kCollectRows];
+  uint32_t cnts[kCollectRows], k0[kCollectRows];
+#pragma unroll
+  for (uint32_t r = 0; r < kCollectRows; ++r) {
+    const uint32_t row = min(row0 + r, (uint32_t)T.nrows - 1u);
+    ls[r] = T.row_seg[row];
+    cnts[r] = ws.counts[row];
+    k0[r] = ws.cand_key[(size_t)row * kTile + lane];  // the first 64 keys (past the count: unused)
   }
-  // class: 2 = certain winner, 1 = undecided (listed), 0 = loses
-  auto cls = [&](uint32_t k) -> uint32_t {
+#pragma unroll
+  for (uint32_t r = 0; r < kCollectRows; ++r) {
+    const uint32_t row = row0 + r;
+    if (row >= (uint32_t)T.nrows) break;
+    const int l = ls[r];
+    const uint32_t* R = res_of(ws, l);
+    uint32_t A = 0, sh = 0, B = 0, ulo = 0;
     if constexpr (KIND == 0) {
-      const uint32_t b = cand_bin(k, A, sh);
-      return b > B ? 2u : (b == B ? 1u : 0u);
+      if (R[R_SLOW] || R[R_MODE]) continue;
+      A = R[R_A];
+      sh = R[R_SH];
+      B = R[R_B];
     } else {
-      return ~k < ulo ? 2u : 1u;
+      ulo = T.seg_ulo[l];
     }
-  };
-  const uint32_t cnt = ws.counts[row];
-  const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
-  const bool tie_bin = KIND == 0 && B == 0;  // the threshold bin is the single key A: count, do not list
-  uint32_t na = 0, ne = 0;
-  for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
-    const uint32_t c = cls(ck[j]);
-    na += c == 2u ? 1u : 0u;
-    ne += c == 1u ? 1u : 0u;
-  }
-  uint32_t tot;
-  const uint32_t ex = block_excl_scan<kNT>(na | (ne << 16), lds, tot);  // row totals <= kTile
-  const uint32_t tot_e = tot >> 16;
-  const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
-  if (tie_bin) {
-    if (threadIdx.x == 0) {
-      ws.rcnt[row] = tot & 0xFFFFu;
-      ws.rtie[row] = tot_e;
+    // class: 2 = certain winner, 1 = undecided (listed), 0 = loses
+    auto cls = [&](uint32_t k) -> uint32_t {
+      if constexpr (KIND == 0) {
+        const uint32_t b = cand_bin(k, A, sh);
+        return b > B ? 2u : (b == B ? 1u : 0u);
+      } else {
+        return ~k < ulo ? 2u : 1u;
+      }
+    };
+    const bool tie_bin = KIND == 0 && B == 0;  // the threshold bin is the single key A: count, do not list
+    const uint32_t cnt = cnts[r];
+    const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
+    const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
+    const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
+    uint32_t na = 0, ne = 0;
+    for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
+      const uint32_t j = j0 + lane;
+      const uint32_t k = j0 == 0 ? k0[r] : (j < cnt ? ck[j] : 0u);
+      const uint32_t cl = j < cnt ? cls(k) : 0u;
+      na += (uint32_t)__popcll(__ballot(cl == 2u));
+      const uint64_t bu = __ballot(cl == 1u);
+      const uint32_t nu = (uint32_t)__popcll(bu);
+      ne += nu;
+      if (tie_bin || nu == 0) continue;
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(lcnt_of(ws, l, c), nu);
+      base = __shfl(base, 0, 64);
+      if (cl == 1u) {
+        const size_t p = sublist_pos(r0, c, base + lanes_below(bu));
+        ws.list_key[p] = k;
+        ws.list_idx[p] = ci[j];
+      }
     }
-    return;
-  }
-  if (threadIdx.x == 0) {
-    ws.rcnt[row] = tot & 0xFFFFu;
-    s_base = tot_e ? atomicAdd(lcnt_of(ws, l, c), tot_e) : 0u;
-  }
-  __syncthreads();
-  if (tot_e == 0) return;
-  const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
-  uint32_t t = s_base + (ex >> 16);
-  for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
-    const uint32_t k = ck[j];
-    if (cls(k) == 1u) {
-      const size_t p = sublist_pos(r0, c, t);
-      ws.list_key[p] = k;
-      ws.list_idx[p] = ci[j];
-      ++t;
+    if (lane == 0) {
+      ws.rcnt[row] = na;
+      if (tie_bin) ws.rtie[row] = ne;
     }
   }
 }
@@ -1632,6 +1657,21 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     }
   }
   if (slow) {
+    if constexpr (KIND == 1) {
+      if (direct && e_zero) {
+        // the streaming pass stored +0 at the certain winners (keys below ulo); the exact path needs
+        // acc there: every certain winner is a candidate, whose value its row slot keeps
+        const uint32_t ulo = T.seg_ulo[l];
+        for (uint32_t x = a; x < b; ++x) {
+          const size_t sl = (size_t)(r0 + x) * kTile;
+          const uint32_t cnt = ws.counts[r0 + x];
+          for (uint32_t j = 0; j < cnt; ++j)
+            if (~ws.cand_key[sl + j] < ulo) e_zero[ws.cand_idx[sl + j]] = ws.cand_val[sl + j];
+        }
+        __threadfence();
+        __syncthreads();
+      }
+    }
     slow_select<KIND>(T, l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
     return;
   }
@@ -1882,45 +1922,106 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
   if (threadIdx.x == 0 && total != (uint32_t)T.seg_k[l]) atomicOr(ws.diag, kDiagCount);
 }
 
-// Per row, one wavefront each (kNT / 64 rows per workgroup, no workgroup barriers): the winners,
-// in index order, to the message at the row's offset; e = +0 there.
-constexpr uint32_t kEmitRows = kNT / 64;
-__global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT) {
+// Emission: per row, the winners in index order to the message at the row's offset, and e = +0
+// there.  One wavefront per RW consecutive rows: lanes j < RW hold row j's count, offset and
+// threshold; the rows' candidates are laid out one after another over the 64 lanes (a wave prefix
+// of the counts; each lane finds its row by a binary search over those lanes), so a wavefront
+// serves its rows in one or a few passes of 64 candidates, the next pass's loads in flight while
+// the current one is written.  A winner's position is its row's offset plus the row's winners
+// before it: earlier passes (kept by the row's lane) and a ballot count over the row's lanes in
+// this pass.  RW = 16 for random-k (a few candidates per row); 4 for top-k, whose rows in the
+// layers of largest magnitude hold hundreds.
+template <uint32_t RW>
+__global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT,
+                                              int certain_zeroed) {
+  static_assert(RW >= 1 && RW <= 64 && (RW & (RW - 1)) == 0, "one lane per row, a power of two");
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   float* e_zero = BT.e[blockIdx.y];
   out_idx = shifted(out_idx, (uint64_t)blockIdx.y * BT.msg * 4u);
   out_val = shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u);
-  const uint32_t row = blockIdx.x * kEmitRows + (threadIdx.x >> 6);
-  if (row >= (uint32_t)T.nrows) return;
-  const int lane = threadIdx.x & 63;
-  const int l = T.row_seg[row];
-  const uint32_t* R = res_of(ws, l);
-  if (R[R_SLOW]) return;
-  const uint32_t Tk = R[R_T], IT = R[R_IT];
-  const uint32_t cnt = ws.counts[row], pend = (uint32_t)T.seg_P[l + 1];
-  uint32_t base = ws.roff[row];
-  const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
-  const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
-  const float* cv = ws.cand_val + (size_t)row * kTile;
-  for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
-    const uint32_t j = j0 + (uint32_t)lane;
-    const bool in = j < cnt;
-    uint32_t k = 0, i = 0;
-    float v = 0.0f;
-    if (in) {
-      k = ck[j];
-      i = ci[j];
-      v = cv[j];
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * RW;
+  if (row0 >= (uint32_t)T.nrows) return;
+  // lane j < RW: row row0 + j (rows past the end and rows of exact-path segments count 0)
+  const uint32_t myrow = row0 + lane;
+  const bool has_row = lane < RW && myrow < (uint32_t)T.nrows;
+  uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, ulo = 0;
+  if (has_row) {
+    const int l = T.row_seg[myrow];
+    const uint32_t* R = res_of(ws, l);
+    cnt = ws.counts[myrow];
+    off = ws.roff[myrow];
+    pend = (uint32_t)T.seg_P[l + 1];
+    ulo = certain_zeroed ? T.seg_ulo[l] : 0u;
+    if (R[R_SLOW]) cnt = 0;
+    Tk = R[R_T];
+    IT = R[R_IT];
+  }
+  const uint32_t incl = wave_incl_scan(cnt);
+  const uint32_t total = __shfl(incl, 63, 64);
+  const uint32_t pre = incl - cnt;  // this lane's row: first flattened candidate
+  // flattened candidate f -> its row lane r (the last row lane with pre_r <= f; for f < total that
+  // row's count is nonzero, so f lies inside it) and its slot
+  auto locate = [&](uint32_t f, uint32_t& r, size_t& sl) {
+    r = 0;
+#pragma unroll
+    for (uint32_t step = RW / 2; step >= 1; step >>= 1) {
+      const uint32_t p = __shfl(pre, (int)(r + step), 64);
+      if (f < total && p <= f) r += step;
     }
-    const bool win = in && (k > Tk || (k == Tk && i < IT));
+    sl = (size_t)(row0 + r) * kTile + (f - __shfl(pre, (int)r, 64));
+  };
+  uint32_t done = 0;  // this lane's row: winners emitted in earlier passes
+  uint32_t r;
+  size_t sl;
+  locate(lane, r, sl);
+  uint32_t k = 0, i = 0;
+  float v = 0.0f;
+  if (lane < total) {
+    k = ws.cand_key[sl];
+    i = ws.cand_idx[sl];
+    v = ws.cand_val[sl];
+  }
+  for (uint32_t f0 = 0; f0 < total; f0 += 64) {
+    const uint32_t f = f0 + lane;
+    const bool in = f < total;
+    const uint32_t rpre = __shfl(pre, (int)r, 64);
+    const uint32_t rTk = __shfl(Tk, (int)r, 64), rIT = __shfl(IT, (int)r, 64);
+    const uint32_t roffr = __shfl(off, (int)r, 64) + __shfl(done, (int)r, 64);
+    const uint32_t rpend = __shfl(pend, (int)r, 64), rulo = __shfl(ulo, (int)r, 64);
+    const uint32_t ck = k, ci = i;
+    const float cv = v;
+    // the next pass's candidates, in flight while this pass is written
+    uint32_t rn = 0;
+    size_t sn = 0;
+    locate(f + 64, rn, sn);
+    if (f + 64 < total) {
+      k = ws.cand_key[sn];
+      i = ws.cand_idx[sn];
+      v = ws.cand_val[sn];
+    }
+    const bool win = in && (ck > rTk || (ck == rTk && ci < rIT));
     const uint64_t bw = __ballot(win);
-    const uint32_t pos = base + lanes_below(bw);
-    if (win && pos < pend) {
-      out_idx[pos] = i;
-      out_val[pos] = v;
-      if (e_zero) e_zero[i] = 0.0f;
+    // this pass's lanes of row r before this lane: [lo_r, lane)
+    const uint32_t lo_r = rpre > f0 ? rpre - f0 : 0u;
+    const uint64_t below = (lane ? (~0ull >> (64 - lane)) : 0ull) & ~((lo_r ? (~0ull >> (64 - lo_r)) : 0ull));
+    const uint32_t pos = roffr + (uint32_t)__popcll(bw & below);
+    if (win && pos < rpend) {
+      out_idx[pos] = ci;
+      out_val[pos] = cv;
+      // random-k, direct lists: the streaming pass already zeroed e at the certain winners (key' of
+      // a key below ulo)
+      if (e_zero && !(~ck < rulo)) e_zero[ci] = 0.0f;
     }
-    base += (uint32_t)__popcll(bw);
+    // each row lane adds its winners of this pass
+    if (has_row) {
+      const uint32_t a = pre > f0 ? pre - f0 : 0u, z = incl > f0 ? min(incl - f0, 64u) : 0u;
+      if (z > a) {
+        const uint64_t m = (z == 64 ? ~0ull : (~0ull >> (64 - z))) & ~(a ? (~0ull >> (64 - a)) : 0ull);
+        done += (uint32_t)__popcll(bw & m);
+      }
+    }
+    r = rn;
   }
 }
 

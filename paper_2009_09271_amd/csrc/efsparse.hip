@@ -418,6 +418,8 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     const WSel w = ws_of(c0);
     const Batch bt = batch_of(c0, (int)nw);
     const dim3 rgrid((unsigned)L->nrows, nw), sgrid((unsigned)L->L, nw);
+    constexpr uint32_t kEmitRW = KIND == 0 ? 4u : 16u;  // rows per wavefront of the emission
+    constexpr uint32_t kEmitRows = (kNT / 64) * kEmitRW;
     const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows), nw);
     uint32_t* idx = P.idx + (uint64_t)c0 * K;
     float* val = P.val + (uint64_t)c0 * K;
@@ -426,7 +428,8 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
         EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w, bt);
         EF_TRY(launched());
       }
-      EF_LAUNCH(k_collect<KIND>, rgrid, blk, 0, st, T, w, bt);
+      const dim3 cgrid((unsigned)((L->nrows + kCollectRowsWG - 1) / kCollectRowsWG), nw);
+      EF_LAUNCH(k_collect<KIND>, cgrid, blk, 0, st, T, w, bt);
       EF_TRY(launched());
     }
     if (L->big) {
@@ -439,7 +442,7 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
       EF_LAUNCH((k_select<KIND, false>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
     }
     EF_TRY(launched());
-    EF_LAUNCH(k_emit, egrid, blk, 0, st, T, w, idx, val, bt);
+    EF_LAUNCH(k_emit<kEmitRW>, egrid, blk, 0, st, T, w, idx, val, bt, KIND == 1 && L->rk_direct && P.e ? 1 : 0);
     EF_TRY(launched());
   }
   return EF_OK;
