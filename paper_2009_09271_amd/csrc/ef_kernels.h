@@ -312,7 +312,7 @@ __global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc
 // ---------------------------------------------------------------------------------------------
 // Output tiles of the sparse aggregate: kAggTile elements, summed by one wavefront (kAggRounds
 // float4 groups per lane).
-constexpr uint32_t kAggTile = 1024;
+constexpr uint32_t kAggTile = 1024;  // 1024: 20.6 us on random-k messages; 2048: 23.8; 4096: 31.2
 constexpr int kAggRounds = (int)kAggTile / (4 * 64);
 
 // Column sum over W rows of K values (shared coordinates): sum_u v[u K + j] in row order from +0.0,
