@@ -395,13 +395,11 @@ def main():
             E.ef_step_randk_batch(lay0, g, ev, seeds, t, mi, mv, wsb["randk"][0], wsb["randk"][1], stream=sA)
         aggregate(v, sA)
 
-    def run_step(t, vs=None, schedule=None):
+    def run_step(t, vs=None):
         vs = vs or variants
-        schedule = schedule or args.schedule
+        schedule = args.schedule
         for k, bufs in msg_bufs.items():
             msg[k] = bufs[t % 2]
-        if schedule == "serial":
-            return run_step_serial(t, vs)
         if schedule == "batch":
             return run_step_batch(t, vs)
         if schedule == "fused":
@@ -501,12 +499,18 @@ def main():
         }
 
     # ---- per-kernel durations from library-recorded HIP events ---------------------------------
-    # (1) the same schedule as the timed steps (the roofline kernel's launches); (2) every launch
-    # one after another on one stream (each kernel's duration without concurrency)
-    def kernel_table(schedule):
+    # (1) the same schedule as the timed steps (the roofline kernel's launches); (2) per variant,
+    # its W steps and aggregate alone on one stream (each kernel's duration without concurrency)
+    def kernel_table(run_one):
         E.timing_collect(reset=True)
         E.timing_enable(True)
-        nonlocal_step[0] = run_steps(nonlocal_step[0], args.steps, schedule)
+        with torch.cuda.stream(sA):
+            for _ in range(args.steps):
+                t = nonlocal_step[0]
+                for k, bufs in msg_bufs.items():
+                    msg[k] = bufs[t % 2]
+                run_one(t)
+                nonlocal_step[0] = t + 1
         torch.cuda.synchronize()
         E.timing_enable(False)
         tm = E.timing_collect(reset=True)
@@ -521,17 +525,16 @@ def main():
                 table[name]["frac"] = round(ab / (avg_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
         return table
 
-    def run_steps(t0, n, schedule):
-        with torch.cuda.stream(sA):
-            for i in range(n):
-                run_step(t0 + i, schedule=schedule)
-        return t0 + n
+    def alone(v):
+        if args.schedule == "batch":
+            return lambda t: run_variant_alone(t, v)
+        return lambda t: run_step_serial(t, [v])
 
     nonlocal_step = [step_no]
     kernels, kernels_serial, roofline = {}, {}, None
     if not args.no_kernel_timing:
-        kernels = kernel_table(args.schedule)
-        kernels_serial = kernel_table("serial")
+        kernels = kernel_table(lambda t: run_step(t))
+        kernels_serial = {vname(v): kernel_table(alone(v)) for v in variants}
         dom = next(iter(kernels))
         ab = kernel_alg_bytes(dom, d, K, L, W)
         if ab is not None:
