@@ -134,6 +134,90 @@ def measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, ar
     return res
 
 
+def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20):
+    """Each compressor at the given scope: one worker's step alone (the fused entry point, and the
+    composed calls accumulate + compress + update), and the aggregate of the W workers' messages
+    alone; back-to-back repetitions on one stream, timed with events on that stream.  Also the
+    library's plain copy kernel over d floats, as a measured streaming ceiling."""
+    d = offs[-1]
+    st = torch.cuda.Stream(dev)
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                fn()
+            a.record(st)
+            for _ in range(reps):
+                fn()
+            b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    def entry(us, alg_bytes, elements):
+        return {"us": round(us, 3), "elements_per_s": elements / (us * 1e-6), "alg_bytes": int(alg_bytes),
+                "frac_of_hbm_peak": round(alg_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    acc = torch.empty(d, dtype=torch.float32, device=dev)
+    e = torch.zeros(d, dtype=torch.float32, device=dev)
+    out = torch.empty(d, dtype=torch.float32, device=dev)
+    res = {}
+    for kind, b in variants:
+        lay = E.Layout(d, offs, density, b if kind == "randblock" else 1).bind(dev)
+        K, L = lay.K, lay.n_seg
+        block = kind == "randblock"
+        mi = torch.empty((W, L if block else K), dtype=torch.int32, device=dev)
+        mv = torch.empty((W, K), dtype=torch.float32, device=dev)
+        ws = None if block else lay.workspace(E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK, 1, dev)
+        ws_agg = None if block else lay.workspace(E.EF_OP_AGG_SPARSE, W, dev)
+        kindm = E.EF_MSG_BLOCK if block else E.EF_MSG_SPARSE
+
+        def fused(w=0):
+            if kind == "topk":
+                E.ef_step_topk(lay, g[w], e, mi[w], mv[w], ws)
+            elif kind == "randk":
+                E.ef_step_randk(lay, g[w], e, seeds[w], 0, mi[w], mv[w], ws)
+            else:
+                E.ef_step_randblock(lay, g[w], e, seeds[w], 0, mi[w], mv[w])
+
+        def composed():
+            E.ef_accumulate(lay, g[0], e, acc)
+            if kind == "topk":
+                E.compress_topk(lay, acc, mi[0], mv[0], ws)
+            elif kind == "randk":
+                E.compress_randk(lay, acc, seeds[0], 0, mi[0], mv[0], ws)
+            else:
+                E.compress_randblock(lay, acc, seeds[0], 0, mi[0], mv[0])
+            E.ef_update(lay, acc, kindm, mi[0], e)
+
+        step_b, agg_b = alg_bytes_op(kind, d, K, L, W)
+        r = {"fused_step": entry(timed(fused), step_b, d)}
+        # the step's kernels (library events per launch, a separate pass)
+        E.timing_collect(reset=True)
+        E.timing_enable(True)
+        timed(fused)
+        E.timing_enable(False)
+        r["fused_step"]["kernels_us"] = {name: round(tot * 1e3 / nl, 3)
+                                         for name, (tot, nl) in E.timing_collect(reset=True).items()}
+        # composed: the same algorithmic bytes (the intermediate acc costs 8d more by construction)
+        r["composed_step"] = entry(timed(composed), step_b, d)
+        with torch.cuda.stream(st):
+            for w in range(W):
+                fused(w)
+        r["aggregate"] = entry(timed(lambda: E.decompress_aggregate(lay, kindm, W, mi, mv, out, ws_agg)), agg_b, d)
+        res[vname((kind, b))] = r
+    none = torch.full((1,), d, dtype=torch.int32, device=dev)
+    lay = E.Layout(d, [0, d], 1.0 / d, 1).bind(dev)  # k = 1: a one-entry message past the end zeroes nothing
+    E.timing_collect(reset=True)
+    E.timing_enable(True)
+    timed(lambda: E.ef_update(lay, acc, E.EF_MSG_SPARSE, none, out))
+    E.timing_enable(False)
+    tot_ms, n = E.timing_collect(reset=True)["k_copy"]
+    res["copy_ceiling"] = entry(tot_ms * 1e3 / n, 8 * d, d)
+    res["copy_ceiling"]["kernel"] = "k_copy: read d floats, write d floats (per-launch events)"
+    return res
+
+
 def cpu_baseline(wl, offs, ks, variants, W, grads, budget_note):
     """Time the CPU oracle on a bounded sample of worker steps plus one aggregate per variant,
     and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
@@ -197,6 +281,8 @@ def main():
     ap.add_argument("--variants", default="topk,randk,randblock")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--no-single", action="store_true", help="skip the one-worker step and aggregate "
+                    "measurements per compressor at flat and per-layer scope")
     ap.add_argument("--no-next", action="store_true", help="skip the shared-coordinate, fused-update and "
                     "dense-average measurements")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="N",
@@ -551,6 +637,13 @@ def main():
                         "traffic_source": os.path.relpath(tfile, os.path.dirname(os.path.abspath(__file__)))
                         if traffic is not None else None}
 
+    # ---- each compressor alone, one worker's step and one aggregate, at both scopes ---------------
+    single = {}
+    if not args.no_single:
+        for scope in ("flat", "layer"):
+            single[scope] = measure_single(E, torch, dev, wl.seg_offsets(scope), density, variants, W, g,
+                                           seeds)
+
     # ---- the paths next to the hot path, on the same workload (each alone, events on one stream) --
     nxt = {} if args.no_next else measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, args)
 
@@ -591,6 +684,7 @@ def main():
         "per_compressor": per,
         "kernels": kernels,
         "kernels_serial": kernels_serial,
+        "single": single,
         "next_rows": nxt,
         "input_generation_s": round(t_gen, 2),
     }

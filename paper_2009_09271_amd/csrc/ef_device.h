@@ -69,7 +69,9 @@ struct Tables {
   const int32_t* chunk_sf;     // [nchunks] first / last segment of each data tile
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row
-  int32_t d, L, nchunks, nrows, nruns;
+  const uint32_t* btile;       // [2 nbtiles] block aggregate, multi-segment layouts: (1024-element
+                               // data tile, segment) for every pair with an element in common
+  int32_t d, L, nchunks, nrows, nruns, nbtiles;
   int32_t rk_direct;           // random-k: k_stream_sel counts the certain winners and lists the
                                // undecided candidates of every row; k_select gathers the lists
 };

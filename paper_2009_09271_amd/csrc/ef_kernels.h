@@ -438,7 +438,6 @@ __device__ __forceinline__ void agg_emit4(const AggOut& O, uint32_t i0, int nv, 
   }
 }
 
-constexpr int kAggStarts = 1024;    // block starts (workers x segments of the tile) held in LDS
 constexpr int kAggChunk = 4;        // sparse aggregate: entries per lane loaded together past the first 64
 constexpr int kAggClaim = 256;      // sparse aggregate: claim slots (positions hash to x mod 256)
 
@@ -579,7 +578,7 @@ __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t
 // Single-segment layouts (flat scope): one workgroup per tile of R float4 groups per thread, no
 // tables to look up and no barrier.  Each wavefront loads the starts of 64 workers at a time
 // (lane j: worker wb + j), finds those whose run meets the tile with one ballot and visits them in
-// ascending order, as in k_agg_block.
+// ascending order.
 template <int R>
 __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_t K, const uint32_t* start,
                                                     const float* val, AggOut O) {
@@ -631,102 +630,71 @@ __global__ __launch_bounds__(kNT) void k_agg_block1(int32_t d, int32_t W, int32_
   }
 }
 
-// Persistent workgroups, each walking data tiles (blockIdx.x, then every gridDim.x-th), sums held
-// in registers (each thread its kRounds float4 groups; few enough registers for 8 waves per SIMD).  Per pass over up to kAggSegs
-// segments of the tile and a group of workers, the segments' sizes and the workers' block starts
-// come in one round trip, and stay cached while consecutive tiles lie in the same segments with
-// all workers in one group (the common case: a workgroup loads them once).  Then, for every worker
-// in order and every segment, the run pieces that meet the tile are added element by element
-// (each element gets at most one value per worker, and the segments of a tile are disjoint).
-constexpr int kAggSegs = 64;
+// Output stage for the elements q of the group at i0 whose bit q is set in `mask` (any subset: a
+// group that straddles a segment boundary is written in parts by the two segments' workgroups).
+__device__ __forceinline__ void agg_emit4m(const AggOut& O, uint32_t i0, uint32_t mask, const float sum[4]) {
+  if (mask == 0xFu) {
+    agg_emit4(O, i0, 4, sum);
+    return;
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    if (!((mask >> q) & 1u)) continue;
+    const float s1[4] = {sum[q], 0.0f, 0.0f, 0.0f};
+    agg_emit4(O, i0 + (uint32_t)q, 1, s1);
+  }
+}
+
+// Multi-segment layouts: one workgroup per (1024-element data tile, segment) pair with an element
+// in common, listed by a table built with the layout; otherwise as k_agg_block1 within the
+// segment: the segment's block starts of 64 workers at a time, the workers whose run meets the
+// tile found with one ballot and visited in ascending order.  Each element gets at most one value
+// per worker, and the tile's elements outside the segment belong to the other pairs of the tile.
+constexpr uint32_t kAggBT = 4u * kNT;  // one float4 group per thread
 
 __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t K, const uint32_t* start,
                                                    const float* val, AggOut O) {
-  __shared__ uint32_t s_st[kAggStarts];
-  __shared__ uint32_t s_seg[4][kAggSegs];  // o, n, k, P of the pass's segments
-  int c_sf = -1, c_sl = -1;                // segments whose starts s_st holds (one pass, one group)
-  constexpr int kR = kRounds;
-  for (uint32_t c = blockIdx.x; c < (uint32_t)T.nchunks; c += gridDim.x) {
-    const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
-    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-    float a[kR][4];
+  const uint2 bt = reinterpret_cast<const uint2*>(T.btile)[blockIdx.x];
+  const int l = (int)bt.y;
+  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
+  const uint32_t k = (uint32_t)T.seg_k[l], P = (uint32_t)T.seg_P[l];
+  const uint32_t tlo = bt.x * kAggBT;
+  const uint32_t lo = max(tlo, o), hi = min(tlo + kAggBT, o + n);
+  const uint32_t i0 = tlo + threadIdx.x * 4u;
+  const int lane = threadIdx.x & 63;
+  float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int wb = 0; wb < W; wb += 64) {
+    const int nw = min(64, W - wb);
+    uint32_t s = 0;
+    bool hit = false;
+    if (lane < nw) {
+      s = start[(size_t)(wb + lane) * T.L + l] % n;
+      // run piece 1: [o + s, o + e1), e1 = min(s + k, n); piece 2 (wrapped): [o, o + s + k - e1),
+      // empty unless the run wraps (written without a conditional, as in k_agg_block1)
+      const uint32_t e1 = min(s + k, n);
+      hit = max(lo, o + s) < min(hi, o + e1) || lo < min(hi, o + (s + k - e1));
+    }
+    uint64_t todo = __ballot(hit);
+    while (todo) {
+      const int j = __ffsll((long long)todo) - 1;
+      todo &= todo - 1;
+      const uint32_t sw = __shfl(s, j, 64);
+      const float* v = val + (size_t)(wb + j) * K + P;
+      const uint32_t e1 = min(sw + k, n);
+      const uint32_t a1 = max(lo, o + sw), b1 = min(hi, o + e1), b2 = min(hi, o + (sw + k - e1));
 #pragma unroll
-    for (int r = 0; r < kR; ++r)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) a[r][q] = 0.0f;
-    for (int l0 = sf; l0 <= sl; l0 += kAggSegs) {
-      const int ns = min(kAggSegs, sl - l0 + 1);
-      const int gw = kAggStarts / ns;  // workers per group
-      const bool one = l0 == sf && sl - sf < kAggSegs && W <= gw;  // whole tile in one pass and group
-      for (int w0 = 0; w0 < W; w0 += gw) {
-        const int nw = min(gw, W - w0);
-        if (!(one && c_sf == sf && c_sl == sl)) {
-          __syncthreads();  // the previous pass is done with s_st / s_seg
-          if ((int)threadIdx.x < ns) {
-            const int l = l0 + threadIdx.x;
-            s_seg[0][threadIdx.x] = (uint32_t)T.seg_off[l];
-            s_seg[1][threadIdx.x] = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
-            s_seg[2][threadIdx.x] = (uint32_t)T.seg_k[l];
-            s_seg[3][threadIdx.x] = (uint32_t)T.seg_P[l];
-          }
-          for (int x = threadIdx.x; x < nw * ns; x += kNT) {
-            const int w = x / ns, l = l0 + x % ns;
-            const uint32_t n = (uint32_t)(T.seg_off[l + 1] - T.seg_off[l]);
-            s_st[x] = start[(size_t)(w0 + w) * T.L + l] % n;
-          }
-          __syncthreads();
-          c_sf = one ? sf : -1;
-          c_sl = one ? sl : -1;
-        }
-        // workers of the group with a run piece in this tile, 64 at a time: each wave finds them
-        // with a ballot (lane j tests worker wb + j) and visits them in ascending order
-        for (int wb = 0; wb < nw; wb += 64) {
-          const int wl = wb + (int)(threadIdx.x & 63);
-          bool hit = false;
-          if (wl < nw) {
-            for (int x = 0; x < ns; ++x) {
-              const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], s = s_st[wl * ns + x];
-              const uint32_t e1 = min(s + k, n);  // piece 2 below is empty unless the run wraps
-              hit = hit || (max(lo, o + s) < min(hi, o + e1)) || (max(lo, o) < min(hi, o + (s + k - e1)));
-            }
-          }
-          uint64_t todo = __ballot(hit);
-          while (todo) {
-            const int w = wb + __ffsll((long long)todo) - 1;
-            todo &= todo - 1;
-            const float* v = val + (size_t)(w0 + w) * K;
-            for (int x = 0; x < ns; ++x) {
-              const uint32_t o = s_seg[0][x], n = s_seg[1][x], k = s_seg[2][x], P = s_seg[3][x];
-              const uint32_t s = s_st[w * ns + x];
-              // run piece 1: global [o + s, o + e1), e1 = min(s + k, n), t = i - o - s;
-              // run piece 2: global [o, o + s + k - e1) (empty unless the run wraps), t = i - o + n - s.
-              // (Written without a conditional: a select of this form was folded away by the compiler.)
-              const uint32_t e1 = min(s + k, n);
-              const uint32_t a1 = max(lo, o + s), b1 = min(hi, o + e1);
-              const uint32_t a2 = max(lo, o), b2 = min(hi, o + (s + k - e1));
-              if (a1 >= b1 && a2 >= b2) continue;
-#pragma unroll
-              for (int r = 0; r < kR; ++r) {
-                const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                  const uint32_t i = i0 + q;
-                  if (i >= a1 && i < b1) a[r][q] += v[P + (i - o - s)];
-                  else if (i >= a2 && i < b2) a[r][q] += v[P + (i - o + n - s)];
-                }
-              }
-            }
-          }
-        }
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t i = i0 + (uint32_t)q;
+        if (i >= a1 && i < b1) a[q] += v[i - o - sw];
+        else if (i >= lo && i < b2) a[q] += v[i - o + n - sw];
       }
     }
-#pragma unroll
-    for (int r = 0; r < kR; ++r) {
-      const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-      const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-      agg_emit4(O, i0, nv, a[r]);
-    }
   }
+  uint32_t mask = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (i0 + (uint32_t)q >= lo && i0 + (uint32_t)q < hi) mask |= 1u << q;
+  if (mask) agg_emit4m(O, i0, mask, a);
 }
 
 // Shared block starts: the column sums of the W workers' values (worker order, from +0.0).

@@ -54,6 +54,7 @@ struct ef_layout {
   double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0;
 
   std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg;
+  std::vector<uint32_t> btile;  // block aggregate, multi-segment: (data tile, segment) pairs
   std::vector<uint64_t> tau;
   std::vector<uint32_t> ulo;
   int64_t K = 0;
@@ -63,7 +64,7 @@ struct ef_layout {
   bool rk_direct = false;  // random-k: every segment's rows and expected window fit k_select's LDS
 
   Blob blob;
-  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg;
+  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_btile;
   Tables T{};
   bool bound = false;
 
@@ -156,6 +157,19 @@ void ef_layout::build() {
     csl[c] = m;
   }
 
+  // block aggregate over several segments: every (1024-element data tile, segment) pair with an
+  // element in common, segment by segment
+  btile.clear();
+  if (n > 1) {
+    for (int s = 0; s < n; ++s) {
+      const int64_t t0 = off64[s] / kAggBT, t1 = (off64[s + 1] - 1) / kAggBT;
+      for (int64_t t = t0; t <= t1; ++t) {
+        btile.push_back((uint32_t)t);
+        btile.push_back((uint32_t)s);
+      }
+    }
+  }
+
   blob = Blob();
   o_off = blob.add(off);
   o_k = blob.add(k);
@@ -171,6 +185,7 @@ void ef_layout::build() {
   o_csf = blob.add(csf);
   o_csl = blob.add(csl);
   o_rseg = blob.add(rseg);
+  o_btile = blob.add(btile);
   bound = false;
 }
 
@@ -290,24 +305,6 @@ bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
     const int _rc = (x);       \
     if (_rc != EF_OK) return _rc; \
   } while (0)
-
-// Workgroups of `threads` threads that fit on the device at once for a persistent kernel
-// (computed once per kernel; every GPU this library drives is the same part).
-unsigned resident_blocks(const void* kernel, int threads) {
-  static std::mutex mu;
-  static std::vector<std::pair<const void*, unsigned>> cache;
-  std::lock_guard<std::mutex> lk(mu);
-  for (const auto& c : cache)
-    if (c.first == kernel) return c.second;
-  int dev = 0, cus = 0, per = 0;
-  unsigned n = 1024u;
-  if (hipGetDevice(&dev) == hipSuccess &&
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, 0) == hipSuccess && cus > 0 && per > 0)
-    n = (unsigned)(cus * per);
-  cache.emplace_back(kernel, n);
-  return n;
-}
 
 int check_bound(const ef_layout* L) {
   if (!L || !L->bound) return EF_EINVAL;
@@ -630,6 +627,8 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_ulo = reinterpret_cast<const uint32_t*>(b + L->o_ulo);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
   T.chunk_sl = reinterpret_cast<const int32_t*>(b + L->o_csl);
+  T.btile = reinterpret_cast<const uint32_t*>(b + L->o_btile);
+  T.nbtiles = (int32_t)(L->btile.size() / 2);
   T.d = (int32_t)L->d;
   T.L = L->L;
   T.nchunks = L->nchunks;
@@ -841,8 +840,7 @@ int run_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m
                 m, val, O);
       return launched();
     }
-    const unsigned g = std::min<unsigned>((unsigned)L->nchunks, resident_blocks((const void*)k_agg_block, kNT));
-    EF_LAUNCH(k_agg_block, dim3(g), blk, 0, st, L->T, W, (int32_t)L->K, m, val, O);
+    EF_LAUNCH(k_agg_block, dim3((unsigned)L->T.nbtiles), blk, 0, st, L->T, W, (int32_t)L->K, m, val, O);
     return launched();
   }
   return EF_EINVAL;
