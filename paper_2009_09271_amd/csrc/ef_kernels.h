@@ -1365,12 +1365,11 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 // any order: the selection over the list does not depend on it; row r appends to sub-list
 // r % kSubLists, which spreads the atomics on the list counters).  Top-k: above / inside bin B of
 // a histogrammed segment.  Random-k: Philox key below ulo_l / in [ulo_l, tau_l).
-// One wavefront per kCollectRows consecutive rows: the rows' segments, candidate counts and first
-// 64 candidate keys are loaded together; counts and list positions come from ballots, and each
-// chunk of 64 candidates reserves its list space with one atomic.
-constexpr uint32_t kCollectRows = 4;                          // rows per wavefront
-constexpr uint32_t kCollectRowsWG = (kNT / 64) * kCollectRows;  // rows per workgroup
-template <int KIND>
+// One wavefront per CR consecutive rows (CR = 1 for one or a few workers, where the rows are the
+// whole grid; more per wavefront for a batch): the rows' segments, candidate counts and first 64
+// candidate keys are loaded together; counts and list positions come from ballots, and each chunk
+// of 64 candidates reserves its list space with one atomic.
+template <int KIND, uint32_t kCollectRows>
 __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   const uint32_t lane = threadIdx.x & 63;
@@ -1897,8 +1896,8 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
 // serves its rows in one or a few passes of 64 candidates, the next pass's loads in flight while
 // the current one is written.  A winner's position is its row's offset plus the row's winners
 // before it: earlier passes (kept by the row's lane) and a ballot count over the row's lanes in
-// this pass.  RW = 16 for random-k (a few candidates per row); 4 for top-k, whose rows in the
-// layers of largest magnitude hold hundreds.
+// this pass.  RW = 16 for random-k (a few candidates per row); for top-k, whose rows in the layers
+// of largest magnitude hold hundreds, 1 for one or a few workers and 4 for a batch.
 template <uint32_t RW>
 __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT,
                                               int certain_zeroed) {

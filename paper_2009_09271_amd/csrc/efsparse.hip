@@ -352,6 +352,8 @@ struct Steps {
 // Each phase runs for all W workers before the next: the streaming passes one launch per worker,
 // every other kernel once per kBatchMax workers (the worker is the grid's second dimension), so
 // the short latency-bound selection kernels are paid once for the batch.
+constexpr int kWideBatch = 8;  // batches of at least this many workers take the batch forms
+
 template <int KIND>
 int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream) {
   WsLayout wl;
@@ -415,9 +417,13 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     const WSel w = ws_of(c0);
     const Batch bt = batch_of(c0, (int)nw);
     const dim3 rgrid((unsigned)L->nrows, nw), sgrid((unsigned)L->L, nw);
-    constexpr uint32_t kEmitRW = KIND == 0 ? 4u : 16u;  // rows per wavefront of the emission
-    constexpr uint32_t kEmitRows = (kNT / 64) * kEmitRW;
-    const dim3 egrid((unsigned)((L->nrows + kEmitRows - 1) / kEmitRows), nw);
+    // rows per wavefront of the collection and of the emission: top-k rows hold hundreds of
+    // candidates, so one row per wavefront for one or a few workers (the most parallel form) and
+    // four for a batch (fewer, fuller wavefronts); random-k rows hold a few, 16 per wavefront
+    const bool wide = nw >= kWideBatch;
+    const uint32_t emit_rw = KIND == 1 ? 16u : wide ? 4u : 1u;
+    const uint32_t emit_rows = (kNT / 64) * emit_rw;
+    const dim3 egrid((unsigned)((L->nrows + emit_rows - 1) / emit_rows), nw);
     uint32_t* idx = P.idx + (uint64_t)c0 * K;
     float* val = P.val + (uint64_t)c0 * K;
     if (KIND == 0 ? !L->all_exact : !L->rk_direct) {
@@ -425,8 +431,10 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
         EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w, bt);
         EF_TRY(launched());
       }
-      const dim3 cgrid((unsigned)((L->nrows + kCollectRowsWG - 1) / kCollectRowsWG), nw);
-      EF_LAUNCH(k_collect<KIND>, cgrid, blk, 0, st, T, w, bt);
+      const uint32_t crows = (kNT / 64) * (wide ? 4u : 1u);  // rows per workgroup
+      const dim3 cgrid((unsigned)((L->nrows + crows - 1) / crows), nw);
+      if (wide) EF_LAUNCH((k_collect<KIND, 4>), cgrid, blk, 0, st, T, w, bt);
+      else EF_LAUNCH((k_collect<KIND, 1>), cgrid, blk, 0, st, T, w, bt);
       EF_TRY(launched());
     }
     if (L->big) {
@@ -439,7 +447,10 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
       EF_LAUNCH((k_select<KIND, false>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
     }
     EF_TRY(launched());
-    EF_LAUNCH(k_emit<kEmitRW>, egrid, blk, 0, st, T, w, idx, val, bt, KIND == 1 && L->rk_direct && P.e ? 1 : 0);
+    const int cz = KIND == 1 && L->rk_direct && P.e ? 1 : 0;
+    if (emit_rw == 16u) EF_LAUNCH(k_emit<16>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else if (emit_rw == 4u) EF_LAUNCH(k_emit<4>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else EF_LAUNCH(k_emit<1>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
     EF_TRY(launched());
   }
   return EF_OK;
