@@ -76,6 +76,7 @@ extern "C" {
 #define EF_OP_AGG_SPARSE 3
 #define EF_OP_AGG_BLOCK 4
 #define EF_OP_AGG_SHARED 5
+#define EF_OP_RANDK_PREP 6
 
 /* message kinds */
 #define EF_MSG_SPARSE 0
@@ -131,7 +132,8 @@ int ef_layout_bind(ef_layout* layout, void* dev_tables, size_t bytes, void* stre
  * ef_step_topk, EF_OP_RANDK for compress_randk / ef_step_randk,
  * EF_OP_AGG_SPARSE / EF_OP_AGG_BLOCK for decompress_aggregate and
  * decompress_aggregate_apply with W workers, EF_OP_AGG_SHARED for
- * decompress_aggregate_shared (W is ignored otherwise).  Random-block needs
+ * decompress_aggregate_shared, EF_OP_RANDK_PREP for ef_randk_prepare and
+ * ef_step_randk_prepared (W is ignored otherwise).  Random-block needs
  * none (returns 0).
  * Returns 0 for a null layout or unknown op. */
 size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W);
@@ -286,6 +288,39 @@ int ef_step_topk_batch(const ef_layout* layout, unsigned phases, int32_t W, cons
 int ef_step_randk_batch(const ef_layout* layout, unsigned phases, int32_t W, const void* const* g,
                         int g_dtype, float* const* e, const uint64_t* seeds, uint32_t step, uint32_t* idx,
                         float* val, void* ws, size_t ws_stride, void* stream);
+
+/* Random-k with the selection prepared ahead (Section 3, random-k).  The
+ * keys that choose the k_l coordinates of every segment depend only on the
+ * seed, the step and the position, not on the gradient, so the message
+ * indices can be computed before the gradient exists (for instance for step
+ * t + 1 while step t runs, or during the backward pass); the step itself is
+ * then one streaming pass.  ef_randk_prepare followed by
+ * ef_step_randk_prepared gives bitwise the result of ef_step_randk.
+ *
+ * ef_randk_prepare: the message indices of (seed, step) and their tile table.
+ *   idx   uint32[K], written: the indices, ascending within each segment
+ *   ws    device, 256-byte aligned, ws_bytes >= ef_workspace_bytes(layout,
+ *         EF_OP_RANDK_PREP, 1); on return it holds the tile table that
+ *         ef_step_randk_prepared reads, valid until the next call on ws
+ * ef_step_randk_prepared: the worker step given the prepared indices:
+ *   acc = g + e; val[j] = acc[idx[j]]; e = acc with +0 at idx (e_{t+1}).
+ *   idx, ws as written by ef_randk_prepare for this layout (read only);
+ *   g, g_dtype, e, val as for ef_step_randk.
+ * The _batch forms do W workers: seeds a host array of W seeds, idx and val
+ * [W][K] (row w is worker w's), worker w's workspace at ws + w * ws_stride
+ * (ws_stride a multiple of 256, >= the single worker's bytes), g and e host
+ * arrays of W device pointers.  Errors are reported before anything is
+ * enqueued, except that a batch checks all its arguments first and then
+ * launches worker by worker. */
+int ef_randk_prepare(const ef_layout* layout, uint64_t seed, uint32_t step, uint32_t* idx, void* ws,
+                     size_t ws_bytes, void* stream);
+int ef_randk_prepare_batch(const ef_layout* layout, int32_t W, const uint64_t* seeds, uint32_t step,
+                           uint32_t* idx, void* ws, size_t ws_stride, void* stream);
+int ef_step_randk_prepared(const ef_layout* layout, const void* g, int g_dtype, float* e, const uint32_t* idx,
+                           float* val, const void* ws, size_t ws_bytes, void* stream);
+int ef_step_randk_prepared_batch(const ef_layout* layout, int32_t W, const void* const* g, int g_dtype,
+                                 float* const* e, const uint32_t* idx, float* val, const void* ws,
+                                 size_t ws_stride, void* stream);
 
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could

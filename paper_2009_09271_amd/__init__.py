@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("EFSPARSE_LIB") or os.path.join(_HERE, "libefsparse.so
 
 EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP = range(5)
 EF_F32, EF_BF16 = 0, 1
-EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK, EF_OP_AGG_SHARED = range(6)
+EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK, EF_OP_AGG_SHARED, EF_OP_RANDK_PREP = range(7)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
 EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA = range(4)
 EF_PHASE_PREPARE, EF_PHASE_STREAM, EF_PHASE_FINISH, EF_PHASE_ALL = 1, 2, 4, 7
@@ -74,6 +74,10 @@ _SIGS = {
     "ef_step_topk_batch": (_c.c_int, [_P, _c.c_uint, _c.c_int32, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk_batch": (_c.c_int, [_P, _c.c_uint, _c.c_int32, _P, _c.c_int, _P, _P, _c.c_uint32, _P, _P, _P,
                                        _c.c_size_t, _P]),
+    "ef_randk_prepare": (_c.c_int, [_P, _c.c_uint64, _c.c_uint32, _P, _P, _c.c_size_t, _P]),
+    "ef_randk_prepare_batch": (_c.c_int, [_P, _c.c_int32, _P, _c.c_uint32, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randk_prepared": (_c.c_int, [_P, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
+    "ef_step_randk_prepared_batch": (_c.c_int, [_P, _c.c_int32, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_topk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _P, _P, _P, _c.c_size_t, _P]),
     "ef_step_randk_phases": (_c.c_int, [_P, _c.c_uint, _P, _c.c_int, _P, _c.c_uint64, _c.c_uint32, _P, _P, _P,
                                         _c.c_size_t, _P]),
@@ -301,6 +305,35 @@ def ef_step_randk_batch(layout, g, e, seeds, step, idx, val, ws, ws_stride, phas
     _check(_lib.ef_step_randk_batch(layout.handle, int(phases), len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
                                     sd.ctypes.data, int(step), _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride),
                                     _stream(e[0], stream)), "ef_step_randk_batch")
+
+
+def ef_randk_prepare(layout, seed, step, idx, ws, stream=None):
+    """The random-k message indices of (seed, step) and their tile table in ws (EF_OP_RANDK_PREP)."""
+    _check(_lib.ef_randk_prepare(layout.handle, int(seed), int(step), _ptr(idx), _ptr(ws), ws.numel(),
+                                 _stream(idx, stream)), "ef_randk_prepare")
+
+
+def ef_randk_prepare_batch(layout, seeds, step, idx, ws, ws_stride, stream=None):
+    """W workers' prepared selections: seeds W integers (host); idx [W][K]; ws rows from batch_workspace
+    (EF_OP_RANDK_PREP)."""
+    sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64))
+    _check(_lib.ef_randk_prepare_batch(layout.handle, sd.shape[0], sd.ctypes.data, int(step), _ptr(idx), _ptr(ws),
+                                       int(ws_stride), _stream(idx, stream)), "ef_randk_prepare_batch")
+
+
+def ef_step_randk_prepared(layout, g, e, idx, val, ws, stream=None):
+    """The random-k step given prepared indices and workspace."""
+    _check(_lib.ef_step_randk_prepared(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val), _ptr(ws),
+                                       ws.numel(), _stream(e, stream)), "ef_step_randk_prepared")
+
+
+def ef_step_randk_prepared_batch(layout, g, e, idx, val, ws, ws_stride, stream=None):
+    """W workers' random-k steps given their prepared indices (rows of idx) and workspaces (rows of ws)."""
+    if len(g) != len(e):
+        raise ValueError("one gradient and one residual per worker")
+    _check(_lib.ef_step_randk_prepared_batch(layout.handle, len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
+                                             _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride), _stream(e[0], stream)),
+           "ef_step_randk_prepared_batch")
 
 
 def ef_step_randblock(layout, g, e, seed, step, start, val, stream=None):

@@ -331,8 +331,9 @@ __device__ __forceinline__ float column_sum(const float* v, int32_t W, int32_t K
   return s;
 }
 
-// tile_start[w][tau] = first entry of message w whose index lies in an aggregate tile >= tau
-// (tau = 0..nt; an index >= d counts as tile nt).  Grid: (ceil(K / kNT), W), one thread per entry.
+// tile_start[w * ts_stride + tau] = first entry of message w whose index lies in an aggregate tile
+// >= tau (tau = 0..nt; an index >= d counts as tile nt).  Grid: (ceil(K / kNT), W), one thread per
+// entry.
 // With `sums` (shared coordinates: W = 1 message whose values are vW workers' rows `vals`), entry
 // j's thread also writes sums[j], the column sum of the rows in worker order.
 // Entry j starts the tiles after its predecessor's tile, up to its own (past the last entry the
@@ -343,14 +344,14 @@ constexpr uint32_t kRunOwn = 128;  // runs of at most this many tiles are writte
                                    // longer ones (at most nt / 128 per message) by the workgroup
 
 __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
-                                                    uint32_t* tile_start, const float* vals, int32_t vW,
-                                                    float* sums) {
+                                                    uint32_t* tile_start, uint64_t ts_stride, const float* vals,
+                                                    int32_t vW, float* sums) {
   __shared__ uint32_t s_nlong;
   __shared__ uint32_t s_ta[kNT], s_n[kNT], s_j[kNT], s_own[kNT];  // the workgroup's long runs
   const uint32_t j = blockIdx.x * kNT + threadIdx.x;
   const int w = blockIdx.y;
   const uint32_t* m = idx + (size_t)w * K;
-  uint32_t* ts = tile_start + (size_t)w * (nt + 1);
+  uint32_t* ts = tile_start + (size_t)w * ts_stride;
   auto tile = [&](uint32_t i) -> uint32_t { return i < (uint32_t)d ? i / kAggTile : (uint32_t)nt; };
   // tile tau of entry e's run starts at e, except past the last entry's own tile (at K)
   auto value = [&](uint32_t e, uint32_t tau, uint32_t e_own) -> uint32_t {
@@ -379,7 +380,7 @@ __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_
   for (uint32_t q = 0; q < s_nlong; ++q) {
     const uint32_t qa = s_ta[q], qe = qa + s_n[q], qj = s_j[q], qown = s_own[q];
     // 16-byte stores over the part of the run aligned in memory, single words at its two ends
-    const size_t base = (size_t)w * (nt + 1);
+    const size_t base = (size_t)w * ts_stride;
     const uint32_t a4 = min(qe, qa + (uint32_t)((4u - (base + qa) % 4u) % 4u));
     const uint32_t b4 = a4 + (qe - a4) / 4u * 4u;
     if (threadIdx.x < a4 - qa) ts[qa + threadIdx.x] = value(qj, qa + threadIdx.x, qown);
@@ -697,6 +698,54 @@ __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t 
   if (mask) agg_emit4m(O, i0, mask, a);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Random-k with the selection prepared ahead: the keys depend only on the seed, the step and the
+// position (Section 3, random-k), so the message indices can be chosen before the gradient
+// exists.  The step is then one streaming pass, one workgroup per kAggTile-element tile (one
+// float4 group per thread): acc = g + e; the tile's winners (entries [ts[t], ts[t + 1]) of the
+// prepared message, in ascending order) take their values from acc, and e = acc with +0 there.
+// ---------------------------------------------------------------------------------------------
+static_assert(kAggTile == 4u * kNT, "one float4 group per thread");
+
+template <int GDT>
+__global__ __launch_bounds__(kNT) void k_randk_apply(int32_t d, int32_t K, const uint32_t* ts, const uint32_t* idx,
+                                                     const void* g, float* e, float* val) {
+  __shared__ int32_t slot[kAggTile];  // element of the tile -> its winner's message entry, or -1
+  const uint32_t t = blockIdx.x, lo = t * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
+  const uint32_t i0 = lo + threadIdx.x * 4u;
+  const uint32_t ja = ts[t], jb = min(ts[t + 1], (uint32_t)K);
+  const bool whole = hi - lo == kAggTile;
+  const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+  float gv[4], ev[4];
+  if (whole) {
+    load4gf<GDT>(g, i0, gv);
+    load4f(e, i0, ev);
+  } else {
+    load4g<GDT>(g, i0, nv, gv);
+    load4(e, i0, nv, ev);
+  }
+  *reinterpret_cast<int4*>(&slot[threadIdx.x * 4u]) = make_int4(-1, -1, -1, -1);
+  __syncthreads();
+  for (uint32_t j = ja + threadIdx.x; j < jb; j += kNT) {
+    const uint32_t x = idx[j] - lo;
+    if (x < kAggTile) slot[x] = (int32_t)j;
+  }
+  __syncthreads();
+  const int4 sl = *reinterpret_cast<const int4*>(&slot[threadIdx.x * 4u]);
+  const int32_t s4[4] = {sl.x, sl.y, sl.z, sl.w};
+  float a[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    a[q] = gv[q] + ev[q];
+    if (s4[q] >= 0) {
+      val[s4[q]] = a[q];
+      a[q] = 0.0f;
+    }
+  }
+  if (whole) store4(e, i0, 4, a);
+  else store4(e, i0, nv, a);
+}
+
 // Shared block starts: the column sums of the W workers' values (worker order, from +0.0).
 __global__ __launch_bounds__(kNT) void k_shared_sum(int32_t W, int32_t K, const float* val, float* sum) {
   const uint32_t j = blockIdx.x * kNT + threadIdx.x;
@@ -841,7 +890,11 @@ __device__ void slow_select(const Tables& T, int l, const float* data, float* e_
                             float* out_val, uint32_t s0, uint32_t s1, uint32_t step, uint32_t* hist, uint32_t* lds) {
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
   const uint32_t P = (uint32_t)T.seg_P[l], kl = (uint32_t)T.seg_k[l];
-  auto keyat = [&](uint32_t j) -> uint32_t { return sel_key<KIND>(o + j, data[o + j], o, l, step, s0, s1); };
+  // random-k keys depend on the position only: without data (a selection prepared ahead of the
+  // step) only the indices are written
+  auto keyat = [&](uint32_t j) -> uint32_t {
+    return sel_key<KIND>(o + j, KIND == 1 && !data ? 0.0f : data[o + j], o, l, step, s0, s1);
+  };
   uint32_t prefix = 0, need = kl;
   int known = 0;
   while (known < 32) {
@@ -877,7 +930,7 @@ __device__ void slow_select(const Tables& T, int l, const float* data, float* e_
     if ((a || (b && eb < r)) && ea + min(eb, r) < kl) {
       const uint32_t pos = P + ea + min(eb, r);
       out_idx[pos] = o + j;
-      out_val[pos] = data[o + j];
+      if (out_val) out_val[pos] = data[o + j];
       if (e_zero) e_zero[o + j] = 0.0f;
     }
     run_a += tot & 0xFFFFu;
@@ -1172,6 +1225,12 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       // random-k, direct lists: stored below, once the certain winners are known
       if (!(KIND == 1 && direct)) store4m(acc_out, i0, vm[r], v[r]);
     }
+  } else if (KIND == 1 && !src) {
+    // random-k without data (a selection prepared ahead of the step): keys and positions only
+#pragma unroll
+    for (int r = 0; r < kSR; ++r)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[r][q] = 0.0f;
   } else {
 #pragma unroll
     for (int r = 0; r < kSR; ++r) {
@@ -1559,7 +1618,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   float* e_zero = BT.e[blockIdx.y];
   const float* data = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];  // acc
   out_idx = shifted(out_idx, (uint64_t)blockIdx.y * BT.msg * 4u);
-  out_val = shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u);
+  out_val = out_val ? shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u) : nullptr;
   const uint32_t s0 = BT.seed_lo[blockIdx.y], s1 = BT.seed_hi[blockIdx.y];
   constexpr uint32_t kPer = kSelPer;  // rows per thread held in registers (more are re-read)
   __shared__ uint32_t hist[kHBins];
@@ -1905,7 +1964,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   float* e_zero = BT.e[blockIdx.y];
   out_idx = shifted(out_idx, (uint64_t)blockIdx.y * BT.msg * 4u);
-  out_val = shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u);
+  out_val = out_val ? shifted(out_val, (uint64_t)blockIdx.y * BT.msg * 4u) : nullptr;
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * RW;
   if (row0 >= (uint32_t)T.nrows) return;
@@ -1975,7 +2034,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
     const uint32_t pos = roffr + (uint32_t)__popcll(bw & below);
     if (win && pos < rpend) {
       out_idx[pos] = ci;
-      out_val[pos] = cv;
+      if (out_val) out_val[pos] = cv;
       // random-k, direct lists: the streaming pass already zeroed e at the certain winners (key' of
       // a key below ulo)
       if (e_zero && !(~ck < rulo)) e_zero[ci] = 0.0f;

@@ -425,7 +425,7 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     const uint32_t emit_rows = (kNT / 64) * emit_rw;
     const dim3 egrid((unsigned)((L->nrows + emit_rows - 1) / emit_rows), nw);
     uint32_t* idx = P.idx + (uint64_t)c0 * K;
-    float* val = P.val + (uint64_t)c0 * K;
+    float* val = P.val ? P.val + (uint64_t)c0 * K : nullptr;  // none: a selection prepared ahead
     if (KIND == 0 ? !L->all_exact : !L->rk_direct) {
       if (KIND == 0) {
         EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w, bt);
@@ -660,6 +660,9 @@ size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W) {
       if (W < 1) return 0;
       return align_up((size_t)W * ((size_t)agg_tiles(layout->d) + 1) * 4, kAlign);
     case EF_OP_AGG_BLOCK: return 0;
+    case EF_OP_RANDK_PREP:
+      // the random-k selection's workspace, then the prepared message's tile table
+      return layout->ws_layout(EF_OP_RANDK).total + align_up(((size_t)agg_tiles(layout->d) + 1) * 4, kAlign);
     case EF_OP_AGG_SHARED:
       if (W < 1) return 0;
       // the column sums and one message's tile ranges
@@ -750,6 +753,82 @@ int ef_step_randk_batch(const ef_layout* L, unsigned phases, int32_t W, const vo
   return step_batch(1, L, phases, W, g, g_dtype, e, seeds, step, idx, val, ws, ws_stride, stream);
 }
 
+// Random-k prepared ahead: W workers' selections without data (their streaming passes compute
+// keys only), the message indices emitted, and each message's tile table after the selection's
+// part of its workspace.
+static int prepare_randk(const ef_layout* L, int32_t W, const uint64_t* seeds, uint32_t step, uint32_t* idx, void* ws,
+                  size_t ws_bytes, size_t ws_stride, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!seeds || !word_ok(idx) || !ws || !aligned(ws, kAlign)) return EF_EINVAL;
+  if (ws_bytes < ef_workspace_bytes(L, EF_OP_RANDK_PREP, 1)) return EF_EWORKSPACE;
+  std::vector<const float*> none((size_t)W, nullptr);
+  Steps P;
+  P.W = W;
+  P.src = none.data();
+  P.idx = idx;
+  P.ws = static_cast<uint8_t*>(ws);
+  P.ws_bytes = ws_bytes;
+  P.ws_stride = ws_stride;
+  P.seeds = seeds;
+  P.step = step;
+  EF_TRY(run_select<1>(L, P, EF_PHASE_ALL, stream));
+  const int32_t nt = agg_tiles(L->d);
+  const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
+  uint32_t* ts = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + L->ws_layout(EF_OP_RANDK).total);
+  EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), dim3(kNT), 0, S(stream), L->T.d, (int32_t)L->K, nt,
+            idx, ts, (uint64_t)(ws_stride / 4), nullptr, 0, nullptr);
+  return launched();
+}
+
+static int apply_randk(const ef_layout* L, const void* g, int g_dtype, float* e, const uint32_t* idx, float* val,
+                const void* ws, size_t ws_bytes, hipStream_t st) {
+  EF_TRY(check_g(g, g_dtype));
+  if (!vec_ok(e) || !word_ok(idx) || !word_ok(val) || !ws || !aligned(ws, kAlign)) return EF_EINVAL;
+  if (ws_bytes < ef_workspace_bytes(L, EF_OP_RANDK_PREP, 1)) return EF_EWORKSPACE;
+  const uint32_t* ts =
+      reinterpret_cast<const uint32_t*>(static_cast<const uint8_t*>(ws) + L->ws_layout(EF_OP_RANDK).total);
+  const dim3 grid((unsigned)agg_tiles(L->d)), blk(kNT);
+  if (g_dtype == EF_F32)
+    EF_LAUNCH(k_randk_apply<0>, grid, blk, 0, st, L->T.d, (int32_t)L->K, ts, idx, g, e, val);
+  else
+    EF_LAUNCH(k_randk_apply<1>, grid, blk, 0, st, L->T.d, (int32_t)L->K, ts, idx, g, e, val);
+  return launched();
+}
+
+int ef_randk_prepare(const ef_layout* L, uint64_t seed, uint32_t step, uint32_t* idx, void* ws, size_t ws_bytes,
+                     void* stream) {
+  return prepare_randk(L, 1, &seed, step, idx, ws, ws_bytes, 0, stream);
+}
+
+int ef_randk_prepare_batch(const ef_layout* L, int32_t W, const uint64_t* seeds, uint32_t step, uint32_t* idx,
+                           void* ws, size_t ws_stride, void* stream) {
+  if (ws_stride % kAlign) return EF_EINVAL;
+  return prepare_randk(L, W, seeds, step, idx, ws, ws_stride, ws_stride, stream);
+}
+
+int ef_step_randk_prepared(const ef_layout* L, const void* g, int g_dtype, float* e, const uint32_t* idx,
+                           float* val, const void* ws, size_t ws_bytes, void* stream) {
+  EF_TRY(check_bound(L));
+  return apply_randk(L, g, g_dtype, e, idx, val, ws, ws_bytes, S(stream));
+}
+
+int ef_step_randk_prepared_batch(const ef_layout* L, int32_t W, const void* const* g, int g_dtype, float* const* e,
+                                 const uint32_t* idx, float* val, const void* ws, size_t ws_stride, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!g || !e || !word_ok(idx) || !word_ok(val) || ws_stride % kAlign) return EF_EINVAL;
+  for (int32_t w = 0; w < W; ++w) {  // every argument before the first launch
+    EF_TRY(check_g(g[w], g_dtype));
+    if (!vec_ok(e[w])) return EF_EINVAL;
+  }
+  const uint64_t K = (uint64_t)L->K;
+  for (int32_t w = 0; w < W; ++w)
+    EF_TRY(apply_randk(L, g[w], g_dtype, e[w], idx + (uint64_t)w * K, val + (uint64_t)w * K,
+                       static_cast<const uint8_t*>(ws) + (uint64_t)w * ws_stride, ws_stride, S(stream)));
+  return EF_OK;
+}
+
 int compress_randk(const ef_layout* L, const float* acc, uint64_t seed, uint32_t step, uint32_t* idx, float* val,
                    void* ws, size_t ws_bytes, void* stream) {
   EF_TRY(check_bound(L));
@@ -838,7 +917,7 @@ int run_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m
     uint32_t* ts = reinterpret_cast<uint32_t*>(ws);
     const int32_t nt = agg_tiles(L->d);
     EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts,
-              val, vW, sums);
+              (uint64_t)(nt + 1), val, vW, sums);
     EF_TRY(launched());
     EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), dim3(64), 0, st, L->T.d, W, (int32_t)L->K, nt, m,
               sums ? sums : val, ts, O);
