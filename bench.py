@@ -134,6 +134,27 @@ def measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, ar
     return res
 
 
+def measure_prepared(E, torch, dev, timed, entry, lay, g, e, seeds, mv, step_b, d):
+    """Random-k with the selection prepared ahead: the prepare call alone (it needs no gradient, so
+    it can run any time before the step) and the prepared step alone, with its kernel split."""
+    res = {}
+    wsp = [lay.workspace(E.EF_OP_RANDK_PREP, 1, dev)]
+    idx = [torch.empty(lay.K, dtype=torch.int32, device=dev)]
+    def split(fn):  # per-kernel averages of fn's launches (library events, a separate pass)
+        E.timing_collect(reset=True)
+        E.timing_enable(True)
+        timed(fn)
+        E.timing_enable(False)
+        return {name: round(tot * 1e3 / nl, 3) for name, (tot, nl) in E.timing_collect(reset=True).items()}
+
+    prep = lambda: E.ef_randk_prepare(lay, seeds[0], 0, idx[0], wsp[0])  # noqa: E731
+    res["prepare"] = {"us": round(timed(prep), 3), "kernels_us": split(prep)}
+    step = lambda: E.ef_step_randk_prepared(lay, g[0], e, idx[0], mv[0], wsp[0])  # noqa: E731
+    res["prepared_step"] = entry(timed(step), step_b, d)
+    res["prepared_step"]["kernels_us"] = split(step)
+    return res
+
+
 def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20):
     """Each compressor at the given scope: one worker's step alone (the fused entry point, and the
     composed calls accumulate + compress + update), and the aggregate of the W workers' messages
@@ -201,6 +222,8 @@ def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20)
                                          for name, (tot, nl) in E.timing_collect(reset=True).items()}
         # composed: the same algorithmic bytes (the intermediate acc costs 8d more by construction)
         r["composed_step"] = entry(timed(composed), step_b, d)
+        if kind == "randk":
+            r.update(measure_prepared(E, torch, dev, timed, entry, lay, g, e, seeds, mv, step_b, d))
         with torch.cuda.stream(st):
             for w in range(W):
                 fused(w)
