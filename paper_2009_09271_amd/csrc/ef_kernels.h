@@ -129,39 +129,44 @@ struct SubLists {
 // ---------------------------------------------------------------------------------------------
 // Utility kernels
 // ---------------------------------------------------------------------------------------------
-// Algorithm 1 accumulate step: acc = g + e.
-template <int GDT>
-__global__ __launch_bounds__(kNT) void k_accumulate(int32_t d, const void* g, const float* e, float* acc) {
-  const uint32_t lo = blockIdx.x * kTile, hi = min((uint32_t)d, lo + kTile);
-  float gv[kRounds][4], ev[kRounds][4];
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    load4g<GDT>(g, i0, nv, gv[r]);
-    load4(e, i0, nv, ev[r]);
-  }
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float a[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) a[q] = gv[r][q] + ev[r][q];
-    store4(acc, i0, nv, a);
-  }
+// The plain streaming kernels take one float4 group per thread in 64-thread workgroups (kRbTile
+// elements each): short-lived workgroups keep the end of the grid short, where a streaming pass
+// otherwise loses bandwidth.  Measured for the fused block-random-k step on ResNet-50 flat: 64
+// threads 47.2 us per step, 128: 48.2, 256: 48.6; four float4 groups per thread: about 50.5.
+constexpr int kRbNT = 64;
+constexpr uint32_t kRbTile = 4u * kRbNT;
+
+__device__ __forceinline__ int group_extent(uint32_t i0, uint32_t hi) {
+  return i0 < hi ? (int)min(4u, hi - i0) : 0;
 }
 
-__global__ __launch_bounds__(kNT) void k_copy(int32_t d, const float* src, float* dst) {
-  const uint32_t lo = blockIdx.x * kTile, hi = min((uint32_t)d, lo + kTile);
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float v[4];
-    load4(src, i0, nv, v);
-    store4(dst, i0, nv, v);
+// Algorithm 1 accumulate step: acc = g + e.
+template <int GDT>
+__global__ __launch_bounds__(kRbNT) void k_accumulate(int32_t d, const void* g, const float* e, float* acc) {
+  const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)d, lo + kRbTile);
+  const uint32_t i0 = lo + threadIdx.x * 4u;
+  const int nv = group_extent(i0, hi);
+  float gv[4], ev[4], a[4];
+  if (hi - lo == kRbTile) {  // whole group (every workgroup but the last)
+    load4gf<GDT>(g, i0, gv);
+    load4f(e, i0, ev);
+  } else {
+    load4g<GDT>(g, i0, nv, gv);
+    load4(e, i0, nv, ev);
   }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) a[q] = gv[q] + ev[q];
+  store4(acc, i0, nv, a);
+}
+
+__global__ __launch_bounds__(kRbNT) void k_copy(int32_t d, const float* src, float* dst) {
+  const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)d, lo + kRbTile);
+  const uint32_t i0 = lo + threadIdx.x * 4u;
+  const int nv = group_extent(i0, hi);
+  float v[4];
+  if (hi - lo == kRbTile) load4f(src, i0, v);
+  else load4(src, i0, nv, v);
+  store4(dst, i0, nv, v);
 }
 
 // e[idx[j]] = +0 for every message entry (indices outside [0, d) are skipped).
@@ -197,10 +202,7 @@ __device__ __forceinline__ uint32_t run_pos(const RunSeg& r, uint32_t i) {
 }
 
 // Fused worker step: acc = g + e; val[P_l + t] = acc on the run; e' = +0 on the run, acc elsewhere.
-// One float4 group per thread (kRbTile elements per workgroup): short-lived workgroups keep the
-// end of the grid short, where a pure streaming pass otherwise loses bandwidth.
-constexpr int kRbNT = 64;  // threads per workgroup (64: 47.2 us per step on ResNet-50 flat; 128: 48.2; 256: 48.6)
-constexpr uint32_t kRbTile = 4u * kRbNT;
+// One float4 group per thread (kRbTile elements per workgroup).
 template <int GDT>
 __global__ __launch_bounds__(kRbNT) void k_randblock_step(Tables T, const void* g, float* e, uint32_t s0,
                                                         uint32_t s1, uint32_t step, uint32_t* start,
@@ -280,30 +282,29 @@ __global__ __launch_bounds__(kNT) void k_block_zero(Tables T, int32_t K, const u
   e[o + j] = 0.0f;
 }
 
-// Out-of-place residual update for a block message: e = +0 on the runs, acc elsewhere.
-__global__ __launch_bounds__(kNT) void k_block_update(Tables T, const float* acc, const uint32_t* start, float* e) {
-  const uint32_t c = blockIdx.x;
-  const uint32_t lo = c * kTile, hi = min((uint32_t)T.d, lo + kTile);
+// Out-of-place residual update for a block message: e = +0 on the runs, acc elsewhere.  One float4
+// group per thread (kRbTile elements per workgroup).
+__global__ __launch_bounds__(kRbNT) void k_block_update(Tables T, const float* acc, const uint32_t* start, float* e) {
+  const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)T.d, lo + kRbTile);
+  const uint32_t c = lo / kTile;  // the data tile holding this group: its first and last segment
   const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
+  const uint32_t i0 = lo + threadIdx.x * 4u;
+  const int nv = group_extent(i0, hi);
+  float v[4];
+  if (hi - lo == kRbTile) load4f(acc, i0, v);
+  else load4(acc, i0, nv, v);
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const uint32_t i0 = lo + (uint32_t)(r * kNT + threadIdx.x) * 4u;
-    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-    float v[4];
-    load4(acc, i0, nv, v);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if (q < nv) {
-        const uint32_t i = i0 + q;
-        const int l = sf == sl ? sf : seg_of(i, sf, sl, T.seg_off);
-        const uint32_t o = T.seg_off[l], n = T.seg_off[l + 1] - o;
-        const uint32_t s = start[l] % n, j = i - o;
-        const uint32_t t = j >= s ? j - s : j + n - s;
-        if (t < (uint32_t)T.seg_k[l]) v[q] = 0.0f;
-      }
+  for (int q = 0; q < 4; ++q) {
+    if (q < nv) {
+      const uint32_t i = i0 + q;
+      const int l = sf == sl ? sf : seg_of(i, sf, sl, T.seg_off);
+      const uint32_t o = T.seg_off[l], n = T.seg_off[l + 1] - o;
+      const uint32_t s = start[l] % n, j = i - o;
+      const uint32_t t = j >= s ? j - s : j + n - s;
+      if (t < (uint32_t)T.seg_k[l]) v[q] = 0.0f;
     }
-    store4(e, i0, nv, v);
   }
+  store4(e, i0, nv, v);
 }
 
 // ---------------------------------------------------------------------------------------------

@@ -680,7 +680,7 @@ int ef_accumulate(const ef_layout* L, const void* g, int g_dtype, const float* e
   EF_TRY(check_bound(L));
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !vec_ok(acc)) return EF_EINVAL;
-  const dim3 grid((unsigned)L->nchunks), blk(kNT);
+  const dim3 grid((unsigned)((L->d + kRbTile - 1) / kRbTile)), blk(kRbNT);
   if (g_dtype == EF_F32)
     EF_LAUNCH(k_accumulate<0>, grid, blk, 0, S(stream), L->T.d, g, e, acc);
   else
@@ -883,7 +883,7 @@ int ef_update(const ef_layout* L, const float* acc, int msg_kind, const uint32_t
   const unsigned kblocks = (unsigned)((L->K + kNT - 1) / kNT);
   if (msg_kind == EF_MSG_SPARSE) {
     if (e != acc) {
-      EF_LAUNCH(k_copy, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T.d, acc, e);
+      EF_LAUNCH(k_copy, dim3((unsigned)((L->d + kRbTile - 1) / kRbTile)), dim3(kRbNT), 0, st, L->T.d, acc, e);
       EF_TRY(launched());
     }
     EF_LAUNCH(k_sparse_zero, dim3(kblocks), dim3(kNT), 0, st, L->T.d, (int32_t)L->K, m, e);
@@ -893,7 +893,8 @@ int ef_update(const ef_layout* L, const float* acc, int msg_kind, const uint32_t
     if (e == acc)
       EF_LAUNCH(k_block_zero, dim3(kblocks), dim3(kNT), 0, st, L->T, (int32_t)L->K, m, e);
     else
-      EF_LAUNCH(k_block_update, dim3((unsigned)L->nchunks), dim3(kNT), 0, st, L->T, acc, m, e);
+      EF_LAUNCH(k_block_update, dim3((unsigned)((L->d + kRbTile - 1) / kRbTile)), dim3(kRbNT), 0, st, L->T, acc, m,
+                e);
     return launched();
   }
   return EF_EINVAL;
