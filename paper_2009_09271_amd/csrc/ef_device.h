@@ -7,26 +7,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-// Optional phase timestamps for profiling single-workgroup kernels (off unless the library is
-// built with EFS_PHASE_TIMING; then thread 0 of workgroup 0 records wall-clock ticks).
-#ifdef EFS_PHASE_TIMING
-__device__ unsigned long long g_efs_phase[64];
-#define EFS_PHASE(i)                                                          \
-  do {                                                                        \
-    if (blockIdx.x == 0 && threadIdx.x == 0) g_efs_phase[i] = wall_clock64(); \
-  } while (0)
-#else
-#define EFS_PHASE(i) \
-  do {               \
-  } while (0)
-#endif
-
 namespace efs {
 
-constexpr int kNT = 256;                      // threads per workgroup of the streaming kernels
+constexpr int kNT = 256;                      // threads per workgroup of most kernels
 constexpr int kSelNT = 1024;                  // threads per workgroup of the per-segment kernels
-constexpr uint32_t kTile = 4096;              // data elements per tile (4 float4 groups per thread)
-constexpr int kRounds = kTile / (4 * kNT);    // float4 groups per thread per chunk
+constexpr uint32_t kTile = 4096;              // data elements per tile (the rows of the selection kernels)
 constexpr int kHBins = 2048;                  // LDS histogram bins (11 bits per radix level)
 constexpr int kResWords = 16;                // per-segment selection record (uint32 words)
 constexpr int kSubLists = 16;                // a segment's list of undecided candidates is kept as 16

@@ -1,8 +1,8 @@
 // HIP kernels of the efsparse hot path (gfx950).
 //
-// Streaming kernels walk the gradient in tiles of kTile elements (kRounds coalesced float4
-// groups per thread of a kNT-thread workgroup).  The selection kernels work on rows: a row is the
-// part of one segment inside one tile, so that every workgroup of the selection pipeline serves
+// The plain streaming kernels give each thread one coalesced float4 group (64-thread workgroups,
+// kRbTile elements each).  The selection kernels work on rows: a row is the part of one segment
+// inside one data tile of kTile elements, so that every workgroup of the selection pipeline serves
 // exactly one segment.
 //
 // Top-k and random-k (Section 3) share one pipeline; no kernel synchronises across workgroups:
@@ -24,8 +24,11 @@
 //                    and scan the rows' winners in k_rowcount and k_rowscan.
 //   k_emit           per row: the winners in index order to the message, e = +0 there.
 // A segment with fewer than k_l candidates is resolved exactly over all of its elements by
-// k_select.  Block-random-k is one fused streaming pass (k_randblock_step).  The aggregate
-// (Algorithm 1) accumulates each output tile in LDS in worker order.
+// k_select.  Random-k's selection can also run without data, ahead of the step (the keys depend
+// only on seed, step and position); the step is then one streaming pass (k_randk_apply).
+// Block-random-k is one fused streaming pass (k_randblock_step).  The aggregates (Algorithm 1) sum
+// each output element over the workers in worker order: in registers for block messages, in an
+// LDS tile for sparse ones.
 #pragma once
 
 #include "ef_device.h"
@@ -308,8 +311,8 @@ __global__ __launch_bounds__(kRbNT) void k_block_update(Tables T, const float* a
 }
 
 // ---------------------------------------------------------------------------------------------
-// Aggregate (Algorithm 1): out = (sum over workers in order, from +0) / W.  One workgroup per
-// output tile of kTile elements accumulates in LDS; a barrier separates consecutive workers.
+// Aggregate (Algorithm 1): out = (sum over workers in order, from +0) / W, each output tile
+// written once.
 // ---------------------------------------------------------------------------------------------
 // Output tiles of the sparse aggregate: kAggTile elements, summed by one wavefront (kAggRounds
 // float4 groups per lane).

@@ -505,12 +505,6 @@ const char* ef_status_string(int status) {
   }
 }
 
-#ifdef EFS_PHASE_TIMING
-int ef_debug_phases(unsigned long long* out) {
-  return hipMemcpyFromSymbol(out, HIP_SYMBOL(g_efs_phase), sizeof(unsigned long long) * 64) == hipSuccess ? 0 : 4;
-}
-#endif
-
 int ef_last_hip_error(void) { return g_last_hip_error; }
 
 const char* ef_last_hip_error_string(void) {
