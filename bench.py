@@ -30,6 +30,11 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, 8 TB/s
 METRIC = "compressed gradient elements/s per compressor at 1 GPU; % of MI355X HBM BW"
 
 
+def _note(msg):
+    """A progress line on stderr (the JSON result goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def _gen(args):
     name, w, t = args
     from workloads import WORKLOADS, gradient
@@ -41,8 +46,17 @@ def gen_gradients(wl, W, t=0):
     n = max(1, min(8, os.cpu_count() or 1, W))
     if n == 1:
         return [_gen((wl.name, w, t)) for w in range(W)]
-    with mp.get_context("fork").Pool(n) as pool:
-        return pool.map(_gen, [(wl.name, w, t) for w in range(W)])
+    # close + join: the workers exit on their own (the pool's context manager would end them with
+    # SIGTERM, which a profiler's preloaded signal handler in the forked workers does not survive)
+    pool = mp.get_context("fork").Pool(n)
+    try:
+        out = pool.map(_gen, [(wl.name, w, t) for w in range(W)])
+        pool.close()
+    except BaseException:
+        pool.terminate()
+        raise
+    pool.join()
+    return out
 
 
 def variant_list(spec, blocks):
@@ -334,6 +348,7 @@ def main():
     offs = wl.seg_offsets(args.scope)
     d = offs[-1]
 
+    _note(f"generating {W} gradients of {d} elements")
     t_gen = time.perf_counter()
     grads = gen_gradients(wl, W)
     t_gen = time.perf_counter() - t_gen
@@ -561,6 +576,7 @@ def main():
         for st in [sA, astream] + sB:
             cur.wait_stream(st)
 
+    _note(f"warm-up ({args.warmup} steps), then {args.steps} timed steps")
     step_no = 0
     with torch.cuda.stream(sA):
         for _ in range(args.warmup):
@@ -583,6 +599,7 @@ def main():
 
     # ---- per-variant breakdown: each variant alone (batch schedule: its W steps and aggregate on
     # one stream; other schedules: their own schedule with one variant) -------------------------
+    _note("each variant alone")
     per = {}
     for v in variants:
         torch.cuda.synchronize()
@@ -642,6 +659,7 @@ def main():
     nonlocal_step = [step_no]
     kernels, kernels_serial, roofline = {}, {}, None
     if not args.no_kernel_timing:
+        _note("per-kernel timing")
         kernels = kernel_table(lambda t: run_step(t))
         kernels_serial = {vname(v): kernel_table(alone(v)) for v in variants}
         dom = next(iter(kernels))
@@ -664,14 +682,18 @@ def main():
     single = {}
     if not args.no_single:
         for scope in ("flat", "layer"):
+            _note(f"one worker's step and the aggregate alone, {scope} scope")
             single[scope] = measure_single(E, torch, dev, wl.seg_offsets(scope), density, variants, W, g,
                                            seeds)
 
     # ---- the paths next to the hot path, on the same workload (each alone, events on one stream) --
+    if not args.no_next:
+        _note("next rows")
     nxt = {} if args.no_next else measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, args)
 
     cpu = None
     if not args.no_cpu_baseline:
+        _note("CPU oracle sample")
         ks = [int(k) for k in lay0.segment_k()]
         cpu = cpu_baseline(wl, offs, ks, variants, W, grads, "")
 
