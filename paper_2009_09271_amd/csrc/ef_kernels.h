@@ -456,7 +456,7 @@ constexpr int kAggClaim = 256;      // sparse aggregate: claim slots (positions 
 // only wait for each other), which is worker order.  Entries past the first 64 are loaded
 // kAggChunk per lane at a time.
 struct AggLds {
-  float acc[kAggTile];
+  alignas(16) float acc[kAggTile];  // read and written as float4 groups
   uint32_t claim[kAggClaim];  // ~0 between adds
   uint32_t pre[65];           // entry prefix of each worker of the group
   uint32_t a[64];             // each worker's first entry in the tile
@@ -714,7 +714,7 @@ static_assert(kAggTile == 4u * kNT, "one float4 group per thread");
 template <int GDT>
 __global__ __launch_bounds__(kNT) void k_randk_apply(int32_t d, int32_t K, const uint32_t* ts, const uint32_t* idx,
                                                      const void* g, float* e, float* val) {
-  __shared__ int32_t slot[kAggTile];  // element of the tile -> its winner's message entry, or -1
+  __shared__ __align__(16) int32_t slot[kAggTile];  // element -> its winner's message entry, or -1
   const uint32_t t = blockIdx.x, lo = t * kAggTile, hi = min((uint32_t)d, lo + kAggTile);
   const uint32_t i0 = lo + threadIdx.x * 4u;
   const uint32_t ja = ts[t], jb = min(ts[t + 1], (uint32_t)K);
