@@ -7,7 +7,7 @@ import time
 import numpy as np
 import pytest
 
-from efs_gpu import Case, announce, dev
+from efs_gpu import Case, announce, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -123,3 +123,57 @@ def test_bad_workspaces_and_pointers_are_rejected_before_launch():
     torch.cuda.synchronize()
     # nothing was enqueued: the outputs still hold their fill values
     assert torch.all(out == 5.0) and torch.all(val == 3.0) and torch.all(idx == 7)
+
+
+@pytest.mark.parametrize("kind", ["topk", "randk"])
+def test_same_step_in_every_launch_configuration(kind):
+    """One worker's step gives the same bits alone (one row per wavefront), as the first worker of
+    batches of 3 and of 12 (the batch forms for 8 or more workers: four rows per wavefront, the
+    worker in the grid's second dimension), split into phases, and for random-k prepared ahead."""
+    import paper_2009_09271_amd as E
+    import torch
+    announce("launch configurations", kind)
+    c = Case([0, 5, 70000, 70004, 300000], 0.01)
+    rng = np.random.default_rng(3)
+    g = dev((rng.standard_normal(c.d) * 10.0 ** rng.integers(-3, 1, c.d)).astype(np.float32))
+    e0 = dev((rng.standard_normal(c.d) * 1e-3).astype(np.float32))
+    op = E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK
+    seed = 41
+
+    def single(phased):
+        e = e0.clone()
+        idx = torch.empty(c.K, dtype=torch.int32, device="cuda")
+        val = torch.empty(c.K, dtype=torch.float32, device="cuda")
+        ws = c.ws(op)
+        phases = [E.EF_PHASE_PREPARE, E.EF_PHASE_STREAM, E.EF_PHASE_FINISH] if phased else [E.EF_PHASE_ALL]
+        for p in phases:
+            if kind == "topk":
+                E.ef_step_topk_phases(c.L, p, g, e, idx, val, ws)
+            else:
+                E.ef_step_randk_phases(c.L, p, g, e, seed, 0, idx, val, ws)
+        return idx, val, e
+
+    def batch(W):
+        es = [e0.clone() for _ in range(W)]
+        idx = torch.empty((W, c.K), dtype=torch.int32, device="cuda")
+        val = torch.empty((W, c.K), dtype=torch.float32, device="cuda")
+        ws, stride = E.batch_workspace(c.L, op, W)
+        if kind == "topk":
+            E.ef_step_topk_batch(c.L, [g] * W, es, idx, val, ws, stride)
+        else:
+            E.ef_step_randk_batch(c.L, [g] * W, es, [seed] * W, 0, idx, val, ws, stride)
+        return idx[0], val[0], es[0]
+
+    runs = {"alone": single(False), "phases": single(True), "batch of 3": batch(3), "batch of 12": batch(12)}
+    if kind == "randk":
+        e = e0.clone()
+        idx = torch.empty(c.K, dtype=torch.int32, device="cuda")
+        val = torch.empty(c.K, dtype=torch.float32, device="cuda")
+        ws = c.ws(E.EF_OP_RANDK_PREP)
+        E.ef_randk_prepare(c.L, seed, 0, idx, ws)
+        E.ef_step_randk_prepared(c.L, g, e, idx, val, ws)
+        runs["prepared"] = (idx, val, e)
+    ref = [host(t).view(np.uint32) for t in runs["alone"]]
+    for name, r in runs.items():
+        for got, want, what in zip(r, ref, ("indices", "values", "residual")):
+            assert np.array_equal(host(got).view(np.uint32), want), f"{kind} {name}: {what} differ"
