@@ -1204,6 +1204,27 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
 #pragma unroll
   for (int r = 0; r < kSR; ++r) vm[r] = group_mask(tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u, lo, hi);
   const bool whole = lo == tb && hi == tb + kTile;  // the row is the whole tile (uniform)
+  // random-k: the Philox keys of the thread's elements depend on positions only; they are computed
+  // while the thread's loads are in flight (called right after the loads are issued)
+  uint32_t uk[KIND == 1 ? kSR : 1][4];
+  auto random_keys = [&]() {
+    if constexpr (KIND == 1) {
+#pragma unroll
+      for (int r = 0; r < kSR; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
+        if ((o & 3u) == 0) {  // the float4 group is one Philox block
+          uint4 x = make_uint4(0u, 0u, 0u, 0u);
+          if (vm[r]) x = philox(make_uint4((i0 - o) >> 2, 0u, step, kRandkTag | (uint32_t)l), s0, s1);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) uk[r][q] = word(x, q);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            uk[r][q] = ((vm[r] >> q) & 1u) ? randk_key(i0 + q - o, (uint32_t)l, step, s0, s1) : 0u;
+        }
+      }
+    }
+  };
   if constexpr (FUSED) {
     float gv[kSR][4];
     if (whole) {
@@ -1221,6 +1242,7 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
         load4m(src, i0, vm[r], v[r]);
       }
     }
+    random_keys();
 #pragma unroll
     for (int r = 0; r < kSR; ++r) {
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
@@ -1235,6 +1257,7 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     for (int r = 0; r < kSR; ++r)
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[r][q] = 0.0f;
+    random_keys();
   } else {
 #pragma unroll
     for (int r = 0; r < kSR; ++r) {
@@ -1242,6 +1265,7 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       if (whole) load4f(src, i0, v[r]);
       else load4m(src, i0, vm[r], v[r]);
     }
+    random_keys();
   }
   // candidate flags; wave-level prefixes through ballots, one barrier for the whole row
   uint32_t mask[kSR], lpre[kSR];
@@ -1259,29 +1283,14 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
         if (((vm[r] >> q) & 1u) && (kk[r][q] > A || (kk[r][q] == A && i0 + q < IA))) mk |= 1u << q;
       }
     } else {
-      if ((o & 3u) == 0) {  // the float4 group is one Philox block
-        uint4 x = make_uint4(0u, 0u, 0u, 0u);
-        if (vm[r]) x = philox(make_uint4((i0 - o) >> 2, 0u, step, kRandkTag | (uint32_t)l), s0, s1);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if (((vm[r] >> q) & 1u) && (uint64_t)word(x, q) < tau) {
-            mk |= 1u << q;
-            s_kk[(r * kStrNT + threadIdx.x) * 4 + q] = ~word(x, q);
-          }
-          if (((vm[r] >> q) & 1u) && word(x, q) < ulo) cbits |= 1u << (4 * r + q);
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t u = uk[r][q];
+        if (((vm[r] >> q) & 1u) && (uint64_t)u < tau) {
+          mk |= 1u << q;
+          s_kk[(r * kStrNT + threadIdx.x) * 4 + q] = ~u;
         }
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          if ((vm[r] >> q) & 1u) {
-            const uint32_t u = randk_key(i0 + q - o, (uint32_t)l, step, s0, s1);
-            if ((uint64_t)u < tau) {
-              mk |= 1u << q;
-              s_kk[(r * kStrNT + threadIdx.x) * 4 + q] = ~u;
-            }
-            if (u < ulo) cbits |= 1u << (4 * r + q);
-          }
-        }
+        if (((vm[r] >> q) & 1u) && u < ulo) cbits |= 1u << (4 * r + q);
       }
     }
     mask[r] = mk;
