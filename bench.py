@@ -169,11 +169,12 @@ def measure_prepared(E, torch, dev, timed, entry, lay, g, e, seeds, mv, step_b, 
     return res
 
 
-def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20):
+def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20, g_bf16=None):
     """Each compressor at the given scope: one worker's step alone (the fused entry point, and the
     composed calls accumulate + compress + update), and the aggregate of the W workers' messages
     alone; back-to-back repetitions on one stream, timed with events on that stream.  Also the
-    library's plain copy kernel over d floats, as a measured streaming ceiling."""
+    library's plain copy kernel over d floats, as a measured streaming ceiling.  With g_bf16 (a
+    bf16 copy of worker 0's gradient), the fused steps on it too."""
     d = offs[-1]
     st = torch.cuda.Stream(dev)
 
@@ -227,6 +228,18 @@ def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20)
 
         step_b, agg_b = alg_bytes_op(kind, d, K, L, W)
         r = {"fused_step": entry(timed(fused), step_b, d)}
+        if g_bf16 is not None:  # the same step on a bf16 gradient: 2 bytes fewer per element
+            gb = g_bf16
+
+            def fused_bf16():
+                if kind == "topk":
+                    E.ef_step_topk(lay, gb, e, mi[0], mv[0], ws)
+                elif kind == "randk":
+                    E.ef_step_randk(lay, gb, e, seeds[0], 0, mi[0], mv[0], ws)
+                else:
+                    E.ef_step_randblock(lay, gb, e, seeds[0], 0, mi[0], mv[0])
+
+            r["fused_step_bf16_gradient"] = entry(timed(fused_bf16), step_b - 2 * d, d)
         # the step's kernels (library events per launch, a separate pass)
         E.timing_collect(reset=True)
         E.timing_enable(True)
@@ -681,10 +694,12 @@ def main():
     # ---- each compressor alone, one worker's step and one aggregate, at both scopes ---------------
     single = {}
     if not args.no_single:
+        g_bf16 = g[0].to(torch.bfloat16)
         for scope in ("flat", "layer"):
             _note(f"one worker's step and the aggregate alone, {scope} scope")
             single[scope] = measure_single(E, torch, dev, wl.seg_offsets(scope), density, variants, W, g,
-                                           seeds)
+                                           seeds, g_bf16=g_bf16 if scope == "flat" else None)
+        del g_bf16
 
     # ---- the paths next to the hot path, on the same workload (each alone, events on one stream) --
     if not args.no_next:
