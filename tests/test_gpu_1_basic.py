@@ -208,3 +208,32 @@ def test_aggregate_sparse_concentrated(W):
     assert c.K == K
     for average in (True, False):
         _agg_check(c, "sparse", msgs, W, average)
+
+
+@pytest.mark.parametrize("offs", LAYOUTS, ids=lambda o: f"d{o[-1]}_L{len(o) - 1}")
+@pytest.mark.parametrize("aligned16", [True, False], ids=["g16", "g8"])
+def test_randblock_bf16_gradient(offs, aligned16):
+    """The fused block-random-k step on a bf16 gradient, 16-byte aligned and only 8-byte aligned
+    (the entry point's requirement for bf16)."""
+    import paper_2009_09271_amd as E
+    import torch
+    from workloads import to_bf16_bits
+    announce("randblock bf16", offs[-1], len(offs) - 1, aligned16)
+    c = Case(offs, 0.05, 256)
+    g, e = _inputs(c.d, 4)
+    gb = to_bf16_bits(g)
+    off = 0 if aligned16 else 4  # 4 bf16 values = 8 bytes past a 256-byte aligned allocation
+    buf = np.zeros(c.d + 8, np.uint16)
+    buf[off:off + c.d] = gb
+    gd = dev(buf)[off:off + c.d].view(torch.bfloat16)
+    assert (gd.data_ptr() % 16 == 0) == aligned16
+    seed = (9 << 32) | 2
+    for step in range(2):
+        ed = dev(e)
+        start = torch.empty(len(c.ks), dtype=torch.int32, device="cuda")
+        val = torch.empty(c.K, dtype=torch.float32, device="cuda")
+        E.ef_step_randblock(c.L, gd, ed, seed, step, start, val)
+        (wst, wval), we = c.oracle_step("randblock", gb, e, seed, step)
+        assert_msg_equal("randblock", (start, val), (wst, wval), f"bf16 step {step}")
+        assert_f32_equal(ed, we, f"bf16 e' step {step}")
+        e = we
