@@ -205,53 +205,120 @@ __device__ __forceinline__ uint32_t run_pos(const RunSeg& r, uint32_t i) {
 }
 
 // Fused worker step: acc = g + e; val[P_l + t] = acc on the run; e' = +0 on the run, acc elsewhere.
-// One float4 group per thread (kRbTile elements per workgroup).
+// One float4 group per thread for a float32 gradient (kRbTile elements per workgroup); two groups
+// (kRbNT groups apart, each coalesced over the wavefront) for bf16, whose groups are 8-byte loads.
+template <int GDT>
+constexpr uint32_t rb_groups() { return GDT == 1 ? 2u : 1u; }
+template <int GDT>
+constexpr uint32_t rb_tile() { return kRbTile * rb_groups<GDT>(); }
+
 template <int GDT>
 __global__ __launch_bounds__(kRbNT) void k_randblock_step(Tables T, const void* g, float* e, uint32_t s0,
                                                         uint32_t s1, uint32_t step, uint32_t* start,
                                                         float* val) {
-  const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)T.d, lo + kRbTile);
-  const uint32_t c = lo / kTile;  // the data tile holding this group: its first and last segment
-  const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
-  const uint32_t i0 = lo + threadIdx.x * 4u;
-  const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
-  float gv[4], ev[4];
-  if (hi - lo == kRbTile) {  // whole group (every workgroup but the last)
-    load4gf<GDT>(g, i0, gv);
-    load4f(e, i0, ev);
-  } else {
-    load4g<GDT>(g, i0, nv, gv);
-    load4(e, i0, nv, ev);
-  }
-  RunSeg rs = run_seg(T, sf, step, s0, s1);
-  int cur = sf;
-  float out[4];
+  if constexpr (GDT == 0) {
+    const uint32_t lo = blockIdx.x * kRbTile, hi = min((uint32_t)T.d, lo + kRbTile);
+    const uint32_t c = lo / kTile;  // the data tile holding this group: its first and last segment
+    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
+    const uint32_t i0 = lo + threadIdx.x * 4u;
+    const int nv = i0 < hi ? (int)min(4u, hi - i0) : 0;
+    float gv[4], ev[4];
+    if (hi - lo == kRbTile) {  // whole group (every workgroup but the last)
+      load4gf<GDT>(g, i0, gv);
+      load4f(e, i0, ev);
+    } else {
+      load4g<GDT>(g, i0, nv, gv);
+      load4(e, i0, nv, ev);
+    }
+    RunSeg rs = run_seg(T, sf, step, s0, s1);
+    int cur = sf;
+    float out[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float a = gv[q] + ev[q];
-    out[q] = a;
-    if (q < nv) {
-      const uint32_t i = i0 + q;
-      if (sf != sl) {
-        const int l = seg_of(i, sf, sl, T.seg_off);
-        if (l != cur) {
-          rs = run_seg(T, l, step, s0, s1);
-          cur = l;
+    for (int q = 0; q < 4; ++q) {
+      const float a = gv[q] + ev[q];
+      out[q] = a;
+      if (q < nv) {
+        const uint32_t i = i0 + q;
+        if (sf != sl) {
+          const int l = seg_of(i, sf, sl, T.seg_off);
+          if (l != cur) {
+            rs = run_seg(T, l, step, s0, s1);
+            cur = l;
+          }
+        }
+        const uint32_t t = run_pos(rs, i);
+        if (t < rs.k) {
+          val[rs.P + t] = a;
+          out[q] = 0.0f;
         }
       }
-      const uint32_t t = run_pos(rs, i);
-      if (t < rs.k) {
-        val[rs.P + t] = a;
-        out[q] = 0.0f;
+    }
+    store4(e, i0, nv, out);
+    // start of every segment that begins in this group
+    for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
+      const uint32_t ol = (uint32_t)T.seg_off[l];
+      if (ol >= lo && ol < hi)
+        start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
+    }
+  } else {
+    constexpr uint32_t NG = rb_groups<GDT>(), TILE = rb_tile<GDT>();
+    const uint32_t lo = blockIdx.x * TILE, hi = min((uint32_t)T.d, lo + TILE);
+    const uint32_t c = lo / kTile;  // the data tile holding these groups: its first and last segment
+    const int sf = T.chunk_sf[c], sl = T.chunk_sl[c];
+    uint32_t i0[NG];
+    int nv[NG];
+#pragma unroll
+    for (uint32_t r = 0; r < NG; ++r) {
+      i0[r] = lo + (r * kRbNT + threadIdx.x) * 4u;
+      nv[r] = i0[r] < hi ? (int)min(4u, hi - i0[r]) : 0;
+    }
+    float gv[NG][4], ev[NG][4];
+    if (hi - lo == TILE) {  // whole tile (every workgroup but the last)
+#pragma unroll
+      for (uint32_t r = 0; r < NG; ++r) {
+        load4gf<GDT>(g, i0[r], gv[r]);
+        load4f(e, i0[r], ev[r]);
+      }
+    } else {
+#pragma unroll
+      for (uint32_t r = 0; r < NG; ++r) {
+        load4g<GDT>(g, i0[r], nv[r], gv[r]);
+        load4(e, i0[r], nv[r], ev[r]);
       }
     }
-  }
-  store4(e, i0, nv, out);
-  // start of every segment that begins in this group
-  for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
-    const uint32_t ol = (uint32_t)T.seg_off[l];
-    if (ol >= lo && ol < hi)
-      start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
+    RunSeg rs = run_seg(T, sf, step, s0, s1);
+    int cur = sf;
+#pragma unroll
+    for (uint32_t r = 0; r < NG; ++r) {
+      float out[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float a = gv[r][q] + ev[r][q];
+        out[q] = a;
+        if (q < nv[r]) {
+          const uint32_t i = i0[r] + q;
+          if (sf != sl) {
+            const int l = seg_of(i, sf, sl, T.seg_off);
+            if (l != cur) {
+              rs = run_seg(T, l, step, s0, s1);
+              cur = l;
+            }
+          }
+          const uint32_t t = run_pos(rs, i);
+          if (t < rs.k) {
+            val[rs.P + t] = a;
+            out[q] = 0.0f;
+          }
+        }
+      }
+      store4(e, i0[r], nv[r], out);
+    }
+    // start of every segment that begins in this workgroup's elements
+    for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
+      const uint32_t ol = (uint32_t)T.seg_off[l];
+      if (ol >= lo && ol < hi)
+        start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
+    }
   }
 }
 

@@ -861,12 +861,14 @@ int ef_step_randblock(const ef_layout* L, const void* g, int g_dtype, float* e, 
   EF_TRY(check_bound(L));
   EF_TRY(check_g(g, g_dtype));
   if (!vec_ok(e) || !word_ok(start) || !word_ok(val)) return EF_EINVAL;
-  const dim3 grid((unsigned)((L->d + kRbTile - 1) / kRbTile)), blk(kRbNT);
+  const dim3 blk(kRbNT);
   const uint32_t s0 = (uint32_t)seed, s1 = (uint32_t)(seed >> 32);
   if (g_dtype == EF_F32)
-    EF_LAUNCH(k_randblock_step<0>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
+    EF_LAUNCH(k_randblock_step<0>, dim3((unsigned)((L->d + rb_tile<0>() - 1) / rb_tile<0>())), blk, 0, S(stream),
+              L->T, g, e, s0, s1, step, start, val);
   else
-    EF_LAUNCH(k_randblock_step<1>, grid, blk, 0, S(stream), L->T, g, e, s0, s1, step, start, val);
+    EF_LAUNCH(k_randblock_step<1>, dim3((unsigned)((L->d + rb_tile<1>() - 1) / rb_tile<1>())), blk, 0, S(stream),
+              L->T, g, e, s0, s1, step, start, val);
   return launched();
 }
 
