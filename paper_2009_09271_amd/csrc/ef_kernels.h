@@ -1473,16 +1473,24 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   __shared__ uint32_t lds[2 * kSelNT / 64];
   const int l = blockIdx.x;
   uint32_t* R = res_of(ws, l);
-  if (R[R_MODE] != 0) return;
+  // the segment's mode and every copy of its histogram in one round trip (a segment of mode 1 has
+  // no histogram: its loads read the unused copies and are dropped)
+  constexpr int kPer = kHBins / kSelNT;
+  static_assert(kHBins % kSelNT == 0, "whole bins per thread");
+  const uint32_t mode = R[R_MODE];
   const uint32_t* gh = ws.hist + (size_t)l * kHCopies * kHBins;
-  for (int b = threadIdx.x; b < kHBins; b += kSelNT) {
-    uint32_t c[kHCopies];
+  uint32_t c[kPer][kHCopies];
 #pragma unroll
-    for (int x = 0; x < kHCopies; ++x) c[x] = gh[x * kHBins + b];
+  for (int u = 0; u < kPer; ++u)
+#pragma unroll
+    for (int x = 0; x < kHCopies; ++x) c[u][x] = gh[x * kHBins + u * kSelNT + threadIdx.x];
+  if (mode != 0) return;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
     uint32_t sum = 0;
 #pragma unroll
-    for (int x = 0; x < kHCopies; ++x) sum += c[x];
-    hist[b] = sum;
+    for (int x = 0; x < kHCopies; ++x) sum += c[u][x];
+    hist[u * kSelNT + threadIdx.x] = sum;
   }
   __syncthreads();
   const uint32_t kl = (uint32_t)T.seg_k[l];
