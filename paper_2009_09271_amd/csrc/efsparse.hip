@@ -418,8 +418,10 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     const Batch bt = batch_of(c0, (int)nw);
     const dim3 rgrid((unsigned)L->nrows, nw), sgrid((unsigned)L->L, nw);
     // rows per wavefront of the collection and of the emission: top-k rows hold hundreds of
-    // candidates, so one row per wavefront for one or a few workers (the most parallel form) and
-    // four for a batch (fewer, fuller wavefronts); random-k rows hold a few, 16 per wavefront
+    // candidates, so one row per wavefront for one or a few workers (the most parallel form) and,
+    // for a batch, two (collection) or four (emission) for fewer, fuller wavefronts (measured on
+    // 16 workers: collection 23.7 us with two, 25.8 with four; emission the same with two or
+    // four); random-k rows hold a few, 16 per wavefront
     const bool wide = nw >= kWideBatch;
     const uint32_t emit_rw = KIND == 1 ? 16u : wide ? 4u : 1u;
     const uint32_t emit_rows = (kNT / 64) * emit_rw;
@@ -431,9 +433,9 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
         EF_LAUNCH(k_resolve, sgrid, sblk, 0, st, T, w, bt);
         EF_TRY(launched());
       }
-      const uint32_t crows = (kNT / 64) * (wide ? 4u : 1u);  // rows per workgroup
+      const uint32_t crows = (kNT / 64) * (wide ? 2u : 1u);  // rows per workgroup
       const dim3 cgrid((unsigned)((L->nrows + crows - 1) / crows), nw);
-      if (wide) EF_LAUNCH((k_collect<KIND, 4>), cgrid, blk, 0, st, T, w, bt);
+      if (wide) EF_LAUNCH((k_collect<KIND, 2>), cgrid, blk, 0, st, T, w, bt);
       else EF_LAUNCH((k_collect<KIND, 1>), cgrid, blk, 0, st, T, w, bt);
       EF_TRY(launched());
     }
