@@ -1,8 +1,8 @@
 """GPU parity on seeded random configurations: random segment layouts (1 to 40 segments, sizes
 from 1 element up), densities, block sizes, worker counts and gradient dtypes.  For each, the
 fused steps of every compressor over two steps (residual carried), the batched steps, random-k
-prepared ahead, and the sparse and block aggregates of the workers' messages, bit for bit against
-the CPU oracle."""
+prepared ahead, and the sparse and block aggregates of the workers' messages (plain, fused with a
+parameter update, and with shared coordinates), bit for bit against the CPU oracle."""
 
 import numpy as np
 import pytest
@@ -80,6 +80,28 @@ def test_random_configuration(i):
             E.decompress_aggregate(c.L, E.EF_MSG_SPARSE, W, mi, mv, out, c.ws(E.EF_OP_AGG_SPARSE, W))
             want = O.decompress_aggregate_sparse(c.d, [m for m, _ in msgs], [v for _, v in msgs])
         assert_f32_equal(out, want, f"cfg {i} {kind} aggregate W={W}")
+        kindm = E.EF_MSG_BLOCK if kind == "randblock" else E.EF_MSG_SPARSE
+        ws_a = None if kind == "randblock" else c.ws(E.EF_OP_AGG_SPARSE, W)
+        # the same aggregate fused with an update of random parameters (momentum, weight decay)
+        beta, wd = float(rng.choice([0.0, 0.9])), float(rng.choice([0.0, 1e-4]))
+        use_m = beta != 0.0 or bool(rng.random() < 0.5)
+        x0 = rng.standard_normal(c.d).astype(np.float32)
+        m0 = (rng.standard_normal(c.d) * 0.1).astype(np.float32)
+        xd, md = dev(x0), dev(m0)
+        E.decompress_aggregate_apply(c.L, kindm, W, mi, mv, xd, md if use_m else None, beta, wd, None, ws_a)
+        wx, wmom = O.apply_update(x0, want, m0 if use_m else None, beta, wd)
+        assert_f32_equal(xd, wx, f"cfg {i} {kind} apply x")
+        if use_m:
+            assert_f32_equal(md, wmom, f"cfg {i} {kind} apply momentum")
+        # shared coordinates: worker 0's indices (or starts) for every worker's values
+        wss = c.ws(E.EF_OP_AGG_SHARED, W)
+        E.decompress_aggregate_shared(c.L, kindm, W, mi[0], mv, out, wss)
+        vals = [v for _, v in msgs]
+        if kind == "randblock":
+            want_s = O.decompress_aggregate_shared_block(c.d, c.offs, c.ks, msgs[0][0], vals)
+        else:
+            want_s = O.decompress_aggregate_shared_sparse(c.d, msgs[0][0], vals)
+        assert_f32_equal(out, want_s, f"cfg {i} {kind} shared aggregate")
         if kind == "randblock":
             continue
         # the same two steps batched, from zero residuals, against the per-worker results above
