@@ -16,7 +16,7 @@ What the paper fixes (Algorithm 1 and Section 3):
 * the worker keeps what it did not send as its new residual (Section 3, the
   worker steps; Algorithm 1's residual update).
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent or leaves a choice open:
 
 * k per segment: k = clamp(floor(rho * d_l + 0.5), 1, d_l) in IEEE double.
 * top-k orders by magnitude; ties go to the lower index.  The magnitude key is
