@@ -917,43 +917,6 @@ __device__ __forceinline__ void for_keys(const K& keys, uint32_t n, F fn) {
   }
 }
 
-// Radix selection of the need-th largest of n keys: returns T and r such that the winners are
-// the keys > T plus the first r keys == T.  kand / kor are the AND and OR of all keys; the levels
-// (11 bits each) start at the highest bit in which the keys differ, so concentrated keys still
-// spread over the histogram.
-template <typename K>
-__device__ __forceinline__ void block_select(const K& keys, uint32_t n, uint32_t need, uint32_t kand, uint32_t kor,
-                             uint32_t* hist, uint32_t* lds, uint32_t& T_out, uint32_t& r_out) {
-  const uint32_t diff = kand ^ kor;
-  if (diff == 0) {  // all keys equal
-    T_out = kand;
-    r_out = need;
-    return;
-  }
-  const int h = 31 - __clz(diff);
-  uint32_t prefix = h == 31 ? 0u : (kand & (0xFFFFFFFFu << (h + 1)));
-  int known = 31 - h;
-  while (known < 32) {
-    const int w = min(11, 32 - known);
-    const int shift = 32 - known - w;
-    for (int b = threadIdx.x; b < (1 << w); b += kSelNT) hist[b] = 0;
-    __syncthreads();
-    const uint32_t pmask = known == 0 ? 0u : (0xFFFFFFFFu << (32 - known));
-    const uint32_t want = prefix & pmask;
-    for_keys(keys, n, [&](uint32_t, uint32_t k) {
-      if ((k & pmask) == want) atomicAdd(&hist[(k >> shift) & ((1u << w) - 1u)], 1u);
-    });
-    __syncthreads();
-    uint32_t above;
-    const int bin = block_resolve<kSelNT>(hist, 1 << w, need, lds, above);
-    prefix |= (uint32_t)max(bin, 0) << shift;
-    need -= above;
-    known += w;
-  }
-  T_out = prefix;
-  r_out = need;
-}
-
 // Exact selection over the whole segment (used when the candidates cannot contain the answer):
 // radix levels over the keys of all d_l elements, then an index-ordered emission.
 template <int KIND>
@@ -1064,8 +1027,8 @@ __device__ __forceinline__ uint32_t block_nth_equal(const uint32_t* keys, uint32
 
 // The r-th smallest idx[j] (r >= 1, indices distinct) among the j < m with keys[j] == x: radix
 // levels over ~idx, whose largest values are the smallest indices.
-template <typename K>
-__device__ __forceinline__ uint32_t block_nth_smallest_tie(const K& keys, const K& idx, uint32_t m, uint32_t x,
+template <typename K, typename I>
+__device__ __forceinline__ uint32_t block_nth_smallest_tie(const K& keys, const I& idx, uint32_t m, uint32_t x,
                                            uint32_t r, uint32_t* hist, uint32_t* lds) {
   uint32_t prefix = 0, need = r;
   int known = 0;
@@ -1107,6 +1070,16 @@ __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t 
 // kSampleRun contiguous elements evenly spread over it.  The runs of a sampled segment also clear
 // its candidate histogram (kHCopies * kHBins = kSampleMax words, one slice per run).
 static_assert(kHCopies * kHBins == kSampleMax, "one histogram slice per sample run");
+static_assert(2 * kRankList <= kHBins, "the ranked entries of an exact segment fit a histogram array");
+
+// Positions 0, 1, ... as the indices of keys held in position order.
+struct LocalPos {
+  __device__ uint32_t operator[](uint32_t f) const { return f; }
+};
+template <typename K, typename I>
+__device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
+                                                  uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
+                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out);
 template <int GDT, bool FUSED>
 __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
@@ -1165,9 +1138,11 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
       kor |= k;
     });
     block_and_or(kand, kor, lds);  // its barriers also publish keys[]
-    uint32_t Tk, r;
-    block_select(keys, n, (uint32_t)T.seg_k[l], kand, kor, hist, lds, Tk, r);
-    const uint32_t it = o + block_nth_equal(keys, n, Tk, r, lds) + 1u;
+    // the k_l best of the segment's keys (positions as indices): hist2 holds the ranked entries
+    uint32_t Tk, IT;
+    list_threshold_ao(keys, LocalPos{}, n, (uint32_t)T.seg_k[l], kand, kor, hist, lds, hist2, hist2 + kRankList,
+                      Tk, IT);
+    const uint32_t it = IT == 0xFFFFFFFFu ? IT : o + IT;  // every tie wins, or one past the last
     if (threadIdx.x == 0) {
       R[R_A] = Tk;
       R[R_IA] = it;
@@ -1625,10 +1600,11 @@ __device__ __forceinline__ void rank_select(const uint32_t* sk, const uint32_t* 
 // m): the key' T of the last winner and one past its index (every listed winner is key' > T, or
 // key' == T with index below that bound).  Radix levels of 11 bits narrow the key' range until
 // the bin holding the need-th best has at most kRankList entries; those are gathered and ranked.
-template <typename K>
-__device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint32_t m, uint32_t need,
-                                               uint32_t* hist, uint32_t* lds, uint32_t* gk, uint32_t* gi,
-                                               uint32_t& T_out, uint32_t& IT_out) {
+// kand / kor: the AND and the OR of the m keys (needed when m > kRankList).
+template <typename K, typename I>
+__device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
+                                                  uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
+                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out) {
   __shared__ uint32_t s_n;
   if (m <= kRankList) {
     for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
@@ -1639,12 +1615,6 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
     rank_select(gk, gi, m, need, T_out, IT_out);
     return;
   }
-  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
-  for_keys(key, m, [&](uint32_t, uint32_t k) {
-    kand &= k;
-    kor |= k;
-  });
-  block_and_or(kand, kor, lds);
   const uint32_t diff = kand ^ kor;
   uint32_t prefix = kand, known = 32;  // all keys equal: nothing to resolve
   uint32_t cnt = m;
@@ -1691,6 +1661,21 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
   // more than kRankList entries share the full key': ties ordered by index
   T_out = prefix;
   IT_out = need >= cnt ? 0xFFFFFFFFu : block_nth_smallest_tie(key, idx, m, prefix, need, hist, lds) + 1u;
+}
+
+template <typename K>
+__device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint32_t m, uint32_t need,
+                                               uint32_t* hist, uint32_t* lds, uint32_t* gk, uint32_t* gi,
+                                               uint32_t& T_out, uint32_t& IT_out) {
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+  if (m > kRankList) {
+    for_keys(key, m, [&](uint32_t, uint32_t k) {
+      kand &= k;
+      kor |= k;
+    });
+    block_and_or(kand, kor, lds);
+  }
+  list_threshold_ao(key, idx, m, need, kand, kor, hist, lds, gk, gi, T_out, IT_out);
 }
 
 // Per segment: the exact threshold among the listed candidates, then every row's message offset;
