@@ -54,6 +54,7 @@ struct Tables {
   const int32_t* chunk_sf;     // [nchunks] first / last segment of each data tile
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row
+  const int32_t* run_seg;      // [nruns] top-k: segment of each sample run
   const uint32_t* btile;       // [2 nbtiles] block aggregate, multi-segment layouts: (1024-element
                                // data tile, segment) for every pair with an element in common
   int32_t d, L, nchunks, nrows, nruns, nbtiles;

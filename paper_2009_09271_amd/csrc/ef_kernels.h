@@ -1086,7 +1086,8 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
   const void* g = BT.g[blockIdx.y];
   const float* src = BT.src[blockIdx.y];
   const uint32_t r = blockIdx.x;
-  const int l = seg_of(r, 0, T.L - 1, T.seg_ro);
+  // a table lookup: one round trip instead of a binary search's chain (none for one segment)
+  const int l = T.L == 1 ? 0 : T.run_seg[r];
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
   const uint32_t q = r - (uint32_t)T.seg_ro[l];
   uint32_t i;

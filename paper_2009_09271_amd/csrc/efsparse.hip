@@ -53,7 +53,7 @@ struct ef_layout {
   std::vector<int64_t> off64;
   double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0;
 
-  std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg;
+  std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg, runseg;
   std::vector<uint32_t> btile;  // block aggregate, multi-segment: (data tile, segment) pairs
   std::vector<uint64_t> tau;
   std::vector<uint32_t> ulo;
@@ -64,7 +64,8 @@ struct ef_layout {
   bool rk_direct = false;  // random-k: every segment's rows and expected window fit k_select's LDS
 
   Blob blob;
-  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_btile;
+  size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_runseg,
+      o_btile;
   Tables T{};
   bool bound = false;
 
@@ -144,6 +145,9 @@ void ef_layout::build() {
   rseg.resize(nrows);
   for (int l = 0; l < n; ++l)
     for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) rseg[r] = l;
+  runseg.resize(nruns);
+  for (int l = 0; l < n; ++l)
+    for (int32_t r = ro[l]; r < ro[l + 1]; ++r) runseg[r] = l;
   nchunks = (int32_t)((d + kTile - 1) / kTile);
   csf.assign(nchunks, 0);
   csl.assign(nchunks, 0);
@@ -185,6 +189,7 @@ void ef_layout::build() {
   o_csf = blob.add(csf);
   o_csl = blob.add(csl);
   o_rseg = blob.add(rseg);
+  o_runseg = blob.add(runseg);
   o_btile = blob.add(btile);
   bound = false;
 }
@@ -630,6 +635,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_cbase = reinterpret_cast<const int32_t*>(b + L->o_cbase);
   T.seg_ro = reinterpret_cast<const int32_t*>(b + L->o_ro);
   T.row_seg = reinterpret_cast<const int32_t*>(b + L->o_rseg);
+  T.run_seg = reinterpret_cast<const int32_t*>(b + L->o_runseg);
   T.seg_tau = reinterpret_cast<const uint64_t*>(b + L->o_tau);
   T.seg_ulo = reinterpret_cast<const uint32_t*>(b + L->o_ulo);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
