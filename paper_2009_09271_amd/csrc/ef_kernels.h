@@ -900,17 +900,17 @@ __device__ __forceinline__ void block_and_or(uint32_t& a, uint32_t& o, uint32_t*
 }
 
 // Calls fn(f, keys[f]) for every f < n, in a strided order with kBatch loads in flight.
-template <typename K, typename F>
+template <int B = kBatch, typename K, typename F>
 __device__ __forceinline__ void for_keys(const K& keys, uint32_t n, F fn) {
-  for (uint32_t base = 0; base < n; base += (uint32_t)kSelNT * kBatch) {
-    uint32_t k[kBatch];
+  for (uint32_t base = 0; base < n; base += (uint32_t)kSelNT * B) {
+    uint32_t k[B];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
+    for (int u = 0; u < B; ++u) {
       const uint32_t f = base + (uint32_t)u * kSelNT + threadIdx.x;
       k[u] = f < n ? keys[f] : 0u;
     }
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
+    for (int u = 0; u < B; ++u) {
       const uint32_t f = base + (uint32_t)u * kSelNT + threadIdx.x;
       if (f < n) fn(f, k[u]);
     }
@@ -1070,6 +1070,7 @@ __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t 
 // kSampleRun contiguous elements evenly spread over it.  The runs of a sampled segment also clear
 // its candidate histogram (kHCopies * kHBins = kSampleMax words, one slice per run).
 static_assert(kHCopies * kHBins == kSampleMax, "one histogram slice per sample run");
+constexpr int kSampleKeysPer = kSampleMax / kSelNT;  // sample keys per thread, loaded in one round trip
 static_assert(2 * kRankList <= kHBins, "the ranked entries of an exact segment fit a histogram array");
 
 // Positions 0, 1, ... as the indices of keys held in position order.
@@ -1133,7 +1134,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   uint32_t* R = res_of(ws, l);
   if (n <= (uint32_t)kSampleMax) {
     uint32_t kand = 0xFFFFFFFFu, kor = 0u;
-    for_keys(sk, n, [&](uint32_t f, uint32_t k) {
+    for_keys<kSampleKeysPer>(sk, n, [&](uint32_t f, uint32_t k) {
       keys[f] = k;
       kand &= k;
       kor |= k;
@@ -1158,7 +1159,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
   __syncthreads();
   uint32_t kmax = 0u;
-  for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+  for_keys<kSampleKeysPer>(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
     atomicAdd(&hist[k >> 20], 1u);
     kmax = max(kmax, k);
   });
