@@ -39,6 +39,8 @@ enum : int {
   R_NEED = 8,   // winners still needed from bin R_B
 };
 
+constexpr int kBtWords = 8;  // words per record of the block aggregate's (tile, segment) table
+
 struct Tables {
   const int32_t* seg_off;      // [L+1]
   const int32_t* seg_k;        // [L]
@@ -55,8 +57,9 @@ struct Tables {
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row
   const int32_t* run_seg;      // [nruns] top-k: segment of each sample run
-  const uint32_t* btile;       // [2 nbtiles] block aggregate, multi-segment layouts: (1024-element
-                               // data tile, segment) for every pair with an element in common
+  const uint32_t* btile;       // [kBtWords nbtiles] block aggregate, multi-segment layouts: for every
+                               // (1024-element data tile, segment) pair with an element in common:
+                               // tile, segment, its offset, size, k and message offset, 0, 0
   int32_t d, L, nchunks, nrows, nruns, nbtiles;
   int32_t rk_direct;           // random-k: k_stream_sel counts the certain winners and lists the
                                // undecided candidates of every row; k_select gathers the lists

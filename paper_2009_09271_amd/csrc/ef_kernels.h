@@ -726,11 +726,12 @@ constexpr uint32_t kAggBT = 4u * kNT;  // one float4 group per thread
 
 __global__ __launch_bounds__(kNT) void k_agg_block(Tables T, int32_t W, int32_t K, const uint32_t* start,
                                                    const float* val, AggOut O) {
-  const uint2 bt = reinterpret_cast<const uint2*>(T.btile)[blockIdx.x];
-  const int l = (int)bt.y;
-  const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
-  const uint32_t k = (uint32_t)T.seg_k[l], P = (uint32_t)T.seg_P[l];
-  const uint32_t tlo = bt.x * kAggBT;
+  static_assert(kBtWords == 8, "two 16-byte loads per record");
+  const uint4* rec = reinterpret_cast<const uint4*>(T.btile) + 2u * blockIdx.x;
+  const uint4 r0 = rec[0], r1 = rec[1];  // one round trip: no chain through the segment tables
+  const int l = (int)r0.y;
+  const uint32_t o = r0.z, n = r0.w, k = r1.x, P = r1.y;
+  const uint32_t tlo = r0.x * kAggBT;
   const uint32_t lo = max(tlo, o), hi = min(tlo + kAggBT, o + n);
   const uint32_t i0 = tlo + threadIdx.x * 4u;
   const int lane = threadIdx.x & 63;

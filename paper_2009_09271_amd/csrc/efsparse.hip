@@ -162,14 +162,16 @@ void ef_layout::build() {
   }
 
   // block aggregate over several segments: every (1024-element data tile, segment) pair with an
-  // element in common, segment by segment
+  // element in common, segment by segment, with the segment's offset, size, k and message offset
+  // (eight words: the kernel loads a pair's record in one round trip)
   btile.clear();
   if (n > 1) {
     for (int s = 0; s < n; ++s) {
       const int64_t t0 = off64[s] / kAggBT, t1 = (off64[s + 1] - 1) / kAggBT;
       for (int64_t t = t0; t <= t1; ++t) {
-        btile.push_back((uint32_t)t);
-        btile.push_back((uint32_t)s);
+        const uint32_t rec[kBtWords] = {(uint32_t)t, (uint32_t)s, (uint32_t)off64[s],
+                                        (uint32_t)(off64[s + 1] - off64[s]), (uint32_t)k[s], (uint32_t)P[s], 0u, 0u};
+        btile.insert(btile.end(), rec, rec + kBtWords);
       }
     }
   }
@@ -641,7 +643,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
   T.chunk_sl = reinterpret_cast<const int32_t*>(b + L->o_csl);
   T.btile = reinterpret_cast<const uint32_t*>(b + L->o_btile);
-  T.nbtiles = (int32_t)(L->btile.size() / 2);
+  T.nbtiles = (int32_t)(L->btile.size() / kBtWords);
   T.d = (int32_t)L->d;
   T.L = L->L;
   T.nchunks = L->nchunks;
