@@ -57,6 +57,8 @@ struct Tables {
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row
   const int32_t* run_seg;      // [nruns] top-k: segment of each sample run
+  const uint32_t* row_rec;     // [4 nrows] multi-segment layouts: per row its segment, the
+                               // segment's offset and end, and the row's tile base
   const uint32_t* btile;       // [kBtWords nbtiles] block aggregate, multi-segment layouts: for every
                                // (1024-element data tile, segment) pair with an element in common:
                                // tile, segment, its offset, size, k and message offset, 0, 0

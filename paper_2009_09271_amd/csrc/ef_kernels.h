@@ -1223,9 +1223,17 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
   __shared__ uint32_t wc[kStrW];  // random-k, direct lists: certain winners per wavefront
   __shared__ uint32_t s_und;         // random-k, direct lists: undecided candidates listed so far
   const uint32_t row = blockIdx.x;
-  const int l = T.row_seg[row];
-  const uint32_t o = (uint32_t)T.seg_off[l], e_ = (uint32_t)T.seg_off[l + 1];
-  const uint32_t tb = (o / kTile + (row - (uint32_t)T.seg_cbase[l])) * kTile;
+  // the row's segment and bounds: arithmetic on one segment, else one record load (the data loads
+  // wait for the bounds only, not for a chain through the segment tables)
+  int l = 0;
+  uint32_t o = 0, e_ = (uint32_t)T.d, tb = row * kTile;
+  if (T.L > 1) {
+    const uint4 rr = reinterpret_cast<const uint4*>(T.row_rec)[row];
+    l = (int)rr.x;
+    o = rr.y;
+    e_ = rr.z;
+    tb = rr.w;
+  }
   const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   uint32_t* R = res_of(ws, l);
@@ -1241,7 +1249,7 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     tau = T.seg_tau[l];
     ulo = T.seg_ulo[l];
     // the list counter of k_collect starts from zero (this kernel completes before it runs)
-    if (!direct && row == (uint32_t)T.seg_cbase[l] && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
+    if (!direct && tb == o / kTile * kTile && threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
   }
 
   float v[kSR][4];

@@ -55,6 +55,7 @@ struct ef_layout {
 
   std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg, runseg;
   std::vector<uint32_t> btile;  // block aggregate, multi-segment: (data tile, segment) pairs
+  std::vector<uint32_t> rrec;   // multi-segment: per row (segment, its offset and end, tile base)
   std::vector<uint64_t> tau;
   std::vector<uint32_t> ulo;
   int64_t K = 0;
@@ -65,7 +66,7 @@ struct ef_layout {
 
   Blob blob;
   size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_runseg,
-      o_btile;
+      o_btile, o_rrec;
   Tables T{};
   bool bound = false;
 
@@ -145,6 +146,15 @@ void ef_layout::build() {
   rseg.resize(nrows);
   for (int l = 0; l < n; ++l)
     for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) rseg[r] = l;
+  rrec.clear();
+  if (n > 1) {
+    for (int l = 0; l < n; ++l)
+      for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) {
+        const uint32_t rec[4] = {(uint32_t)l, (uint32_t)off64[l], (uint32_t)off64[l + 1],
+                                 (uint32_t)((off64[l] / kTile + (r - cbase[l])) * kTile)};
+        rrec.insert(rrec.end(), rec, rec + 4);
+      }
+  }
   runseg.resize(nruns);
   for (int l = 0; l < n; ++l)
     for (int32_t r = ro[l]; r < ro[l + 1]; ++r) runseg[r] = l;
@@ -193,6 +203,7 @@ void ef_layout::build() {
   o_rseg = blob.add(rseg);
   o_runseg = blob.add(runseg);
   o_btile = blob.add(btile);
+  o_rrec = blob.add(rrec);
   bound = false;
 }
 
@@ -638,6 +649,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.seg_ro = reinterpret_cast<const int32_t*>(b + L->o_ro);
   T.row_seg = reinterpret_cast<const int32_t*>(b + L->o_rseg);
   T.run_seg = reinterpret_cast<const int32_t*>(b + L->o_runseg);
+  T.row_rec = reinterpret_cast<const uint32_t*>(b + L->o_rrec);
   T.seg_tau = reinterpret_cast<const uint64_t*>(b + L->o_tau);
   T.seg_ulo = reinterpret_cast<const uint32_t*>(b + L->o_ulo);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
