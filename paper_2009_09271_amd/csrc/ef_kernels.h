@@ -204,6 +204,24 @@ __device__ __forceinline__ uint32_t run_pos(const RunSeg& r, uint32_t i) {
   return j >= r.s ? j - r.s : j + r.n - r.s;
 }
 
+// The start of every segment that begins in [lo, hi) (segments sf..sl hold the data tile).  With
+// one segment, its record rs is already loaded: no further load, which would make the
+// workgroup's last wavefront wait for its stores before it ends (loads and stores share one
+// counter).
+__device__ __forceinline__ void write_starts(const Tables& T, int sf, int sl, const RunSeg& rs, uint32_t lo,
+                                             uint32_t hi, uint32_t step, uint32_t s0, uint32_t s1,
+                                             uint32_t* start) {
+  if (sf == sl) {
+    if (threadIdx.x == 0 && rs.o >= lo && rs.o < hi) start[sf] = rs.s;
+    return;
+  }
+  for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
+    const uint32_t ol = (uint32_t)T.seg_off[l];
+    if (ol >= lo && ol < hi)
+      start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
+  }
+}
+
 // Fused worker step: acc = g + e; val[P_l + t] = acc on the run; e' = +0 on the run, acc elsewhere.
 // One float4 group per thread for a float32 gradient (kRbTile elements per workgroup); two groups
 // (kRbNT groups apart, each coalesced over the wavefront) for bf16, whose groups are 8-byte loads.
@@ -254,12 +272,7 @@ __global__ __launch_bounds__(kRbNT) void k_randblock_step(Tables T, const void* 
       }
     }
     store4(e, i0, nv, out);
-    // start of every segment that begins in this group
-    for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
-      const uint32_t ol = (uint32_t)T.seg_off[l];
-      if (ol >= lo && ol < hi)
-        start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
-    }
+    write_starts(T, sf, sl, rs, lo, hi, step, s0, s1, start);
   } else {
     constexpr uint32_t NG = rb_groups<GDT>(), TILE = rb_tile<GDT>();
     const uint32_t lo = blockIdx.x * TILE, hi = min((uint32_t)T.d, lo + TILE);
@@ -313,12 +326,7 @@ __global__ __launch_bounds__(kRbNT) void k_randblock_step(Tables T, const void* 
       }
       store4(e, i0[r], nv[r], out);
     }
-    // start of every segment that begins in this workgroup's elements
-    for (int l = sf + (int)threadIdx.x; l <= sl; l += kRbNT) {
-      const uint32_t ol = (uint32_t)T.seg_off[l];
-      if (ol >= lo && ol < hi)
-        start[l] = block_start((uint32_t)l, step, s0, s1, (uint32_t)T.seg_bl[l], (uint32_t)T.seg_nb[l]);
-    }
+    write_starts(T, sf, sl, rs, lo, hi, step, s0, s1, start);
   }
 }
 
