@@ -1520,7 +1520,7 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
 #pragma unroll
   for (uint32_t r = 0; r < kCollectRows; ++r) {
     const uint32_t row = min(row0 + r, (uint32_t)T.nrows - 1u);
-    ls[r] = T.row_seg[row];
+    ls[r] = T.L == 1 ? 0 : T.row_seg[row];  // one segment: no load before the segment's record
     cnts[r] = ws.counts[row];
     k0[r] = ws.cand_key[(size_t)row * kTile + lane];  // the first 64 keys (past the count: unused)
   }
@@ -1967,7 +1967,7 @@ __global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws0, Batch BT) 
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t lds[kNT / 64];
   const uint32_t row = blockIdx.x;
-  const int l = T.row_seg[row];
+  const int l = T.L == 1 ? 0 : T.row_seg[row];
   const uint32_t* R = res_of(ws, l);
   if (R[R_SLOW]) return;
   const uint32_t cnt = ws.counts[row];
@@ -2065,7 +2065,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
   const bool has_row = lane < RW && myrow < (uint32_t)T.nrows;
   uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, ulo = 0;
   if (has_row) {
-    const int l = T.row_seg[myrow];
+    const int l = T.L == 1 ? 0 : T.row_seg[myrow];  // one segment: no load before the record
     const uint32_t* R = res_of(ws, l);
     cnt = ws.counts[myrow];
     off = ws.roff[myrow];
