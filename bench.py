@@ -35,28 +35,17 @@ def _note(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def _gen(args):
-    name, w, t = args
-    from workloads import WORKLOADS, gradient
-    return gradient(WORKLOADS[name], w, t)
-
-
 def gen_gradients(wl, W, t=0):
-    import multiprocessing as mp
+    """The W workers' gradients of step t.  Drawn on host threads (NumPy's generators release the
+    interpreter lock while they fill an array), not in forked processes: a process forked under a
+    profiler carries the profiler's state with it."""
+    from concurrent.futures import ThreadPoolExecutor
+    from workloads import gradient
     n = max(1, min(8, os.cpu_count() or 1, W))
     if n == 1:
-        return [_gen((wl.name, w, t)) for w in range(W)]
-    # close + join: the workers exit on their own (the pool's context manager would end them with
-    # SIGTERM, which a profiler's preloaded signal handler in the forked workers does not survive)
-    pool = mp.get_context("fork").Pool(n)
-    try:
-        out = pool.map(_gen, [(wl.name, w, t) for w in range(W)])
-        pool.close()
-    except BaseException:
-        pool.terminate()
-        raise
-    pool.join()
-    return out
+        return [gradient(wl, w, t) for w in range(W)]
+    with ThreadPoolExecutor(n) as ex:
+        return list(ex.map(lambda w: gradient(wl, w, t), range(W)))
 
 
 def variant_list(spec, blocks):
@@ -247,6 +236,8 @@ def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20,
         E.timing_enable(False)
         r["fused_step"]["kernels_us"] = {name: round(tot * 1e3 / nl, 3)
                                          for name, (tot, nl) in E.timing_collect(reset=True).items()}
+        if ws is not None:  # the diagnostics word over every run of this step so far
+            r["fused_step"]["diag"] = lay.diag(ws, E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK)
         # composed: the same algorithmic bytes (the intermediate acc costs 8d more by construction)
         r["composed_step"] = entry(timed(composed), step_b, d)
         if kind == "randk":
@@ -268,13 +259,42 @@ def measure_single(E, torch, dev, offs, density, variants, W, g, seeds, reps=20,
     return res
 
 
-def cpu_baseline(wl, offs, ks, variants, W, grads, budget_note):
+def host_description():
+    """The host the oracle runs on: logical CPUs, this process's affinity set and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    aff = sorted(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None
+    return {"os_cpu_count": os.cpu_count(), "affinity": aff, "cpu_model": model}
+
+
+def cpu_baseline(wl, offs, ks, variants, W, grads, budget_note, min_s=10.0):
     """Time the CPU oracle on a bounded sample of worker steps plus one aggregate per variant,
-    and scale to the GPU step's work (W steps + 1 aggregate per variant)."""
+    and scale to the GPU step's work (W steps + 1 aggregate per variant).  The oracle runs on one
+    core: its process is pinned to one CPU of its affinity set and BLAS / OpenMP pools to one
+    thread; the affinity is restored afterwards."""
     from oracle import efsparse_oracle as O
     from threadpoolctl import threadpool_limits
-    with threadpool_limits(1):
-        return _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note)
+    host = host_description()
+    old = set(host["affinity"]) if host["affinity"] else None
+    pinned = None
+    if old and hasattr(os, "sched_setaffinity"):
+        pinned = min(old)
+        os.sched_setaffinity(0, {pinned})
+    try:
+        with threadpool_limits(1):
+            r = _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note, min_s=min_s)
+    finally:
+        if pinned is not None:
+            os.sched_setaffinity(0, old)
+    r["host"] = dict(host, pinned_cpu=pinned)
+    return r
 
 
 def _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note, min_s=10.0):
@@ -613,6 +633,21 @@ def main():
     elems_per_step = len(variants) * W * d
     value = elems_per_step / (ms_per_step / 1e3)
 
+    # diagnostics words of the top-k / random-k workspaces, OR-ed over every worker and every step
+    # so far (warm-up and timed): bit 1 = a segment took the exact whole-segment path, bit 2 = a
+    # row-count mismatch (never expected)
+    diagnostics = {}
+    for k, op in (("topk", E.EF_OP_TOPK), ("randk", E.EF_OP_RANDK)):
+        if k not in kinds:
+            continue
+        rows = [wsb[k][0][w] for w in range(W)] if args.schedule == "batch" else \
+            (ws_topk if k == "topk" else ws_randk)
+        word = 0
+        for r in rows:
+            word |= lay0.diag(r, op)
+        diagnostics[k] = {"word": word, "exact_path_taken": bool(word & E.DIAG_SLOW_PATH),
+                          "count_mismatch": bool(word & E.DIAG_COUNT_MISMATCH)}
+
     # ---- per-variant breakdown: each variant alone (batch schedule: its W steps and aggregate on
     # one stream; other schedules: their own schedule with one variant) -------------------------
     _note("each variant alone")
@@ -709,6 +744,17 @@ def main():
         _note("next rows")
     nxt = {} if args.no_next else measure_next(E, torch, dev, wl, lay0, layouts, msg, variants, W, d, K, L, args)
 
+    # each compressor's own fraction of the HBM roofline, next to the dominant kernel's: its W
+    # batched steps plus aggregate, one worker's lone fused step and the aggregate alone
+    per_roof = {}
+    for v in variants:
+        n = vname(v)
+        ent = {"batched_steps_and_aggregate": per[n]["frac_of_hbm_peak"]}
+        for scope, sres in single.items():
+            ent[f"lone_step_{scope}"] = sres[n]["fused_step"]["frac_of_hbm_peak"]
+            ent[f"aggregate_{scope}"] = sres[n]["aggregate"]["frac_of_hbm_peak"]
+        per_roof[n] = ent
+
     cpu = None
     if not args.no_cpu_baseline:
         _note("CPU oracle sample")
@@ -743,6 +789,8 @@ def main():
                                       "on another"}[args.schedule],
         },
         "roofline": roofline,
+        "per_compressor_roofline": per_roof,
+        "diagnostics": diagnostics,
         "cpu_baseline": cpu,
         "per_compressor": per,
         "kernels": kernels,

@@ -64,6 +64,8 @@ extern "C" {
 #define EF_ERANGE 2     /* d == 0, d >= 2^31, n_seg < 1 or n_seg >= 2^24, W < 1 or W > 65535 */
 #define EF_EWORKSPACE 3 /* ws_bytes smaller than ef_workspace_bytes() */
 #define EF_EHIP 4       /* a HIP runtime or launch error */
+#define EF_ENOMEM 5     /* host memory for a layout's tables (or the timing records) could not be
+                           allocated; a layout whose ef_layout_tune failed this way is unusable */
 
 /* gradient dtypes */
 #define EF_F32 0
@@ -107,7 +109,7 @@ const char* ef_last_hip_error_string(void);
  *   density      k/d fraction in (0, 1] (Section 4.1 uses 1 %)
  *   block        random-block start alignment b >= 1; a segment with d_l <= b uses 1
  *   out          receives the new layout (unchanged on error)
- * Returns EF_OK, EF_EINVAL or EF_ERANGE.  Pure host code. */
+ * Returns EF_OK, EF_EINVAL, EF_ERANGE or EF_ENOMEM.  Pure host code. */
 int ef_layout_create(int64_t d, const int64_t* seg_offsets, int32_t n_seg, double density,
                      int64_t block, ef_layout** out);
 int ef_layout_destroy(ef_layout* layout);
@@ -118,7 +120,8 @@ int32_t ef_layout_num_segments(const ef_layout* layout);
 /* Copies k_l for every segment into the host array k_out[n_seg]. */
 int ef_layout_segment_k(const ef_layout* layout, int64_t* k_out);
 
-/* Change a performance knob (EF_TUNE_*).  Must be called before ef_layout_bind. */
+/* Change a performance knob (EF_TUNE_*).  Unbinds the layout (bind it again before use).
+ * Returns EF_ENOMEM, and leaves the layout unusable, if its tables cannot be rebuilt. */
 int ef_layout_tune(ef_layout* layout, int knob, double value);
 
 /* Bytes of device memory the layout's tables need. */

@@ -19,7 +19,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("EFSPARSE_LIB") or os.path.join(_HERE, "libefsparse.so")
 
-EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP = range(5)
+EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP, EF_ENOMEM = range(6)
 EF_F32, EF_BF16 = 0, 1
 EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK, EF_OP_AGG_SHARED, EF_OP_RANDK_PREP = range(7)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
@@ -96,11 +96,13 @@ EXPORTED = tuple(_SIGS)
 
 
 class EfError(RuntimeError):
-    def __init__(self, code, where):
+    def __init__(self, code, where, detail=None):
         self.code = code
         msg = f"{where}: {_lib.ef_status_string(code).decode()}"
         if code == EF_EHIP:
             msg += f" ({_lib.ef_last_hip_error()}: {_lib.ef_last_hip_error_string().decode()})"
+        if detail:
+            msg += f" ({detail})"
         super().__init__(msg)
 
 
@@ -120,6 +122,40 @@ def _stream(t, stream=None):
 
 def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _nbytes(t):
+    """Byte size of a workspace tensor (0 for None)."""
+    return t.numel() * t.element_size() if t is not None else 0
+
+
+_F32, _IDX, _GRAD, _ANY = "f32", "idx", "grad", "any"
+
+
+def _need(layout, t, n, kind, name, where, optional=False):
+    """Checks a tensor argument before its pointer crosses the ABI: on the layout's device,
+    contiguous, of the expected dtype and holding at least n elements, so that no kernel can write
+    past its end.  Raises EfError(EF_EINVAL) otherwise."""
+    import torch
+    if t is None:
+        if optional:
+            return
+        raise EfError(EF_EINVAL, where, f"{name} is None")
+    ok = {_F32: (torch.float32,), _GRAD: (torch.float32, torch.bfloat16),
+          _IDX: tuple(x for x in (torch.int32, getattr(torch, "uint32", None)) if x is not None)}.get(kind)
+    if not isinstance(t, torch.Tensor):
+        raise EfError(EF_EINVAL, where, f"{name} is not a tensor")
+    if not t.is_cuda:
+        raise EfError(EF_EINVAL, where, f"{name} is not on a GPU")
+    dev = layout.tables.device if getattr(layout, "tables", None) is not None else None
+    if dev is not None and t.device != dev:
+        raise EfError(EF_EINVAL, where, f"{name} is on {t.device}, the layout on {dev}")
+    if not t.is_contiguous():
+        raise EfError(EF_EINVAL, where, f"{name} is not contiguous")
+    if ok is not None and t.dtype not in ok:
+        raise EfError(EF_EINVAL, where, f"{name} has dtype {t.dtype}")
+    if t.numel() < n:
+        raise EfError(EF_EINVAL, where, f"{name} holds {t.numel()} elements, {n} needed")
 
 
 def _gdt(g):
@@ -204,76 +240,137 @@ class Layout:
         return int(ws[off:off + 4].cpu().numpy().view(np.uint32)[0])
 
 
+def _msg_len(layout, msg_kind):
+    """Entries of one message's index (sparse) or start (block) array."""
+    return layout.n_seg if msg_kind == EF_MSG_BLOCK else layout.K
+
+
 def ef_accumulate(layout, g, e, acc):
-    _check(_lib.ef_accumulate(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(acc), _stream(e)), "ef_accumulate")
+    w, d = "ef_accumulate", layout.d
+    _need(layout, g, d, _GRAD, "g", w)
+    _need(layout, e, d, _F32, "e", w)
+    _need(layout, acc, d, _F32, "acc", w)
+    _check(_lib.ef_accumulate(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(acc), _stream(e)), w)
 
 
 def compress_topk(layout, acc, idx, val, ws):
-    _check(_lib.compress_topk(layout.handle, _ptr(acc), _ptr(idx), _ptr(val), _ptr(ws), ws.numel(), _stream(acc)),
-           "compress_topk")
+    w = "compress_topk"
+    _need(layout, acc, layout.d, _F32, "acc", w)
+    _need(layout, idx, layout.K, _IDX, "idx", w)
+    _need(layout, val, layout.K, _F32, "val", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
+    _check(_lib.compress_topk(layout.handle, _ptr(acc), _ptr(idx), _ptr(val), _ptr(ws), _nbytes(ws), _stream(acc)),
+           w)
 
 
 def compress_randk(layout, acc, seed, step, idx, val, ws):
+    w = "compress_randk"
+    _need(layout, acc, layout.d, _F32, "acc", w)
+    _need(layout, idx, layout.K, _IDX, "idx", w)
+    _need(layout, val, layout.K, _F32, "val", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
     _check(_lib.compress_randk(layout.handle, _ptr(acc), int(seed), int(step), _ptr(idx), _ptr(val), _ptr(ws),
-                               ws.numel(), _stream(acc)), "compress_randk")
+                               _nbytes(ws), _stream(acc)), w)
 
 
 def compress_randblock(layout, acc, seed, step, start, val):
+    w = "compress_randblock"
+    _need(layout, acc, layout.d, _F32, "acc", w)
+    _need(layout, start, layout.n_seg, _IDX, "start", w)
+    _need(layout, val, layout.K, _F32, "val", w)
     _check(_lib.compress_randblock(layout.handle, _ptr(acc), int(seed), int(step), _ptr(start), _ptr(val),
-                                   _stream(acc)), "compress_randblock")
+                                   _stream(acc)), w)
 
 
 def ef_update(layout, acc, msg_kind, idx_or_start, e):
-    _check(_lib.ef_update(layout.handle, _ptr(acc), int(msg_kind), _ptr(idx_or_start), _ptr(e), _stream(e)),
-           "ef_update")
+    w = "ef_update"
+    _need(layout, acc, layout.d, _F32, "acc", w)
+    _need(layout, e, layout.d, _F32, "e", w)
+    _need(layout, idx_or_start, _msg_len(layout, msg_kind), _IDX, "idx_or_start", w)
+    _check(_lib.ef_update(layout.handle, _ptr(acc), int(msg_kind), _ptr(idx_or_start), _ptr(e), _stream(e)), w)
+
+
+def _agg_args(layout, msg_kind, W, idx_or_start, val, w):
+    _need(layout, idx_or_start, int(W) * _msg_len(layout, msg_kind), _IDX, "idx_or_start", w)
+    _need(layout, val, int(W) * layout.K, _F32, "val", w)
 
 
 def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, average=True, stream=None):
-    n = ws.numel() if ws is not None else 0
+    w = "decompress_aggregate"
+    _agg_args(layout, msg_kind, W, idx_or_start, val, w)
+    _need(layout, out, layout.d, _F32, "out", w)
+    _need(layout, ws, 0, _ANY, "ws", w, optional=True)
     _check(_lib.decompress_aggregate(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
-                                     1 if average else 0, _ptr(out), _ptr(ws), n, _stream(out, stream)),
-           "decompress_aggregate")
+                                     1 if average else 0, _ptr(out), _ptr(ws), _nbytes(ws), _stream(out, stream)), w)
 
 
 def decompress_aggregate_apply(layout, msg_kind, W, idx_or_start, val, x, mom=None, beta=0.0, wd=0.0, out=None,
                                ws=None, average=True, stream=None):
-    n = ws.numel() if ws is not None else 0
+    w = "decompress_aggregate_apply"
+    _agg_args(layout, msg_kind, W, idx_or_start, val, w)
+    _need(layout, x, layout.d, _F32, "x", w)
+    _need(layout, mom, layout.d, _F32, "mom", w, optional=True)
+    _need(layout, out, layout.d, _F32, "out", w, optional=True)
+    _need(layout, ws, 0, _ANY, "ws", w, optional=True)
     _check(_lib.decompress_aggregate_apply(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
                                            1 if average else 0, _ptr(x), _ptr(mom), float(beta), float(wd),
-                                           _ptr(out), _ptr(ws), n, _stream(x, stream)),
-           "decompress_aggregate_apply")
+                                           _ptr(out), _ptr(ws), _nbytes(ws), _stream(x, stream)), w)
 
 
 def decompress_aggregate_shared(layout, msg_kind, W, idx_or_start, val, out, ws, average=True, stream=None):
+    w = "decompress_aggregate_shared"
+    _need(layout, idx_or_start, _msg_len(layout, msg_kind), _IDX, "idx_or_start", w)
+    _need(layout, val, int(W) * layout.K, _F32, "val", w)
+    _need(layout, out, layout.d, _F32, "out", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
     _check(_lib.decompress_aggregate_shared(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
-                                            1 if average else 0, _ptr(out), _ptr(ws), ws.numel(),
-                                            _stream(out, stream)), "decompress_aggregate_shared")
+                                            1 if average else 0, _ptr(out), _ptr(ws), _nbytes(ws),
+                                            _stream(out, stream)), w)
 
 
 def ef_dense_average(layout, W, g, out, average=True, stream=None):
+    w = "ef_dense_average"
+    _need(layout, g, int(W) * layout.d, _F32, "g", w)
+    _need(layout, out, layout.d, _F32, "out", w)
     _check(_lib.ef_dense_average(layout.handle, int(W), _ptr(g), 1 if average else 0, _ptr(out),
-                                 _stream(out, stream)), "ef_dense_average")
+                                 _stream(out, stream)), w)
+
+
+def _step_args(layout, g, e, idx, val, ws, w, idx_len=None):
+    _need(layout, g, layout.d, _GRAD, "g", w)
+    _need(layout, e, layout.d, _F32, "e", w)
+    _need(layout, idx, layout.K if idx_len is None else idx_len, _IDX, "idx", w)
+    _need(layout, val, layout.K, _F32, "val", w)
+    if ws is not False:
+        _need(layout, ws, 0, _ANY, "ws", w)
 
 
 def ef_step_topk(layout, g, e, idx, val, ws):
-    _check(_lib.ef_step_topk(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val), _ptr(ws), ws.numel(),
-                             _stream(e)), "ef_step_topk")
+    w = "ef_step_topk"
+    _step_args(layout, g, e, idx, val, ws, w)
+    _check(_lib.ef_step_topk(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val), _ptr(ws), _nbytes(ws),
+                             _stream(e)), w)
 
 
 def ef_step_randk(layout, g, e, seed, step, idx, val, ws):
+    w = "ef_step_randk"
+    _step_args(layout, g, e, idx, val, ws, w)
     _check(_lib.ef_step_randk(layout.handle, _ptr(g), _gdt(g), _ptr(e), int(seed), int(step), _ptr(idx), _ptr(val),
-                              _ptr(ws), ws.numel(), _stream(e)), "ef_step_randk")
+                              _ptr(ws), _nbytes(ws), _stream(e)), w)
 
 
 def ef_step_topk_phases(layout, phases, g, e, idx, val, ws, stream=None):
+    w = "ef_step_topk_phases"
+    _step_args(layout, g, e, idx, val, ws, w)
     _check(_lib.ef_step_topk_phases(layout.handle, int(phases), _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val),
-                                    _ptr(ws), ws.numel(), _stream(e, stream)), "ef_step_topk_phases")
+                                    _ptr(ws), _nbytes(ws), _stream(e, stream)), w)
 
 
 def ef_step_randk_phases(layout, phases, g, e, seed, step, idx, val, ws, stream=None):
+    w = "ef_step_randk_phases"
+    _step_args(layout, g, e, idx, val, ws, w)
     _check(_lib.ef_step_randk_phases(layout.handle, int(phases), _ptr(g), _gdt(g), _ptr(e), int(seed), int(step),
-                                     _ptr(idx), _ptr(val), _ptr(ws), ws.numel(), _stream(e, stream)),
-           "ef_step_randk_phases")
+                                     _ptr(idx), _ptr(val), _ptr(ws), _nbytes(ws), _stream(e, stream)), w)
 
 
 def batch_workspace(layout, op, W, device="cuda"):
@@ -287,58 +384,93 @@ def _ptr_table(tensors):
     return (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
 
 
+def _batch_args(layout, g, e, idx, val, ws, ws_stride, w):
+    """Per-worker gradients and residuals, [W][K] messages and W workspace rows of ws_stride bytes."""
+    if g is not None and len(g) != len(e):
+        raise ValueError("one gradient and one residual per worker")
+    W = len(e)
+    if W == 0:
+        raise EfError(EF_ERANGE, w, "no workers")
+    for i in range(W):
+        if g is not None:
+            _need(layout, g[i], layout.d, _GRAD, f"g[{i}]", w)
+        _need(layout, e[i], layout.d, _F32, f"e[{i}]", w)
+    if g is not None and any(x.dtype != g[0].dtype for x in g):
+        raise EfError(EF_EINVAL, w, "the gradients differ in dtype")
+    _need(layout, idx, W * layout.K, _IDX, "idx", w)
+    if val is not None:
+        _need(layout, val, W * layout.K, _F32, "val", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
+    if _nbytes(ws) < W * int(ws_stride):
+        raise EfError(EF_EWORKSPACE, w, f"ws holds {_nbytes(ws)} bytes, {W} rows of {int(ws_stride)} needed")
+
+
 def ef_step_topk_batch(layout, g, e, idx, val, ws, ws_stride, phases=EF_PHASE_ALL, stream=None):
     """W workers' fused top-k steps: g, e lists of W tensors; idx, val [W][K] (rows of the batch); ws rows
     from batch_workspace."""
-    if len(g) != len(e):
-        raise ValueError("one gradient and one residual per worker")
+    w = "ef_step_topk_batch"
+    _batch_args(layout, g, e, idx, val, ws, ws_stride, w)
     _check(_lib.ef_step_topk_batch(layout.handle, int(phases), len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
-                                   _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride), _stream(e[0], stream)),
-           "ef_step_topk_batch")
+                                   _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride), _stream(e[0], stream)), w)
 
 
 def ef_step_randk_batch(layout, g, e, seeds, step, idx, val, ws, ws_stride, phases=EF_PHASE_ALL, stream=None):
     """W workers' fused random-k steps; seeds: W integers (host)."""
+    w = "ef_step_randk_batch"
     sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64))
     if len(g) != len(e) or sd.shape != (len(e),):
         raise ValueError("one gradient, one residual and one seed per worker")
+    _batch_args(layout, g, e, idx, val, ws, ws_stride, w)
     _check(_lib.ef_step_randk_batch(layout.handle, int(phases), len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
                                     sd.ctypes.data, int(step), _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride),
-                                    _stream(e[0], stream)), "ef_step_randk_batch")
+                                    _stream(e[0], stream)), w)
 
 
 def ef_randk_prepare(layout, seed, step, idx, ws, stream=None):
     """The random-k message indices of (seed, step) and their tile table in ws (EF_OP_RANDK_PREP)."""
-    _check(_lib.ef_randk_prepare(layout.handle, int(seed), int(step), _ptr(idx), _ptr(ws), ws.numel(),
-                                 _stream(idx, stream)), "ef_randk_prepare")
+    w = "ef_randk_prepare"
+    _need(layout, idx, layout.K, _IDX, "idx", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
+    _check(_lib.ef_randk_prepare(layout.handle, int(seed), int(step), _ptr(idx), _ptr(ws), _nbytes(ws),
+                                 _stream(idx, stream)), w)
 
 
 def ef_randk_prepare_batch(layout, seeds, step, idx, ws, ws_stride, stream=None):
     """W workers' prepared selections: seeds W integers (host); idx [W][K]; ws rows from batch_workspace
     (EF_OP_RANDK_PREP)."""
+    w = "ef_randk_prepare_batch"
     sd = np.ascontiguousarray(np.asarray(seeds, dtype=np.uint64))
-    _check(_lib.ef_randk_prepare_batch(layout.handle, sd.shape[0], sd.ctypes.data, int(step), _ptr(idx), _ptr(ws),
-                                       int(ws_stride), _stream(idx, stream)), "ef_randk_prepare_batch")
+    W = sd.shape[0]
+    _need(layout, idx, W * layout.K, _IDX, "idx", w)
+    _need(layout, ws, 0, _ANY, "ws", w)
+    if W and _nbytes(ws) < W * int(ws_stride):
+        raise EfError(EF_EWORKSPACE, w, f"ws holds {_nbytes(ws)} bytes, {W} rows of {int(ws_stride)} needed")
+    _check(_lib.ef_randk_prepare_batch(layout.handle, W, sd.ctypes.data, int(step), _ptr(idx), _ptr(ws),
+                                       int(ws_stride), _stream(idx, stream)), w)
 
 
 def ef_step_randk_prepared(layout, g, e, idx, val, ws, stream=None):
     """The random-k step given prepared indices and workspace."""
+    w = "ef_step_randk_prepared"
+    _step_args(layout, g, e, idx, val, ws, w)
     _check(_lib.ef_step_randk_prepared(layout.handle, _ptr(g), _gdt(g), _ptr(e), _ptr(idx), _ptr(val), _ptr(ws),
-                                       ws.numel(), _stream(e, stream)), "ef_step_randk_prepared")
+                                       _nbytes(ws), _stream(e, stream)), w)
 
 
 def ef_step_randk_prepared_batch(layout, g, e, idx, val, ws, ws_stride, stream=None):
     """W workers' random-k steps given their prepared indices (rows of idx) and workspaces (rows of ws)."""
-    if len(g) != len(e):
-        raise ValueError("one gradient and one residual per worker")
+    w = "ef_step_randk_prepared_batch"
+    _batch_args(layout, g, e, idx, val, ws, ws_stride, w)
     _check(_lib.ef_step_randk_prepared_batch(layout.handle, len(e), _ptr_table(g), _gdt(g[0]), _ptr_table(e),
                                              _ptr(idx), _ptr(val), _ptr(ws), int(ws_stride), _stream(e[0], stream)),
-           "ef_step_randk_prepared_batch")
+           w)
 
 
 def ef_step_randblock(layout, g, e, seed, step, start, val, stream=None):
+    w = "ef_step_randblock"
+    _step_args(layout, g, e, start, val, False, w, idx_len=layout.n_seg)
     _check(_lib.ef_step_randblock(layout.handle, _ptr(g), _gdt(g), _ptr(e), int(seed), int(step), _ptr(start),
-                                  _ptr(val), _stream(e, stream)), "ef_step_randblock")
+                                  _ptr(val), _stream(e, stream)), w)
 
 
 def lib():

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -69,6 +70,7 @@ struct ef_layout {
       o_btile, o_rrec;
   Tables T{};
   bool bound = false;
+  bool valid = false;  // build() completed (host memory for the tables was available)
 
   void build();
   WsLayout ws_layout(int op) const;
@@ -279,7 +281,7 @@ struct TimingAgg {
   int64_t n;
 };
 std::mutex g_tm;
-bool g_timing = false;
+std::atomic<bool> g_timing{false};  // read on every launch without the lock
 std::vector<TimingRec> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::vector<TimingAgg> g_totals;
@@ -298,11 +300,17 @@ hipEvent_t pool_event() {
 // While timing is on, a launch gets a start and a stop event that the runtime ties to the kernel's
 // own dispatch (hipExtLaunchKernelGGL), so the elapsed time is the kernel's execution alone.
 bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
-  if (!g_timing) return false;
+  if (!g_timing.load(std::memory_order_relaxed)) return false;
   std::lock_guard<std::mutex> lk(g_tm);
   TimingRec r{name, pool_event(), pool_event()};
   if (!r.a || !r.b) return false;
-  g_pending.push_back(r);
+  try {
+    g_pending.push_back(r);
+  } catch (const std::bad_alloc&) {  // no room to record it: the launch goes untimed
+    g_pool.push_back(r.a);
+    g_pool.push_back(r.b);
+    return false;
+  }
   *a = r.a;
   *b = r.b;
   return true;
@@ -325,7 +333,7 @@ bool timing_slot(const char* name, hipEvent_t* a, hipEvent_t* b) {
   } while (0)
 
 int check_bound(const ef_layout* L) {
-  if (!L || !L->bound) return EF_EINVAL;
+  if (!L || !L->valid || !L->bound) return EF_EINVAL;
   return EF_OK;
 }
 
@@ -521,6 +529,7 @@ const char* ef_status_string(int status) {
     case EF_ERANGE: return "EF_ERANGE: size out of range";
     case EF_EWORKSPACE: return "EF_EWORKSPACE: workspace too small";
     case EF_EHIP: return "EF_EHIP: HIP runtime or launch error";
+    case EF_ENOMEM: return "EF_ENOMEM: out of host memory";
     default: return "unknown efsparse status";
   }
 }
@@ -533,7 +542,7 @@ const char* ef_last_hip_error_string(void) {
 
 int ef_timing_enable(int enable) {
   std::lock_guard<std::mutex> lk(g_tm);
-  g_timing = enable != 0;
+  g_timing.store(enable != 0);
   return EF_OK;
 }
 
@@ -546,14 +555,20 @@ int ef_timing_collect(void) {
     TimingAgg* agg = nullptr;
     for (TimingAgg& t : g_totals)
       if (t.name == r.name) agg = &t;
-    if (!agg) {
-      g_totals.push_back(TimingAgg{r.name, 0.0, 0});
-      agg = &g_totals.back();
+    try {
+      if (!agg) {
+        g_totals.push_back(TimingAgg{r.name, 0.0, 0});
+        agg = &g_totals.back();
+      }
+      g_pool.push_back(r.a);
+      g_pool.push_back(r.b);
+    } catch (const std::bad_alloc&) {
+      rc = EF_ENOMEM;
     }
-    agg->ms += ms;
-    agg->n += 1;
-    g_pool.push_back(r.a);
-    g_pool.push_back(r.b);
+    if (agg) {
+      agg->ms += ms;
+      agg->n += 1;
+    }
   }
   g_pending.clear();
   return rc;
@@ -590,13 +605,21 @@ int ef_layout_create(int64_t d, const int64_t* seg_offsets, int32_t n_seg, doubl
   for (int32_t i = 0; i < n_seg; ++i)
     if (seg_offsets[i + 1] <= seg_offsets[i]) return EF_EINVAL;
   ef_layout* L = new (std::nothrow) ef_layout();
-  if (!L) return EF_EINVAL;
+  if (!L) return EF_ENOMEM;
   L->d = d;
   L->L = n_seg;
   L->density = density;
   L->block = block;
-  L->off64.assign(seg_offsets, seg_offsets + n_seg + 1);
-  L->build();
+  // the tables are host vectors: an allocation failure ends here as a status, never as an
+  // exception through the C ABI
+  try {
+    L->off64.assign(seg_offsets, seg_offsets + n_seg + 1);
+    L->build();
+  } catch (const std::bad_alloc&) {
+    delete L;
+    return EF_ENOMEM;
+  }
+  L->valid = true;
   *out = L;
   return EF_OK;
 }
@@ -606,11 +629,11 @@ int ef_layout_destroy(ef_layout* layout) {
   return EF_OK;
 }
 
-int64_t ef_layout_total_k(const ef_layout* layout) { return layout ? layout->K : -1; }
+int64_t ef_layout_total_k(const ef_layout* layout) { return layout && layout->valid ? layout->K : -1; }
 int32_t ef_layout_num_segments(const ef_layout* layout) { return layout ? layout->L : -1; }
 
 int ef_layout_segment_k(const ef_layout* layout, int64_t* k_out) {
-  if (!layout || !k_out) return EF_EINVAL;
+  if (!layout || !layout->valid || !k_out) return EF_EINVAL;
   for (int l = 0; l < layout->L; ++l) k_out[l] = layout->k[l];
   return EF_OK;
 }
@@ -624,14 +647,24 @@ int ef_layout_tune(ef_layout* layout, int knob, double value) {
     case EF_TUNE_TOPK_EXTRA: layout->tk_extra = value; break;
     default: return EF_EINVAL;
   }
-  layout->build();
+  // a failed rebuild leaves the layout unusable (every later call on it returns EF_EINVAL)
+  layout->valid = false;
+  layout->bound = false;
+  try {
+    layout->build();
+  } catch (const std::bad_alloc&) {
+    return EF_ENOMEM;
+  }
+  layout->valid = true;
   return EF_OK;
 }
 
-size_t ef_layout_device_bytes(const ef_layout* layout) { return layout ? layout->blob.bytes.size() : 0; }
+size_t ef_layout_device_bytes(const ef_layout* layout) {
+  return layout && layout->valid ? layout->blob.bytes.size() : 0;
+}
 
 int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
-  if (!L || !dev || !aligned(dev, kAlign)) return EF_EINVAL;
+  if (!L || !L->valid || !dev || !aligned(dev, kAlign)) return EF_EINVAL;
   if (bytes < L->blob.bytes.size()) return EF_EWORKSPACE;
   hipStream_t st = S(stream);
   EF_TRY(hip_status(hipMemcpyAsync(dev, L->blob.bytes.data(), L->blob.bytes.size(), hipMemcpyHostToDevice, st)));
@@ -667,7 +700,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
 }
 
 size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W) {
-  if (!layout) return 0;
+  if (!layout || !layout->valid) return 0;
   switch (op) {
     case EF_OP_TOPK:
     case EF_OP_RANDK: return layout->ws_layout(op).total;
@@ -778,7 +811,12 @@ static int prepare_randk(const ef_layout* L, int32_t W, const uint64_t* seeds, u
   if (W < 1 || W > 65535) return EF_ERANGE;
   if (!seeds || !word_ok(idx) || !ws || !aligned(ws, kAlign)) return EF_EINVAL;
   if (ws_bytes < ef_workspace_bytes(L, EF_OP_RANDK_PREP, 1)) return EF_EWORKSPACE;
-  std::vector<const float*> none((size_t)W, nullptr);
+  std::vector<const float*> none;
+  try {
+    none.assign((size_t)W, nullptr);
+  } catch (const std::bad_alloc&) {
+    return EF_ENOMEM;
+  }
   Steps P;
   P.W = W;
   P.src = none.data();

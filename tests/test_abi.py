@@ -121,5 +121,28 @@ def test_tune_rejects_bad_knobs():
 
 
 def test_status_strings():
-    for c in range(5):
+    for c in range(6):
         assert E.lib().ef_status_string(c).decode().startswith("EF_")
+    assert "memory" in E.lib().ef_status_string(E.EF_ENOMEM).decode()
+
+
+def test_binding_refuses_tensors_that_do_not_fit_before_calling_the_library():
+    """The binding checks every tensor argument (device, contiguity, dtype, size) before its
+    pointer crosses the ABI; host tensors and short or mistyped ones raise EF_EINVAL."""
+    import torch
+    L = E.Layout(1000, None, 0.1)
+    g = torch.zeros(1000)
+    idx = torch.zeros(L.K, dtype=torch.int32)
+    with pytest.raises(E.EfError) as ex:
+        E.ef_step_topk(L, g, g, idx, torch.zeros(L.K), torch.zeros(256, dtype=torch.uint8))
+    assert ex.value.code == E.EF_EINVAL and "not on a GPU" in str(ex.value)
+    with pytest.raises(E.EfError) as ex:
+        E.ef_step_randblock(L, None, g, 1, 0, idx, torch.zeros(L.K))
+    assert ex.value.code == E.EF_EINVAL and "g is None" in str(ex.value)
+
+
+def test_tune_unbinds_and_keeps_the_layout_usable():
+    L = E.Layout(100, None, 0.1)
+    K = L.K
+    assert E.lib().ef_layout_tune(L.handle, E.EF_TUNE_TOPK_SIGMA, 3.0) == E.EF_OK
+    assert L.K == K and L.device_bytes() > 0

@@ -58,3 +58,19 @@ def test_cpu_baseline_record():
     assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "elements/s"
     assert r["value"] > 0 and r["measured_s"] >= 0
     assert "workers 0..0" in r["sample"] and "randblock256" in r["sample"]
+
+
+def test_cpu_baseline_pins_one_core_and_describes_the_host():
+    from oracle import efsparse_oracle as O
+    from workloads import WORKLOADS
+    wl = WORKLOADS["flat1m"]
+    offs = [0, 20000]
+    ks = O.segment_ks(offs, 0.01)
+    grads = [np.random.default_rng(6).standard_normal(offs[-1]).astype(np.float32)]
+    before = os.sched_getaffinity(0)
+    r = bench.cpu_baseline(wl, offs, ks, [("topk", 1)], 1, grads, "", min_s=0.0)
+    assert os.sched_getaffinity(0) == before  # restored
+    h = r["host"]
+    assert h["os_cpu_count"] == os.cpu_count() and h["affinity"] == sorted(before)
+    assert h["pinned_cpu"] in before and r["cores"] == 1
+    assert h["cpu_model"] is None or isinstance(h["cpu_model"], str)
