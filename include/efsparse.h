@@ -208,6 +208,25 @@ int decompress_aggregate_apply(const ef_layout* layout, int msg_kind, int32_t W,
                                float* mom, float beta, float wd, float* out, void* ws, size_t ws_bytes,
                                void* stream);
 
+/* decompress_aggregate for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same operation, arguments and result, bitwise, without a
+ * workspace argument.  The sparse aggregate's tile-range table lives in a
+ * static device array of ef_noalloc_scratch_bytes() bytes (16 MiB) that each
+ * GPU the library runs on holds until the process ends; the call allocates
+ * nothing (its first call on a device resolves that device's copy).
+ *   Limit: ef_workspace_bytes(layout, EF_OP_AGG_SPARSE, W) must not exceed
+ *   ef_noalloc_scratch_bytes() (W * (ceil(d / 1024) + 1) * 4 bytes, rounded
+ *   up to 256), else EF_EWORKSPACE; block messages need no scratch.
+ *   Every call on one GPU shares that GPU's array: calls that overlap on one
+ *   GPU (on different streams or from different threads) race and must be
+ *   ordered by the caller.  The stream must belong to the device whose memory
+ *   the layout, messages and out live in. */
+int decompress_aggregate_noalloc(const ef_layout* layout, int msg_kind, int32_t W,
+                                 const uint32_t* idx_or_start, const float* val, int average,
+                                 float* out, void* stream);
+size_t ef_noalloc_scratch_bytes(void);
+
 /* Algorithm 1's aggregate step when the workers share coordinates (Section
  * 3: equal seeds, the allReduce mode): every message has the same indices
  * (sparse) or block starts (block), given once:

@@ -65,6 +65,8 @@ _SIGS = {
     "decompress_aggregate": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_size_t, _P]),
     "decompress_aggregate_apply": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_float,
                                               _c.c_float, _P, _P, _c.c_size_t, _P]),
+    "decompress_aggregate_noalloc": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P]),
+    "ef_noalloc_scratch_bytes": (_c.c_size_t, []),
     "decompress_aggregate_shared": (_c.c_int, [_P, _c.c_int, _c.c_int32, _P, _P, _c.c_int, _P, _P, _c.c_size_t,
                                                _P]),
     "ef_dense_average": (_c.c_int, [_P, _c.c_int32, _P, _c.c_int, _P, _P]),
@@ -302,6 +304,15 @@ def decompress_aggregate(layout, msg_kind, W, idx_or_start, val, out, ws=None, a
     _need(layout, ws, 0, _ANY, "ws", w, optional=True)
     _check(_lib.decompress_aggregate(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
                                      1 if average else 0, _ptr(out), _ptr(ws), _nbytes(ws), _stream(out, stream)), w)
+
+
+def decompress_aggregate_noalloc(layout, msg_kind, W, idx_or_start, val, out, average=True, stream=None):
+    """decompress_aggregate with its scratch in the library's static device array (no workspace)."""
+    w = "decompress_aggregate_noalloc"
+    _agg_args(layout, msg_kind, W, idx_or_start, val, w)
+    _need(layout, out, layout.d, _F32, "out", w)
+    _check(_lib.decompress_aggregate_noalloc(layout.handle, int(msg_kind), int(W), _ptr(idx_or_start), _ptr(val),
+                                             1 if average else 0, _ptr(out), _stream(out, stream)), w)
 
 
 def decompress_aggregate_apply(layout, msg_kind, W, idx_or_start, val, x, mom=None, beta=0.0, wd=0.0, out=None,

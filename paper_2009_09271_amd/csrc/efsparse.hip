@@ -19,6 +19,13 @@
 
 using namespace efs;
 
+// Scratch of decompress_aggregate_noalloc, for callers that cannot allocate device memory: the
+// sparse aggregate's tile-range table.  Every device the library runs on holds its own copy until
+// the process ends.  In host code this name only stands in for the device array: kernels and copies
+// take the device address resolved by scratch_on(), never the name itself.
+constexpr size_t kNoAllocScratch = (size_t)16 << 20;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratch];
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -993,9 +1000,52 @@ int run_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m
   return EF_EINVAL;
 }
 
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The address of `scratch` on device dev, resolved once per device with that device current.
+int scratch_on(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return EF_ERANGE;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    EF_TRY(hip_status(hipGetDevice(&cur)));
+    if (cur != dev) EF_TRY(hip_status(hipSetDevice(dev)));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    EF_TRY(hip_status(e));
+    if (!p) return EF_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return EF_OK;
+}
+
 }  // namespace
 
 extern "C" {
+
+size_t ef_noalloc_scratch_bytes(void) { return kNoAllocScratch; }
+
+int decompress_aggregate_noalloc(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
+                                 int average, float* out, void* stream) {
+  EF_TRY(check_bound(L));
+  if (W < 1 || W > 65535) return EF_ERANGE;
+  if (!word_ok(m) || !word_ok(val) || !vec_ok(out)) return EF_EINVAL;
+  if (msg_kind != EF_MSG_SPARSE && msg_kind != EF_MSG_BLOCK) return EF_EINVAL;
+  if (ef_workspace_bytes(L, msg_kind == EF_MSG_SPARSE ? EF_OP_AGG_SPARSE : EF_OP_AGG_BLOCK, W) > kNoAllocScratch)
+    return EF_EWORKSPACE;
+  hipStream_t st = S(stream);
+  int dev = 0;
+  if (st) EF_TRY(hip_status(hipStreamGetDevice(st, &dev)));
+  else EF_TRY(hip_status(hipGetDevice(&dev)));
+  void* ws = nullptr;
+  EF_TRY(scratch_on(dev, &ws));
+  const AggOut O{out, nullptr, nullptr, 0.0f, 0.0f, W, average ? 1 : 0};
+  return run_aggregate(L, msg_kind, W, m, val, O, ws, kNoAllocScratch, st);
+}
 
 int decompress_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m, const float* val,
                          int average, float* out, void* ws, size_t ws_bytes, void* stream) {
