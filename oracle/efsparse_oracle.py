@@ -123,12 +123,17 @@ def compress_topk(acc, seg_offsets, ks):
 # ----------------------------------------------------------------------------
 # Section 3, random-k sparsification: keep k entries chosen at random.
 # ----------------------------------------------------------------------------
-def randk_keys(n: int, l: int, seed: int, step: int) -> np.ndarray:
-    """Random keys u_j, j = 0..n-1, of segment l."""
-    c = np.arange((n + 3) // 4, dtype=np.uint64)
+def randk_keys(n: int, l: int, seed: int, step: int, j0: int = 0, j1=None) -> np.ndarray:
+    """Random keys u_j of segment l (n elements) for the local positions j = j0..j1-1 (default: the
+    whole segment).  A range evaluates the same definition on part of the segment, so that a very
+    large segment can be checked piece by piece."""
+    j1 = n if j1 is None else int(j1)
+    assert 0 <= j0 <= j1 <= n
+    b0 = j0 // 4
+    c = np.arange(b0, (j1 + 3) // 4, dtype=np.uint64)
     x = philox4x32_10(c & np.uint64(0xFFFFFFFF), c >> np.uint64(32), np.uint64(step & 0xFFFFFFFF),
                       np.uint64(RANDK_TAG | l), seed & 0xFFFFFFFF, seed >> 32)
-    return np.stack(x, axis=1).reshape(-1)[:n]
+    return np.stack(x, axis=1).reshape(-1)[j0 - 4 * b0:j1 - 4 * b0]
 
 
 def randk_support(seg_offsets, ks, seed: int, step: int):

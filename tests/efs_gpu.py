@@ -169,6 +169,87 @@ def certify_randk(acc, offs, ks, idx, val, e_new, seed, step, where="randk"):
             assert tie_sent.max() < tie_unsent.min(), f"{where} seg {l}: ties must go to lower indices"
 
 
+# ---- the same certificates, piece by piece (for segments of up to 1e9 elements) -----------------
+# A segment's sent set S (k sorted distinct positions) is the definition's answer exactly when its
+# worst member beats the best position outside it under the selection order (score descending,
+# then index ascending).  Each piece of positions gives its worst sent and best unsent (score,
+# -index) pair; the pieces run on host threads (NumPy releases the interpreter lock in its loops).
+
+def _piece(S, a, b, score):
+    sc = score(a, b)
+    sel = np.zeros(b - a, dtype=bool)
+    lo, hi = np.searchsorted(S, [a, b])
+    sel[S[lo:hi] - a] = True
+    worst = best = None
+    if hi > lo:
+        m = sc[sel].min()
+        worst = (int(m), -int(np.nonzero(sel & (sc == m))[0].max() + a))
+    uns = ~sel
+    if uns.any():
+        M = sc[uns].max()
+        best = (int(M), -int(np.nonzero(uns & (sc == M))[0].min() + a))
+    return worst, best
+
+
+def order_certificate(S, n, k, score, where, chunk=1 << 24, threads=8):
+    """S: sent local positions of a segment of n elements; score(a, b): uint32 scores of positions
+    a..b-1 (larger is better).  Asserts |S| = k, S sorted, distinct and inside the segment, and that
+    every sent position beats every unsent one (equal scores: the lower index wins)."""
+    from concurrent.futures import ThreadPoolExecutor
+    S = np.asarray(S, dtype=np.int64)
+    assert S.size == k and S.min() >= 0 and S.max() < n and np.all(np.diff(S) > 0), f"{where}: support"
+    bounds = [(a, min(n, a + chunk)) for a in range(0, n, chunk)]
+    with ThreadPoolExecutor(max(1, min(threads, len(bounds)))) as ex:
+        parts = list(ex.map(lambda ab: _piece(S, ab[0], ab[1], score), bounds))
+    worst = min(p[0] for p in parts if p[0] is not None)
+    bests = [p[1] for p in parts if p[1] is not None]
+    if bests:
+        best = max(bests)
+        assert worst > best, f"{where}: an unsent position {-best[1]} (score {best[0]}) beats the sent " \
+                             f"position {-worst[1]} (score {worst[0]})"
+
+
+def certify_topk_chunked(acc, offs, ks, idx, val, e_new, where="topk", chunk=1 << 24):
+    """certify_topk piece by piece: score = magnitude key."""
+    idx = _check_message_and_residual(acc, idx, val, e_new, where)
+    P = 0
+    for l, k in enumerate(ks):
+        o, n = offs[l], offs[l + 1] - offs[l]
+        S = idx[P:P + k] - o
+        P += k
+        order_certificate(S, n, k, lambda a, b: acc[o + a:o + b].view(np.uint32) & np.uint32(0x7FFFFFFF),
+                          f"{where} seg {l}", chunk)
+
+
+def certify_randk_chunked(acc, offs, ks, idx, val, e_new, seed, step, where="randk", chunk=1 << 24):
+    """certify_randk piece by piece, the oracle's keys computed per range: score = complement of
+    the Philox key (smaller keys are better)."""
+    idx = _check_message_and_residual(acc, idx, val, e_new, where)
+    P = 0
+    for l, k in enumerate(ks):
+        o, n = offs[l], offs[l + 1] - offs[l]
+        S = idx[P:P + k] - o
+        P += k
+        order_certificate(S, n, k, lambda a, b: ~O.randk_keys(n, l, seed, step, a, b), f"{where} seg {l}", chunk)
+
+
+def topk_shaped_messages(grads, offs, ks):
+    """Sparse messages with top-k's shape (each worker's largest magnitudes per segment, ascending
+    indices; ties in any order), from the workers' gradients.  Test inputs only."""
+    idx, val = [], []
+    for g in grads:
+        key = g.view(np.uint32) & np.uint32(0x7FFFFFFF)
+        sup = []
+        for l, k in enumerate(ks):
+            o, n = offs[l], offs[l + 1] - offs[l]
+            part = np.argpartition(key[o:o + n], n - k)[n - k:] if k < n else np.arange(n)
+            sup.append(np.sort(part) + o)
+        s = np.concatenate(sup).astype(np.uint32)
+        idx.append(s)
+        val.append(g[s.astype(np.int64)])
+    return np.stack(idx), np.stack(val).astype(np.float32)
+
+
 def synthetic_sparse_messages(d, K, W, seed):
     """W messages of K ascending distinct indices with random values (seeded; message shape only)."""
     rng = np.random.default_rng(seed)

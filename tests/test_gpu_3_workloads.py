@@ -6,15 +6,18 @@
   consecutive steps with the residual carried, bit-exact against the oracle, and the aggregate of
   16 full-size messages;
 * the BERT shape (1.1e8 elements) and the 1e9-element flat case: exact certificates of the top-k
-  and random-k definitions (the sent set is unique, and the certificate accepts it and no other),
-  the block-random-k step against the oracle, and the aggregate of 32 messages.
+  and random-k definitions (the sent set is unique, and the certificate accepts it and no other)
+  over the densities of the workloads, the block-random-k step against the oracle, and the
+  aggregates of 32 messages;
+* the ResNet-50 flat case over all 10 steps with the residual carried, and aggregates of 16
+  messages of top-k's shape taken from the workers' own gradients.
 """
 
 import numpy as np
 import pytest
 
-from efs_gpu import (Case, announce, assert_f32_equal, assert_msg_equal, certify_randk, certify_topk, dev, host,
-                     synthetic_sparse_messages)
+from efs_gpu import (Case, announce, assert_f32_equal, assert_msg_equal, certify_randk, certify_randk_chunked,
+                     certify_topk, certify_topk_chunked, dev, host, synthetic_sparse_messages, topk_shaped_messages)
 from oracle import efsparse_oracle as O
 from workloads import WORKLOADS, gradient, to_bf16_bits, worker_seed
 
@@ -142,38 +145,102 @@ def test_bert_full_size(bert_g, scope, density, kind):
         certify_randk(acc, c.offs, c.ks, host(m), host(val), host(ed), seed, 0, f"bert {scope} {density}")
 
 
+@pytest.mark.parametrize("scope", ["layer", "flat"])
+def test_bert_randk_10_percent(bert_g, scope):
+    """Random-k at the densest BERT setting (K = 10.9 M): the exact certificate of the definition."""
+    wl = WORKLOADS["bert"]
+    announce("bert randk 10%", scope)
+    c = Case(wl.seg_offsets(scope), 0.1)
+    e = np.zeros(c.d, np.float32)
+    ed = dev(e)
+    seed = worker_seed(wl, 0)
+    m, val, _ = c.step("randk", bert_g, ed, seed, 0)
+    acc = O.ef_accumulate(bert_g, e)
+    certify_randk_chunked(acc, c.offs, c.ks, host(m), host(val), host(ed), seed, 0, f"bert {scope} 10%")
+
+
+def _grads(wl, W, t=0):
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(8) as ex:
+        return list(ex.map(lambda w: gradient(wl, w, t), range(W)))
+
+
+@pytest.mark.parametrize("wname,scope,density", [("resnet50", "flat", 0.001), ("resnet50", "layer", 0.001),
+                                                 ("bert", "flat", 0.01)])
+def test_aggregate_16_topk_shaped_messages(wname, scope, density):
+    """The aggregate of the 16 workers' messages of top-k's shape (crowded into the layers of largest
+    magnitude), taken from the workers' own gradients, against the oracle."""
+    wl = WORKLOADS[wname]
+    announce("aggregate of 16 top-k-shaped messages", wname, scope, density)
+    c = Case(wl.seg_offsets(scope), density)
+    idx, val = topk_shaped_messages(_grads(wl, 16), c.offs, c.ks)
+    _agg(c, "sparse", list(zip(idx, val)), 16)
+
+
+@pytest.mark.parametrize("kind,block", [("topk", 1), ("randk", 1), ("randblock", 4096)])
+def test_resnet50_flat_ef_carried_ten_steps(kind, block):
+    """Worker 0 over the workload's 10 steps, the residual carried from step to step."""
+    wl = WORKLOADS["resnet50"]
+    announce("resnet50 flat, 10 steps", kind, block)
+    c = Case(wl.seg_offsets("flat"), wl.densities[0], block)
+    _steps(c, wl, kind, workers=[0], steps=list(range(wl.steps)), block=block)
+
+
 @pytest.fixture(scope="module")
 def flat1g_g():
     return gradient(WORKLOADS["flat1g"], 0, 0)
 
 
-@pytest.mark.parametrize("case", ["topk-f32-0.01%", "topk-bf16-1%", "randblock-f32-1%-b2^20", "aggregate-W32-0.01%"])
+FLAT1G_CASES = ["topk-f32-0.01%", "topk-f32-0.1%", "topk-f32-10%", "topk-bf16-1%",
+                "randk-f32-0.01%", "randk-f32-1%", "randk-bf16-1%",
+                "randblock-f32-1%-b2^20", "randblock-bf16-1%-b2^8",
+                "aggregate-W32-0.01%", "block-aggregate-W32-0.1%-b2^12"]
+
+
+@pytest.mark.parametrize("case", FLAT1G_CASES)
 def test_flat1g(flat1g_g, case):
-    """1e9 elements: top-k by certificate (fp32 and bf16 gradients), block-random-k against the
-    oracle, and the aggregate of 32 messages against the oracle."""
+    """1e9 elements: top-k and random-k by exact certificates checked piece by piece (fp32 and bf16
+    gradients), block-random-k against the oracle, and the sparse and block aggregates of 32
+    messages against the oracle."""
     wl = WORKLOADS["flat1g"]
     announce("flat1g", case)
     offs = wl.seg_offsets("flat")
     g = flat1g_g
-    if case.startswith("topk"):
-        density = 0.0001 if "0.01%" in case else 0.01
+    parts = case.split("-")
+    pct = {"0.01%": 1e-4, "0.1%": 1e-3, "1%": 1e-2, "10%": 1e-1}
+    density = pct.get(parts[2]) if len(parts) > 2 else None
+    if parts[0] in ("topk", "randk"):
+        kind = parts[0]
         c = Case(offs, density)
-        gi = to_bf16_bits(g) if "bf16" in case else g
+        gi = to_bf16_bits(g) if parts[1] == "bf16" else g
         e = np.zeros(c.d, np.float32)
         ed = dev(e)
-        m, val, _ = c.step("topk", gi, ed)
+        seed = worker_seed(wl, 0)
+        m, val, _ = c.step(kind, gi, ed, seed, 0)
         acc = O.ef_accumulate(gi, e)
         del e
-        certify_topk(acc, c.offs, c.ks, host(m), host(val), host(ed), f"flat1g {case}")
-    elif case.startswith("randblock"):
-        c = Case(offs, 0.01, 1 << 20)
+        if kind == "topk":
+            certify_topk_chunked(acc, c.offs, c.ks, host(m), host(val), host(ed), f"flat1g {case}")
+        else:
+            certify_randk_chunked(acc, c.offs, c.ks, host(m), host(val), host(ed), seed, 0, f"flat1g {case}")
+    elif parts[0] == "randblock":
+        b = 1 << int(parts[3][3:])
+        c = Case(offs, density, b)
+        gi = to_bf16_bits(g) if parts[1] == "bf16" else g
         e = np.zeros(c.d, np.float32)
         ed = dev(e)
-        st, val, _ = c.step("randblock", g, ed, worker_seed(wl, 0), 0)
-        (wst, wval), we = c.oracle_step("randblock", g, e, worker_seed(wl, 0), 0)
-        assert_msg_equal("randblock", (st, val), (wst, wval), "flat1g randblock")
-        assert_f32_equal(ed, we, "flat1g randblock e'")
-    else:
+        st, val, _ = c.step("randblock", gi, ed, worker_seed(wl, 0), 0)
+        (wst, wval), we = c.oracle_step("randblock", gi, e, worker_seed(wl, 0), 0)
+        assert_msg_equal("randblock", (st, val), (wst, wval), f"flat1g {case}")
+        assert_f32_equal(ed, we, f"flat1g {case} e'")
+    elif parts[0] == "aggregate":
         c = Case(offs, 0.0001)
         idx, val = synthetic_sparse_messages(c.d, c.K, wl.W, 78)
         _agg(c, "sparse", list(zip(idx, val)), wl.W)
+    else:  # the block aggregate of 32 workers' messages: their own random starts, synthetic values
+        b = 1 << 12
+        c = Case(offs, 0.001, b)
+        rng = np.random.default_rng(79)
+        msgs = [(np.array([O.randblock_start(c.d, 0, b, worker_seed(wl, w), 0)], dtype=np.uint32),
+                 rng.standard_normal(c.K).astype(np.float32)) for w in range(wl.W)]
+        _agg(c, "block", msgs, wl.W)

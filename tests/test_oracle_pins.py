@@ -215,6 +215,25 @@ def test_randk_key_mapping_matches_independent_philox():
             assert int(u[j]) == w[j & 3]
 
 
+def test_randk_key_ranges_match_independent_philox():
+    """Keys of a position range (the form the certificates of 1e9-element segments use) at offsets
+    far into a segment, including ranges that start and end inside a Philox block, against ATen;
+    and every range of a small segment equals the same slice of the whole-segment call."""
+    seed, step, n = (4 << 32) | 5, 3, 1_000_000_000
+    for l, j0, m in ((0, 999_999_963, 37), (0, 123_456_789, 11), (2, 536_870_910, 9)):
+        u = O.randk_keys(n, l, seed, step, j0, j0 + m)
+        assert u.shape == (m,)
+        sub = step | ((O.RANDK_TAG | l) << 32)
+        want = _aten([(seed, sub, j >> 2) for j in range(j0, j0 + m)])
+        for t, w in enumerate(want):
+            assert int(u[t]) == w[(j0 + t) & 3]
+    full = O.randk_keys(1001, 6, seed, step)
+    rng = np.random.default_rng(11)
+    for _ in range(50):
+        a, b = sorted(int(v) for v in rng.integers(0, 1002, 2))
+        assert np.array_equal(O.randk_keys(1001, 6, seed, step, a, b), full[a:b])
+
+
 def test_randblock_start_matches_independent_philox():
     seed = (2 << 32) | 3
     for l, n, b in ((0, 25557032, 4096), (7, 1000, 256), (3, 64, 256), (1, 10, 2)):
