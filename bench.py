@@ -339,6 +339,145 @@ def _cpu_baseline(O, wl, offs, ks, variants, W, grads, budget_note, min_s=10.0):
     }
 
 
+def flat1g_gradient(torch, wl, w, out, gen, chunk=1 << 27):
+    """Worker w's 1e9-element gradient drawn on the device (the host would need 4 GB and tens of
+    seconds per worker): per element N(0, 1e-4) with probability 0.99, else N(0, 1e-1) (variances),
+    from a torch generator seeded with (cfg_id << 32) | w.  Timing input only: parity tests use the
+    host generator."""
+    gen.manual_seed((wl.cfg_id << 32) | w)
+    for a in range(0, out.numel(), chunk):
+        part = out[a:a + chunk]
+        torch.randn(part.shape, generator=gen, device=out.device, out=part)
+        wide = torch.rand(part.shape, generator=gen, device=out.device) < 0.01
+        part.mul_(torch.where(wide, 0.1 ** 0.5, 1e-4 ** 0.5))
+
+
+def measure_flat1g(args, E, torch, dev, reps=20):
+    """The 1e9-element flat workload: for every density of the workload, one worker's fused step
+    of each compressor (fp32 and bf16 gradient) and the aggregate of W = 32 workers' messages; for
+    the block sizes 2^8 ... 2^20 at 1 %, the block-random-k step and its aggregate.  Messages come
+    from 32 workers' own gradients (drawn on the device one after another); the timed steps use
+    worker 0's gradient.  Back-to-back repetitions on one stream, timed with events."""
+    from workloads import WORKLOADS, worker_seed
+    wl = WORKLOADS["flat1g"]
+    d, W = wl.d, args.workers or wl.W
+    st = torch.cuda.Stream(dev)
+    gen = torch.Generator(device=dev)
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(st):
+            for _ in range(3):
+                fn()
+            a.record(st)
+            for _ in range(reps):
+                fn()
+            b.record(st)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    def split(fn):
+        E.timing_collect(reset=True)
+        E.timing_enable(True)
+        with torch.cuda.stream(st):
+            fn()
+        torch.cuda.synchronize()
+        E.timing_enable(False)
+        return {n: round(t * 1e3 / c, 3) for n, (t, c) in E.timing_collect(reset=True).items()}
+
+    def entry(us, alg):
+        return {"us": round(us, 3), "elements_per_s": d / (us * 1e-6), "alg_bytes": int(alg),
+                "frac_of_hbm_peak": round(alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+
+    g0 = torch.empty(d, dtype=torch.float32, device=dev)
+    flat1g_gradient(torch, wl, 0, g0, gen)
+    gb = g0.to(torch.bfloat16)
+    gw = torch.empty(d, dtype=torch.float32, device=dev)
+    e = torch.zeros(d, dtype=torch.float32, device=dev)
+    out = torch.empty(d, dtype=torch.float32, device=dev)
+    seeds = [worker_seed(wl, w) for w in range(W)]
+
+    def run_variant(kind, density, block):
+        lay = E.Layout(d, [0, d], density, block).bind(dev)
+        K, L = lay.K, lay.n_seg
+        blk = kind == "randblock"
+        op = E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK
+        ws = None if blk else lay.workspace(op, 1, dev)
+        mi = torch.empty((W, L if blk else K), dtype=torch.int32, device=dev)
+        mv = torch.empty((W, K), dtype=torch.float32, device=dev)
+
+        def step(g, w=0):
+            if kind == "topk":
+                E.ef_step_topk(lay, g, e, mi[w], mv[w], ws)
+            elif kind == "randk":
+                E.ef_step_randk(lay, g, e, seeds[w], 0, mi[w], mv[w], ws)
+            else:
+                E.ef_step_randblock(lay, g, e, seeds[w], 0, mi[w], mv[w])
+
+        for w in range(W):  # the workers' messages, each from its own gradient and a zero residual
+            flat1g_gradient(torch, wl, w, gw, gen)
+            e.zero_()
+            with torch.cuda.stream(st):
+                step(gw, w)
+        torch.cuda.synchronize()
+        step_b, agg_b = alg_bytes_op(kind, d, K, L, W)
+        ws_a = None if blk else lay.workspace(E.EF_OP_AGG_SPARSE, W, dev)
+        kindm = E.EF_MSG_BLOCK if blk else E.EF_MSG_SPARSE
+        agg = lambda: E.decompress_aggregate(lay, kindm, W, mi, mv, out, ws_a)  # noqa: E731
+        r = {"K": K, "aggregate": entry(timed(agg), agg_b)}
+        r["aggregate"]["kernels_us"] = split(agg)
+        e.zero_()
+        r["fused_step"] = entry(timed(lambda: step(g0)), step_b)
+        r["fused_step"]["kernels_us"] = split(lambda: step(g0))
+        e.zero_()
+        r["fused_step_bf16_gradient"] = entry(timed(lambda: step(gb)), step_b - 2 * d)
+        if ws is not None:
+            r["fused_step"]["diag"] = lay.diag(ws, op)
+        del ws, ws_a, mi, mv
+        return r
+
+    res = {"densities": {}, "blocks_at_1pct": {}}
+    for density in wl.densities:
+        _note(f"flat1g: density {density}")
+        res["densities"][str(density)] = {f"{k}{b if k == 'randblock' else ''}": run_variant(k, density, b)
+                                          for k, b in (("topk", 1), ("randk", 1), ("randblock", 4096))}
+    for s in range(8, 21, 2):
+        _note(f"flat1g: block 2^{s}")
+        res["blocks_at_1pct"][f"2^{s}"] = run_variant("randblock", 0.01, 1 << s)
+    cpu = None
+    if not args.no_cpu_baseline:
+        _note("CPU oracle sample (1e7 elements of the same distribution)")
+        cpu = flat1g_cpu_sample(wl)
+    line = {"metric": METRIC, "n_gpus": 1, "unit": "elements/s", "higher_is_better": True, "dtype": "f32",
+            "data": "synthetic (drawn on the device)",
+            "config": {"workload": f"flat1g: flat 1e9-element fp32 / bf16 gradients, densities "
+                                   f"{list(wl.densities)}, block sizes 2^8..2^20, W={W} messages aggregated",
+                       "d": d, "W": W},
+            "flat1g": res, "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
+def flat1g_cpu_sample(wl, n=10_000_000, density=0.01):
+    """The oracle's worker step per compressor on a 1e7-element slice of the same distribution, one
+    core (the full 1e9-element sort would take minutes per step)."""
+    from oracle import efsparse_oracle as O
+    from threadpoolctl import threadpool_limits
+    from workloads import worker_seed
+    rng = np.random.default_rng([wl.cfg_id, 0, 0])
+    g = (rng.standard_normal(n) * np.where(rng.random(n) < 0.01, 0.1 ** 0.5, 1e-4 ** 0.5)).astype(np.float32)
+    e0 = np.zeros(n, np.float32)
+    offs = [0, n]
+    ks = O.segment_ks(offs, density)
+    out = {}
+    with threadpool_limits(1):
+        for kind, b in (("topk", 1), ("randk", 1), ("randblock", 4096)):
+            t0 = time.perf_counter()
+            O.ef_step(kind, g, e0, offs, ks, seed=worker_seed(wl, 0), step=0, block=b)
+            out[kind] = {"s": round(time.perf_counter() - t0, 3), "elements_per_s": n / (time.perf_counter() - t0)}
+    return {"kind": "oracle", "cores": 1, "sample": f"one worker step per compressor on {n} elements at "
+            f"density {density}, NumPy, 1 thread", "per_compressor": out, "host": host_description()}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -373,6 +512,13 @@ def main():
               "(the library has no multi-GPU path; the value is one GPU's share of the data-parallel step).",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "flat1g":  # 4 GB per array: a sweep of one-worker steps and 32-worker aggregates
+        import torch
+        import paper_2009_09271_amd as E
+        dev = torch.device("cuda", 0)
+        torch.cuda.set_device(dev)
+        return measure_flat1g(args, E, torch, dev)
 
     from workloads import WORKLOADS, worker_seed
     wl = WORKLOADS[args.workload]

@@ -17,10 +17,13 @@ constexpr int kResWords = 16;                // per-segment selection record (ui
 constexpr int kSubLists = 16;                // a segment's list of undecided candidates is kept as 16
                                               // sub-lists (row r appends to sub-list r % 16)
 constexpr int kSampleMax = 32768;             // top-k threshold sample size (keys held in LDS)
-constexpr int kSampleRun = 256;               // contiguous elements per sample run
+constexpr int kSampleRun = 256;               // samples per sample run (one workgroup each)
+constexpr int kSampleTotal = 16384;           // top-k: samples shared by a layout's sampled segments
+constexpr int kSampleMinRuns = 4;             // top-k: at least this many runs per sampled segment
 
 constexpr uint32_t kRandkTag = 0x01000000u;
 constexpr uint32_t kRandblockTag = 0x02000000u;
+constexpr uint32_t kSampleTag = 0x03000000u;  // top-k: positions of the threshold sample
 
 constexpr uint32_t kDiagSlowPath = 2u;
 

@@ -1075,10 +1075,16 @@ __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t 
 // Top-k sample
 // ---------------------------------------------------------------------------------------------
 // One workgroup of kSampleRun threads per run: a segment of up to kSampleMax elements is sampled
-// whole (runs of consecutive positions), a larger one by kSampleMax / kSampleRun runs of
-// kSampleRun contiguous elements evenly spread over it.  The runs of a sampled segment also clear
-// its candidate histogram (kHCopies * kHBins = kSampleMax words, one slice per run).
-static_assert(kHCopies * kHBins == kSampleMax, "one histogram slice per sample run");
+// whole (runs of consecutive positions).  A larger one, given s = runs * kSampleRun samples by the
+// layout (a share of kSampleTotal in proportion to its size, at least kSampleMinRuns runs), is
+// split into s strata of equal length (to within one element) and sampled once in each, at a
+// pseudo-random position inside the stratum (stratified sampling): every part of the segment, a
+// small tensor of large values inside a flat gradient included, is represented in proportion to
+// its size, and the count of sampled keys above a value varies no more than a simple random
+// sample's would (runs of contiguous elements, by contrast, sample a handful of clusters: a small
+// tensor is either missed or over-represented many times).  Sample q = run * kSampleRun + thread;
+// the runs of a sampled segment also clear its candidate histogram (kHCopies * kHBins words).
+static_assert(kHCopies * kHBins == kSampleMax, "a sampled segment's histogram is cleared by its samples");
 constexpr int kSampleKeysPer = kSampleMax / kSelNT;  // sample keys per thread, loaded in one round trip
 static_assert(2 * kRankList <= kHBins, "the ranked entries of an exact segment fit a histogram array");
 
@@ -1107,9 +1113,13 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
     in = j < n;
     i = o + j;
   } else {
-    constexpr uint32_t runs = kSampleMax / kSampleRun;
-    i = o + (uint32_t)(((uint64_t)q * (n - kSampleRun)) / (runs - 1)) + threadIdx.x;
-    ws.hist[(size_t)l * kHCopies * kHBins + q * kSampleRun + threadIdx.x] = 0u;
+    const uint32_t ns = ((uint32_t)T.seg_ro[l + 1] - (uint32_t)T.seg_ro[l]) * kSampleRun;  // samples
+    const uint32_t sq = q * kSampleRun + threadIdx.x;  // the stratum
+    const uint32_t a = (uint32_t)(((uint64_t)sq * n) / ns);
+    const uint32_t b = (uint32_t)(((uint64_t)(sq + 1u) * n) / ns);
+    const uint32_t x = philox(make_uint4(sq, 0u, 0u, kSampleTag | (uint32_t)l), 0u, 0u).x;
+    i = o + a + __umulhi(x, b - a);  // uniform in [a, b): b > a because n > kSampleMax >= ns
+    for (uint32_t h = sq; h < (uint32_t)(kHCopies * kHBins); h += ns) ws.hist[(size_t)l * kHCopies * kHBins + h] = 0u;
   }
   uint32_t key = 0;
   if (in) {
@@ -1165,10 +1175,11 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
     return;
   }
   // sampled: bins of the top 11 key bits (8 exponent + 3 mantissa bits); keys stay in registers
+  const uint32_t ns = ((uint32_t)T.seg_ro[l + 1] - (uint32_t)T.seg_ro[l]) * kSampleRun;  // samples
   for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
   __syncthreads();
   uint32_t kmax = 0u;
-  for_keys<kSampleKeysPer>(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+  for_keys<kSampleKeysPer>(sk, ns, [&](uint32_t, uint32_t k) {
     atomicAdd(&hist[k >> 20], 1u);
     kmax = max(kmax, k);
   });
@@ -1180,10 +1191,10 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
     uint32_t above;
     const int bin = block_resolve<kSelNT>(hist, kHBins, rank, lds, above);
     if (bin < 0) return 0u;
-    if (hist[bin] <= (uint32_t)kSampleMax / 8) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
+    if (hist[bin] <= ns / 8) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
     for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist2[b] = 0;
     __syncthreads();
-    for_keys(sk, (uint32_t)kSampleMax, [&](uint32_t, uint32_t k) {
+    for_keys(sk, ns, [&](uint32_t, uint32_t k) {
       if ((k >> 20) == (uint32_t)bin) atomicAdd(&hist2[(k >> 9) & (kHBins - 1)], 1u);
     });
     __syncthreads();
@@ -1193,7 +1204,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   };
   const uint32_t rank = (uint32_t)T.seg_srank[l], urank = (uint32_t)T.seg_urank[l];
   // rank >= sample size: every element is a candidate
-  const uint32_t thr = rank < (uint32_t)kSampleMax ? rank_edge(rank, false) : 0u;
+  const uint32_t thr = rank < ns ? rank_edge(rank, false) : 0u;
   // the bins resolve the range up to the upper edge of where the k-th key very likely lies
   uint32_t top = rank_edge(urank, true);
   if (top <= thr || top > kmax) top = kmax;

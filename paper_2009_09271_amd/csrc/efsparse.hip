@@ -98,6 +98,11 @@ void ef_layout::build() {
   cbase.assign(n + 1, 0);
   ro.assign(n + 1, 0);
   all_exact = true;
+  // top-k threshold sample: segments of more than kSampleMax elements share kSampleTotal samples in
+  // proportion to their sizes (at least kSampleMinRuns runs each, at most kSampleMax samples)
+  double dbig = 0.0;
+  for (int l = 0; l < n; ++l)
+    if (off64[l + 1] - off64[l] > kSampleMax) dbig += (double)(off64[l + 1] - off64[l]);
   for (int l = 0; l < n; ++l) {
     const int64_t dl = off64[l + 1] - off64[l];
     // k per segment: round-half-up of density * d_l in double, clamped to [1, d_l]
@@ -108,13 +113,20 @@ void ef_layout::build() {
     const int64_t b = dl > block ? block : 1;
     bl[l] = (int32_t)b;
     nb[l] = (int32_t)((dl + b - 1) / b);
-    // top-k: rank of the candidate threshold inside a sample of kSampleMax keys, so that the
+    // top-k sample runs: the whole segment when it fits the sample, else its share of kSampleTotal
+    int64_t runs = (dl + kSampleRun - 1) / kSampleRun;
+    if (dl > kSampleMax) {
+      const double want = std::ceil((double)kSampleTotal * (double)dl / dbig / kSampleRun);
+      runs = (int64_t)std::min<double>(std::max<double>(want, kSampleMinRuns), kSampleMax / kSampleRun);
+    }
+    const double ns = (double)(runs * kSampleRun);
+    // top-k: rank of the candidate threshold inside the segment's sample of ns keys, so that the
     // expected sample count above the true threshold plus tk_sigma standard deviations is covered
-    const double mus = (double)kSampleMax * (double)kl / (double)dl;
+    const double mus = ns * (double)kl / (double)dl;
     const double rs = std::ceil(mus + tk_sigma * std::sqrt(mus) + tk_extra);
-    srank[l] = (int32_t)std::min<double>(std::max<double>(rs, 1.0), (double)kSampleMax);
+    srank[l] = (int32_t)std::min<double>(std::max<double>(rs, 1.0), ns);
     const double ru = std::floor(mus - tk_sigma * std::sqrt(mus));
-    urank[l] = (int32_t)std::min<double>(std::max<double>(ru, 1.0), (double)kSampleMax);
+    urank[l] = (int32_t)std::min<double>(std::max<double>(ru, 1.0), ns);
     // random-k: keys below tau are candidates; expected count k + sigma * sqrt(k) + extra
     const double mu = (double)kl + rk_sigma * std::sqrt((double)kl) + rk_extra;
     const double p = mu / (double)dl;
@@ -133,8 +145,6 @@ void ef_layout::build() {
     // rows: one per data tile the segment touches
     const int64_t c0 = off64[l] / kTile, c1 = (off64[l + 1] - 1) / kTile;
     cbase[l + 1] = cbase[l] + (int32_t)(c1 - c0 + 1);
-    // top-k sample runs: the whole segment when it fits the sample, else kSampleMax / kSampleRun
-    const int64_t runs = dl <= kSampleMax ? (dl + kSampleRun - 1) / kSampleRun : kSampleMax / kSampleRun;
     ro[l + 1] = ro[l] + (int32_t)runs;
     if (dl > kSampleMax) all_exact = false;
   }

@@ -113,6 +113,51 @@ def test_resnet50_aggregate_16_workers(scope):
     _agg(c, "sparse", list(zip(idx, val)), wl.W)
 
 
+def _dominated(case):
+    """Worker 0's ResNet-50 gradient with parts of much larger magnitude than the rest: the cases
+    where a threshold sample that misses a small part would leave fewer than k candidates."""
+    from workloads import shapes
+    wl = WORKLOADS["resnet50"]
+    g = gradient(wl, 0, 0).astype(np.float64)
+    offs = wl.seg_offsets("layer")
+    names = [n for n, _ in wl.tensor_shapes]
+    rng = np.random.default_rng(2020)
+
+    def fill(name, scale):
+        i = names.index(name)
+        g[offs[i]:offs[i + 1]] = rng.laplace(0.0, scale, offs[i + 1] - offs[i])
+
+    if case in ("fc.bias", "both"):
+        fill("fc.bias", 0.05)
+    if case in ("conv1", "both"):
+        fill("conv1.weight", 0.03)
+    if case == "both":
+        fill("bn1.bias", 1.0)  # 64 elements
+    if case == "periodic":
+        g[::781] *= 100.0  # a stride close to the sample's strata
+    return g.astype(np.float32)
+
+
+@pytest.mark.parametrize("case", ["fc.bias", "conv1", "both", "periodic"])
+def test_topk_flat_with_a_dominant_small_tensor(case):
+    """Top-k over the flat ResNet-50 gradient when one small tensor (the 1000-element fc.bias at
+    Laplace scale 0.05, the stem convolution at 0.03, a 64-element bias at 1.0) or a periodic set of
+    elements holds values far above the rest: bit-exact against the oracle, and the candidates of
+    the threshold sample always contain the answer (the exact whole-segment path is not taken)."""
+    import paper_2009_09271_amd as E
+    wl = WORKLOADS["resnet50"]
+    announce("resnet50 flat top-k, dominated by", case)
+    c = Case(wl.seg_offsets("flat"), wl.densities[0])
+    g = _dominated(case)
+    e = np.zeros(c.d, np.float32)
+    ed = dev(e)
+    m, val, ws = c.step("topk", g, ed)
+    (wm, wval), we = c.oracle_step("topk", g, e)
+    assert_msg_equal("topk", (m, val), (wm, wval), f"dominated {case}")
+    assert_f32_equal(ed, we, f"dominated {case} e'")
+    assert c.L.diag(ws, E.EF_OP_TOPK) & E.DIAG_SLOW_PATH == 0, f"{case}: the exact whole-segment path ran"
+
+
 @pytest.fixture(scope="module")
 def bert_g():
     return gradient(WORKLOADS["bert"], 0, 0)
