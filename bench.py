@@ -347,8 +347,8 @@ def flat1g_gradient(torch, wl, w, out, gen, chunk=1 << 27):
     gen.manual_seed((wl.cfg_id << 32) | w)
     for a in range(0, out.numel(), chunk):
         part = out[a:a + chunk]
-        torch.randn(part.shape, generator=gen, device=out.device, out=part)
-        wide = torch.rand(part.shape, generator=gen, device=out.device) < 0.01
+        part.normal_(generator=gen)
+        wide = torch.empty_like(part).uniform_(generator=gen) < 0.01
         part.mul_(torch.where(wide, 0.1 ** 0.5, 1e-4 ** 0.5))
 
 
@@ -365,6 +365,7 @@ def measure_flat1g(args, E, torch, dev, reps=20):
     gen = torch.Generator(device=dev)
 
     def timed(fn):
+        torch.cuda.synchronize()  # work enqueued on other streams first
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         with torch.cuda.stream(st):
             for _ in range(3):
@@ -377,6 +378,7 @@ def measure_flat1g(args, E, torch, dev, reps=20):
         return a.elapsed_time(b) * 1e3 / reps
 
     def split(fn):
+        torch.cuda.synchronize()
         E.timing_collect(reset=True)
         E.timing_enable(True)
         with torch.cuda.stream(st):
@@ -415,10 +417,9 @@ def measure_flat1g(args, E, torch, dev, reps=20):
                 E.ef_step_randblock(lay, g, e, seeds[w], 0, mi[w], mv[w])
 
         for w in range(W):  # the workers' messages, each from its own gradient and a zero residual
-            flat1g_gradient(torch, wl, w, gw, gen)
+            flat1g_gradient(torch, wl, w, gw, gen)  # all on the current stream, in order
             e.zero_()
-            with torch.cuda.stream(st):
-                step(gw, w)
+            step(gw, w)
         torch.cuda.synchronize()
         step_b, agg_b = alg_bytes_op(kind, d, K, L, W)
         ws_a = None if blk else lay.workspace(E.EF_OP_AGG_SPARSE, W, dev)
