@@ -411,65 +411,109 @@ __device__ __forceinline__ float column_sum(const float* v, int32_t W, int32_t K
 }
 
 // tile_start[w * ts_stride + tau] = first entry of message w whose index lies in an aggregate tile
-// >= tau (tau = 0..nt; an index >= d counts as tile nt).  Grid: (ceil(K / kNT), W), one thread per
-// entry.
+// >= tau (tau = 0..nt; an index >= d counts as tile nt).  Grid: (gx, W); each thread takes U
+// entries at a time (coalesced, all loads in flight together) and the workgroups stride over the
+// message: U = 1 with a thread per entry for short messages (the quickest form: one round), U = 8
+// and a capped grid for long ones, so that 3.2e9 entries (32 messages of 1e8) do not need as many
+// threads (1e9 elements at 1 %: 692 -> 450 us; at 10 %: 6.8 -> 3.8 ms).
 // With `sums` (shared coordinates: W = 1 message whose values are vW workers' rows `vals`), entry
 // j's thread also writes sums[j], the column sum of the rows in worker order.
 // Entry j starts the tiles after its predecessor's tile, up to its own (past the last entry the
 // tiles up to nt start at K).  A short run of tiles is written by its entry's thread; a longer one
-// (a gap in a message crowded into a few layers) by the whole workgroup as one coalesced run.
+// (a gap in a message crowded into a few layers) by the whole workgroup as one coalesced run, after
+// each round (a thread writes its long run itself if the workgroup's list of them is full).
 // For ascending messages the entries' runs partition 0..nt.
-constexpr uint32_t kRunOwn = 128;  // runs of at most this many tiles are written by their own thread;
-                                   // longer ones (at most nt / 128 per message) by the workgroup
+constexpr uint32_t kRunOwn = 128;       // runs of at most this many tiles are written by their own thread
+constexpr int kRangeUBig = 8;           // entries per thread per round for long messages
+constexpr int64_t kRangeBig = 1 << 22;  // total entries (W K) from which the long form is used
+constexpr uint32_t kRangeStash = 512;   // long runs listed per workgroup and round
 
+template <int kRangeU>
 __global__ __launch_bounds__(kNT) void k_agg_ranges(int32_t d, int32_t K, int32_t nt, const uint32_t* idx,
                                                     uint32_t* tile_start, uint64_t ts_stride, const float* vals,
                                                     int32_t vW, float* sums) {
   __shared__ uint32_t s_nlong;
-  __shared__ uint32_t s_ta[kNT], s_n[kNT], s_j[kNT], s_own[kNT];  // the workgroup's long runs
-  const uint32_t j = blockIdx.x * kNT + threadIdx.x;
+  __shared__ uint32_t s_ta[kRangeStash], s_n[kRangeStash], s_j[kRangeStash], s_own[kRangeStash];
   const int w = blockIdx.y;
   const uint32_t* m = idx + (size_t)w * K;
   uint32_t* ts = tile_start + (size_t)w * ts_stride;
+  const size_t tbase = (size_t)w * ts_stride;
   auto tile = [&](uint32_t i) -> uint32_t { return i < (uint32_t)d ? i / kAggTile : (uint32_t)nt; };
   // tile tau of entry e's run starts at e, except past the last entry's own tile (at K)
   auto value = [&](uint32_t e, uint32_t tau, uint32_t e_own) -> uint32_t {
     return e == (uint32_t)K - 1u && tau > e_own ? (uint32_t)K : e;
   };
   if (threadIdx.x == 0) s_nlong = 0;
-  // shared coordinates (one message for vW workers): also the column sums of their values
-  if (sums && w == 0 && j < (uint32_t)K) sums[j] = column_sum(vals, vW, K, j);
   __syncthreads();
-  if (j < (uint32_t)K) {
-    const uint32_t own = tile(m[j]);
-    const uint32_t ta = j == 0 ? 0u : tile(m[j - 1]) + 1u;
-    const uint32_t tb = j == (uint32_t)K - 1u ? (uint32_t)nt : own;
-    const uint32_t n = tb + 1u > ta ? tb + 1u - ta : 0u;
-    if (n > kRunOwn) {
-      const uint32_t p = atomicAdd(&s_nlong, 1u);
-      s_ta[p] = ta;
-      s_n[p] = n;
-      s_j[p] = j;
-      s_own[p] = own;
-    } else {
-      for (uint32_t k = 0; k < n; ++k) ts[ta + k] = value(j, ta + k, own);
+  const uint32_t round = gridDim.x * (uint32_t)kNT * (uint32_t)kRangeU;
+  for (uint32_t j0 = blockIdx.x * (uint32_t)kNT * (uint32_t)kRangeU; j0 < (uint32_t)K; j0 += round) {
+    uint32_t cur[kRangeU], prv[kRangeU];
+#pragma unroll
+    for (int u = 0; u < kRangeU; ++u) {
+      const uint32_t j = j0 + (uint32_t)u * kNT + threadIdx.x;
+      cur[u] = j < (uint32_t)K ? m[j] : 0u;
+      prv[u] = j < (uint32_t)K && j > 0 ? m[j - 1] : 0u;
     }
-  }
-  __syncthreads();
-  for (uint32_t q = 0; q < s_nlong; ++q) {
-    const uint32_t qa = s_ta[q], qe = qa + s_n[q], qj = s_j[q], qown = s_own[q];
-    // 16-byte stores over the part of the run aligned in memory, single words at its two ends
-    const size_t base = (size_t)w * ts_stride;
-    const uint32_t a4 = min(qe, qa + (uint32_t)((4u - (base + qa) % 4u) % 4u));
-    const uint32_t b4 = a4 + (qe - a4) / 4u * 4u;
-    if (threadIdx.x < a4 - qa) ts[qa + threadIdx.x] = value(qj, qa + threadIdx.x, qown);
-    if (threadIdx.x < qe - b4) ts[b4 + threadIdx.x] = value(qj, b4 + threadIdx.x, qown);
-    for (uint32_t o = a4 + 4u * threadIdx.x; o < b4; o += 4u * kNT) {
-      const uint4 v = make_uint4(value(qj, o, qown), value(qj, o + 1, qown), value(qj, o + 2, qown),
-                                 value(qj, o + 3, qown));
-      *reinterpret_cast<uint4*>(ts + o) = v;
+    // shared coordinates (one message for vW workers): also the column sums of their values
+    if (sums && w == 0) {
+#pragma unroll
+      for (int u = 0; u < kRangeU; ++u) {
+        const uint32_t j = j0 + (uint32_t)u * kNT + threadIdx.x;
+        if (j < (uint32_t)K) sums[j] = column_sum(vals, vW, K, j);
+      }
     }
+#pragma unroll
+    for (int u = 0; u < kRangeU; ++u) {
+      const uint32_t j = j0 + (uint32_t)u * kNT + threadIdx.x;
+      if (j >= (uint32_t)K) continue;
+      const uint32_t own = tile(cur[u]);
+      const uint32_t ta = j == 0 ? 0u : tile(prv[u]) + 1u;
+      const uint32_t tb = j == (uint32_t)K - 1u ? (uint32_t)nt : own;
+      const uint32_t n = tb + 1u > ta ? tb + 1u - ta : 0u;
+      bool mine = n <= kRunOwn;
+      if (!mine) {
+        const uint32_t p = atomicAdd(&s_nlong, 1u);
+        if (p < kRangeStash) {
+          s_ta[p] = ta;
+          s_n[p] = n;
+          s_j[p] = j;
+          s_own[p] = own;
+        } else {
+          mine = true;
+        }
+      }
+      if (mine)
+        for (uint32_t k = 0; k < n; ++k) ts[ta + k] = value(j, ta + k, own);
+    }
+    __syncthreads();
+    const uint32_t nl = min(s_nlong, kRangeStash);
+    for (uint32_t q = 0; q < nl; ++q) {
+      const uint32_t qa = s_ta[q], qe = qa + s_n[q], qj = s_j[q], qown = s_own[q];
+      // 16-byte stores over the part of the run aligned in memory, single words at its two ends
+      const uint32_t a4 = min(qe, qa + (uint32_t)((4u - (tbase + qa) % 4u) % 4u));
+      const uint32_t b4 = a4 + (qe - a4) / 4u * 4u;
+      if (threadIdx.x < a4 - qa) ts[qa + threadIdx.x] = value(qj, qa + threadIdx.x, qown);
+      if (threadIdx.x < qe - b4) ts[b4 + threadIdx.x] = value(qj, b4 + threadIdx.x, qown);
+      for (uint32_t o = a4 + 4u * threadIdx.x; o < b4; o += 4u * kNT) {
+        const uint4 v = make_uint4(value(qj, o, qown), value(qj, o + 1, qown), value(qj, o + 2, qown),
+                                   value(qj, o + 3, qown));
+        *reinterpret_cast<uint4*>(ts + o) = v;
+      }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) s_nlong = 0;
+    __syncthreads();
   }
+}
+
+// Workgroups of the range pass per message: one per kNT * U entries, capped for long messages so
+// that all messages together fill the chip a few times over.
+inline bool agg_ranges_big(int32_t K, int32_t W) { return (int64_t)K * W >= kRangeBig; }
+inline uint32_t agg_ranges_gx(int32_t K, int32_t W) {
+  if (!agg_ranges_big(K, W)) return (uint32_t)(((int64_t)K + kNT - 1) / kNT);
+  const uint32_t need = (uint32_t)(((int64_t)K + kNT * kRangeUBig - 1) / (kNT * kRangeUBig));
+  const uint32_t cap = (uint32_t)std::max<int32_t>(1, 8192 / std::max<int32_t>(W, 1));
+  return std::max<uint32_t>(1u, std::min(need, cap));
 }
 
 // out = sum / W in IEEE float32.  For W a power of two the quotient is the exact scaling
@@ -879,6 +923,7 @@ constexpr uint32_t kListLds = 8192;    // listed candidates held in LDS by k_sel
 constexpr uint32_t kRowsLds = 16384;   // rows per segment whose list additions k_select counts in LDS
 constexpr uint32_t kRankList = 256;    // lists up to this size are ranked directly (no radix levels)
 constexpr uint32_t kBigK = 1u << 20;   // layouts with a k_l this large count row winners in parallel
+constexpr int32_t kBigRows = 16384;    // ... and so do layouts with a segment of more rows than this
 constexpr uint32_t kSelPer = 8;        // rows per k_select thread held in registers
 constexpr uint32_t kHistDirect = 32;   // rows with more candidates histogram them in LDS first
 constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
@@ -1751,26 +1796,48 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   uint32_t lc[kSubLists];
 #pragma unroll
   for (int c = 0; c < kSubLists; ++c) lc[c] = direct ? 0u : *lcnt_of(ws, l, (uint32_t)c);
+  // random-k on a layout with very many rows needs only the totals: the rows are summed with
+  // coalesced strided loads there, not in per-thread runs (one workgroup reading 244,141 rows in
+  // runs of 238 per thread took 0.44 ms at 1e9 elements)
+  const bool strided = KIND == 1 && !direct && BIG;
   uint32_t cr[kPer], cn[kPer];
 #pragma unroll
   for (uint32_t x = 0; x < kPer; ++x) {
-    cr[x] = a + x < b ? rc[a + x] : 0u;
-    cn[x] = a + x < b ? cc[a + x] : 0u;
+    cr[x] = !strided && a + x < b ? rc[a + x] : 0u;
+    cn[x] = !strided && a + x < b ? cc[a + x] : 0u;
   }
   if constexpr (KIND == 1) {
     // random-k: the certain winners S (keys below ulo) and the candidates N decide whether the
     // window [ulo, tau) holds the k_l-th smallest key
     // (direct lists: also the rows whose undecided candidates overflowed their pair slot)
     uint32_t sv[3] = {0u, 0u, 0u};
+    if (strided) {
+      constexpr uint32_t kU = 8;
+      for (uint32_t x0 = threadIdx.x; x0 < nr; x0 += kU * kSelNT) {
+        uint32_t ra[kU], ca[kU];
 #pragma unroll
-    for (uint32_t x = 0; x < kPer; ++x) {
-      sv[0] += cr[x];
-      sv[1] += cn[x];
-      sv[2] += cn[x] - cr[x] > kRowPairs ? 1u : 0u;
-    }
-    for (uint32_t x = a + kPer; x < b; ++x) {
-      sv[0] += rc[x];
-      sv[1] += cc[x];
+        for (uint32_t u = 0; u < kU; ++u) {
+          const uint32_t x = x0 + u * kSelNT;
+          ra[u] = x < nr ? rc[x] : 0u;
+          ca[u] = x < nr ? cc[x] : 0u;
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kU; ++u) {
+          sv[0] += ra[u];
+          sv[1] += ca[u];
+        }
+      }
+    } else {
+#pragma unroll
+      for (uint32_t x = 0; x < kPer; ++x) {
+        sv[0] += cr[x];
+        sv[1] += cn[x];
+        sv[2] += cn[x] - cr[x] > kRowPairs ? 1u : 0u;
+      }
+      for (uint32_t x = a + kPer; x < b; ++x) {
+        sv[0] += rc[x];
+        sv[1] += cc[x];
+      }
     }
     uint32_t ex[3], tot[3];
     block_excl_scan_n<kSelNT, 3>(sv, lds, ex, tot);

@@ -149,7 +149,11 @@ void ef_layout::build() {
     if (dl > kSampleMax) all_exact = false;
   }
   K = P[n];
+  // many-workgroup row counting: a very large k_l, or a segment with more rows than k_select's
+  // workgroup scans quickly (one workgroup walking 244,141 rows took 0.5-0.9 ms at 1e9 elements)
   big = *std::max_element(k.begin(), k.end()) >= kBigK;
+  for (int l = 0; l < n && !big; ++l)
+    if (cbase[l + 1] - cbase[l] > kBigRows) big = true;
   // random-k without k_collect: every row of a segment is held by a k_select thread and the
   // whole window [ulo, tau) fits k_select's LDS list (a window or a row list that overflows at
   // run time takes the exact path)
@@ -845,10 +849,14 @@ static int prepare_randk(const ef_layout* L, int32_t W, const uint64_t* seeds, u
   P.step = step;
   EF_TRY(run_select<1>(L, P, EF_PHASE_ALL, stream));
   const int32_t nt = agg_tiles(L->d);
-  const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
+  const uint32_t blocks = agg_ranges_gx((int32_t)L->K, W);
   uint32_t* ts = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(ws) + L->ws_layout(EF_OP_RANDK).total);
-  EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), dim3(kNT), 0, S(stream), L->T.d, (int32_t)L->K, nt,
-            idx, ts, (uint64_t)(ws_stride / 4), nullptr, 0, nullptr);
+  if (agg_ranges_big((int32_t)L->K, W))
+    EF_LAUNCH(k_agg_ranges<kRangeUBig>, dim3((unsigned)blocks, (unsigned)W), dim3(kNT), 0, S(stream), L->T.d,
+              (int32_t)L->K, nt, idx, ts, (uint64_t)(ws_stride / 4), nullptr, 0, nullptr);
+  else
+    EF_LAUNCH(k_agg_ranges<1>, dim3((unsigned)blocks, (unsigned)W), dim3(kNT), 0, S(stream), L->T.d, (int32_t)L->K,
+              nt, idx, ts, (uint64_t)(ws_stride / 4), nullptr, 0, nullptr);
   return launched();
 }
 
@@ -987,11 +995,15 @@ int run_aggregate(const ef_layout* L, int msg_kind, int32_t W, const uint32_t* m
     const size_t need = ef_workspace_bytes(L, EF_OP_AGG_SPARSE, W);
     if (!ws || !aligned(ws, kAlign)) return EF_EINVAL;
     if (ws_bytes < need) return EF_EWORKSPACE;
-    const size_t blocks = ((size_t)L->K + kNT - 1) / kNT;
+    const uint32_t blocks = agg_ranges_gx((int32_t)L->K, W);
     uint32_t* ts = reinterpret_cast<uint32_t*>(ws);
     const int32_t nt = agg_tiles(L->d);
-    EF_LAUNCH(k_agg_ranges, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts,
-              (uint64_t)(nt + 1), val, vW, sums);
+    if (agg_ranges_big((int32_t)L->K, W))
+      EF_LAUNCH(k_agg_ranges<kRangeUBig>, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt,
+                m, ts, (uint64_t)(nt + 1), val, vW, sums);
+    else
+      EF_LAUNCH(k_agg_ranges<1>, dim3((unsigned)blocks, (unsigned)W), blk, 0, st, L->T.d, (int32_t)L->K, nt, m, ts,
+                (uint64_t)(nt + 1), val, vW, sums);
     EF_TRY(launched());
     EF_LAUNCH(k_agg_sparse, dim3((unsigned)nt), dim3(64), 0, st, L->T.d, W, (int32_t)L->K, nt, m,
               sums ? sums : val, ts, O);
