@@ -781,8 +781,9 @@ def main():
     value = elems_per_step / (ms_per_step / 1e3)
 
     # diagnostics words of the top-k / random-k workspaces, OR-ed over every worker and every step
-    # so far (warm-up and timed): bit 1 = a segment took the exact whole-segment path, bit 2 = a
-    # row-count mismatch (never expected)
+    # so far (warm-up and timed): bit 1 = a segment took the exact whole-segment path, bit 3 = a top-k
+    # segment collected its candidates again at a lower threshold, bit 2 = a row-count mismatch
+    # (never expected)
     diagnostics = {}
     for k, op in (("topk", E.EF_OP_TOPK), ("randk", E.EF_OP_RANDK)):
         if k not in kinds:
@@ -793,6 +794,7 @@ def main():
         for r in rows:
             word |= lay0.diag(r, op)
         diagnostics[k] = {"word": word, "exact_path_taken": bool(word & E.DIAG_SLOW_PATH),
+                          "candidate_retry": bool(word & E.DIAG_RETRY),
                           "count_mismatch": bool(word & E.DIAG_COUNT_MISMATCH)}
 
     # ---- per-variant breakdown: each variant alone (batch schedule: its W steps and aggregate on

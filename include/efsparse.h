@@ -91,6 +91,9 @@ extern "C" {
 #define EF_TUNE_RANDK_EXTRA 1  /* random-k: candidate bound, constant margin (default 32) */
 #define EF_TUNE_TOPK_SIGMA 2   /* top-k: sampled threshold margin in standard deviations (default 6) */
 #define EF_TUNE_TOPK_EXTRA 3   /* top-k: sampled threshold margin, constant part (default 8) */
+#define EF_TUNE_TOPK_RETRY 4   /* top-k: 1 (default) lets a segment whose sampled candidates fall
+                                  short re-collect them at a lower threshold over the whole device;
+                                  0 sends it straight to the exact whole-segment path */
 
 typedef struct ef_layout ef_layout;
 
@@ -347,7 +350,9 @@ int ef_step_randk_prepared_batch(const ef_layout* layout, int32_t W, const void*
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could
  * not contain the answer and the exact whole-segment path ran instead (a
- * slower path with the same result), and whose bit 2 is set if the per-row
+ * slower path with the same result), bit 3 when a top-k segment's sampled
+ * candidates fell short and were collected again at a lower threshold (a few
+ * microseconds more, same result), and whose bit 2 is set if the per-row
  * winner counts of a segment did not add up to k_l (an internal consistency
  * check that should never fire; message writes stay inside the segment's
  * range regardless).  The word is only ever OR-ed: clear it to watch a given

@@ -26,6 +26,7 @@ constexpr uint32_t kRandblockTag = 0x02000000u;
 constexpr uint32_t kSampleTag = 0x03000000u;  // top-k: positions of the threshold sample
 
 constexpr uint32_t kDiagSlowPath = 2u;
+constexpr uint32_t kDiagRetry = 8u;  // a top-k segment re-collected its candidates at a lower threshold
 
 // Per-segment selection record, uint32 words.  Key' is the selection key (top-k: magnitude bits;
 // random-k: complement of the Philox key), larger is better; among equal key' the lower index wins.
@@ -39,7 +40,9 @@ enum : int {
   R_MODE = 5,   // 1: the candidates are exactly the winners (threshold from the whole segment)
   R_SH = 6,     // candidate histogram: bin shift
   R_B = 7,      // candidate histogram: bin holding the k_l-th best candidate
-  R_NEED = 8,   // winners still needed from bin R_B
+  R_NEED = 8,   // winners still needed from bin R_B (retry: from the listed candidates)
+  R_RETRY = 9,  // top-k: 1 when the segment's candidates fell short of k_l and are collected again
+  R_A2 = 10,    // top-k retry: the lower threshold; keys in [R_A2, R_A) are the listed candidates
 };
 
 constexpr int kBtWords = 8;  // words per record of the block aggregate's (tile, segment) table
@@ -68,6 +71,7 @@ struct Tables {
   int32_t d, L, nchunks, nrows, nruns, nbtiles;
   int32_t rk_direct;           // random-k: k_stream_sel counts the certain winners and lists the
                                // undecided candidates of every row; k_select gathers the lists
+  int32_t tk_retry;            // top-k: the candidate retry is enabled
 };
 
 // ---------------------------------------------------------------------------------------------

@@ -1547,13 +1547,58 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   uint32_t above;
   const int bin = block_resolve<kSelNT>(hist, kHBins, kl, lds, above);
   if (threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
-  if (threadIdx.x == 0) {
-    if (bin < 0) {
-      R[R_SLOW] = 1;
-      atomicOr(ws.diag, kDiagSlowPath);
-    } else {
+  if (bin >= 0) {
+    if (threadIdx.x == 0) {
       R[R_B] = (uint32_t)bin;
       R[R_NEED] = kl - above;
+      R[R_RETRY] = 0;
+    }
+    return;
+  }
+  // Fewer than k_l candidates: the sample misjudged the density above A.  The retry threshold A2
+  // is read from the same sample, at the rank where the density actually found (N keys above A
+  // against s sampled ones) predicts 4 k_l + 256 keys above it; its rows then collect every key
+  // >= A2 again (k_collect), and k_select falls back to the exact whole-segment path only if those
+  // are still fewer than k_l.
+  uint32_t mine = 0;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) mine += hist[u * kSelNT + threadIdx.x];
+  uint32_t N;
+  (void)block_excl_scan<kSelNT>(mine, lds, N);
+  const uint32_t A = R[R_A];
+  const uint32_t ns = ((uint32_t)T.seg_ro[l + 1] - (uint32_t)T.seg_ro[l]) * kSampleRun;
+  const uint32_t* sk = ws.samp + (size_t)T.seg_ro[l] * kSampleRun;
+  __syncthreads();
+  for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist[b] = 0;
+  __syncthreads();
+  uint32_t above_a = 0;
+  for_keys(sk, ns, [&](uint32_t, uint32_t k) {
+    atomicAdd(&hist[k >> 20], 1u);
+    above_a += k >= A ? 1u : 0u;
+  });
+  uint32_t sA;
+  (void)block_excl_scan<kSelNT>(above_a, lds, sA);  // its barriers also publish hist
+  // (at least the rank where the sample alone predicts 4 k_l + 64 keys, in case its top was the
+  // only part it misjudged)
+  const uint32_t n_seg = (uint32_t)T.seg_off[l + 1] - (uint32_t)T.seg_off[l];
+  const uint64_t plain = (((uint64_t)4 * kl + 64u) * ns + n_seg - 1u) / n_seg;
+  const uint64_t want = ((uint64_t)4 * kl + 256u) * (uint64_t)(sA + 1u);
+  const uint64_t ratio = (want + max(N, 1u) - 1u) / max(N, 1u);
+  const uint32_t r2 = (uint32_t)min<uint64_t>((uint64_t)ns, max(plain, ratio));
+  uint32_t a2above;
+  const int b2 = block_resolve<kSelNT>(hist, kHBins, r2, lds, a2above);
+  const uint32_t A2 = b2 < 0 || r2 >= ns ? 0u : min(A, (uint32_t)b2 << 20);
+  if (threadIdx.x == 0) {
+    if (!T.tk_retry || A2 >= A) {
+      R[R_SLOW] = 1;
+      R[R_RETRY] = 0;
+      atomicOr(ws.diag, kDiagSlowPath);
+    } else {
+      R[R_RETRY] = 1u;
+      R[R_A2] = A2;
+      R[R_NEED] = kl - N;
+      R[R_B] = 1u;  // not the tie bin: the listed candidates are ranked
+      atomicOr(ws.diag, kDiagRetry);
     }
   }
 }
@@ -1566,6 +1611,59 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 // whole grid; more per wavefront for a batch): the rows' segments, candidate counts and first 64
 // candidate keys are loaded together; counts and list positions come from ballots, and each chunk
 // of 64 candidates reserves its list space with one atomic.
+// Top-k candidate retry, one wavefront per row: the row's keys are read again from acc and every
+// key >= A2 becomes a candidate in the row's slot, in index order; those >= A (the first
+// candidates) are certain winners, those in [A2, A) go to the segment's list.
+__device__ __forceinline__ void collect_retry(const Tables& T, const WSel& ws, const Batch& BT, uint32_t row, int l,
+                                              const uint32_t* R) {
+  const uint32_t lane = threadIdx.x & 63;
+  const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
+  uint32_t o = 0, e_ = (uint32_t)T.d, tb = row * kTile;
+  if (T.L > 1) {
+    const uint4 rr = reinterpret_cast<const uint4*>(T.row_rec)[row];
+    o = rr.y;
+    e_ = rr.z;
+    tb = rr.w;
+  }
+  const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
+  const uint32_t A = R[R_A], A2 = R[R_A2];
+  const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
+  uint32_t* cidx = ws.cand_idx + (size_t)row * kTile;
+  float* cval = ws.cand_val + (size_t)row * kTile;
+  uint32_t* ckey = ws.cand_key + (size_t)row * kTile;
+  uint32_t n = 0, na = 0;
+  for (uint32_t i0 = lo; i0 < hi; i0 += 64) {
+    const uint32_t i = i0 + lane;
+    const float v = i < hi ? acc[i] : 0.0f;
+    const uint32_t key = mag_key(v);
+    const bool take = i < hi && key >= A2, cert = take && key >= A, lst = take && !cert;
+    const uint64_t bt = __ballot(take), bl = __ballot(lst);
+    if (take) {
+      const uint32_t pos = n + lanes_below(bt);
+      cidx[pos] = i;
+      cval[pos] = v;
+      ckey[pos] = key;
+    }
+    n += (uint32_t)__popcll(bt);
+    na += (uint32_t)__popcll(__ballot(cert));
+    const uint32_t nl = (uint32_t)__popcll(bl);
+    if (nl) {
+      uint32_t base = 0;
+      if (lane == 0) base = atomicAdd(lcnt_of(ws, l, c), nl);
+      base = __shfl(base, 0, 64);
+      if (lst) {
+        const size_t p = sublist_pos(r0, c, base + lanes_below(bl));
+        ws.list_key[p] = key;
+        ws.list_idx[p] = i;
+      }
+    }
+  }
+  if (lane == 0) {
+    ws.counts[row] = n;
+    ws.rcnt[row] = na;
+  }
+}
+
 template <int KIND, uint32_t kCollectRows>
 __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
@@ -1589,6 +1687,10 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
     uint32_t A = 0, sh = 0, B = 0, ulo = 0;
     if constexpr (KIND == 0) {
       if (R[R_SLOW] || R[R_MODE]) continue;
+      if (R[R_RETRY]) {
+        collect_retry(T, ws, BT, row, l, R);
+        continue;
+      }
       A = R[R_A];
       sh = R[R_SH];
       B = R[R_B];
@@ -1796,6 +1898,22 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   uint32_t lc[kSubLists];
 #pragma unroll
   for (int c = 0; c < kSubLists; ++c) lc[c] = direct ? 0u : *lcnt_of(ws, l, (uint32_t)c);
+  if constexpr (KIND == 0) {
+    // a candidate retry whose list still cannot give the `need` winners: the exact path
+    if (!slow && listed && R[R_RETRY]) {
+      uint32_t m = 0;
+#pragma unroll
+      for (int c = 0; c < kSubLists; ++c) m += lc[c];
+      if (m < need) {
+        slow = true;
+        __syncthreads();  // every thread has read R_SLOW before it is set
+        if (threadIdx.x == 0) {
+          R[R_SLOW] = 1u;
+          atomicOr(ws.diag, kDiagSlowPath);
+        }
+      }
+    }
+  }
   // random-k on a layout with very many rows needs only the totals: the rows are summed with
   // coalesced strided loads there, not in per-thread runs (one workgroup reading 244,141 rows in
   // runs of 238 per thread took 0.44 ms at 1e9 elements)

@@ -59,7 +59,7 @@ struct ef_layout {
   double density = 0;
   int64_t block = 1;
   std::vector<int64_t> off64;
-  double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0;
+  double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0, tk_retry = 1.0;
 
   std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg, runseg;
   std::vector<uint32_t> btile;  // block aggregate, multi-segment: (data tile, segment) pairs
@@ -666,6 +666,7 @@ int ef_layout_tune(ef_layout* layout, int knob, double value) {
     case EF_TUNE_RANDK_EXTRA: layout->rk_extra = value; break;
     case EF_TUNE_TOPK_SIGMA: layout->tk_sigma = value; break;
     case EF_TUNE_TOPK_EXTRA: layout->tk_extra = value; break;
+    case EF_TUNE_TOPK_RETRY: layout->tk_retry = value; break;
     default: return EF_EINVAL;
   }
   // a failed rebuild leaves the layout unusable (every later call on it returns EF_EINVAL)
@@ -716,6 +717,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.nrows = L->nrows;
   T.nruns = L->nruns;
   T.rk_direct = L->rk_direct ? 1 : 0;
+  T.tk_retry = L->tk_retry != 0.0 ? 1 : 0;
   L->bound = true;
   return EF_OK;
 }

@@ -118,6 +118,7 @@ def test_tune_rejects_bad_knobs():
     assert E.lib().ef_layout_tune(L.handle, 99, 1.0) == E.EF_EINVAL
     assert E.lib().ef_layout_tune(L.handle, 0, float("inf")) == E.EF_EINVAL
     assert E.lib().ef_layout_tune(L.handle, 0, 5.0) == E.EF_OK
+    assert E.lib().ef_layout_tune(L.handle, E.EF_TUNE_TOPK_RETRY, 0.0) == E.EF_OK
 
 
 def test_status_strings():

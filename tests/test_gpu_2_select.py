@@ -87,14 +87,37 @@ def test_bf16_gradient(kind):
                          ids=["flat", "two-large", "mixed"])
 def test_topk_forced_slow_path(offs):
     """A threshold margin of -1e9 standard deviations puts the sampled threshold at the sample's
-    largest key, so every sampled segment has fewer candidates than k: the exact whole-segment
-    path must give the same result."""
+    largest key, so every sampled segment has fewer candidates than k; with the retry switched
+    off, the exact whole-segment path must give the same result."""
     import paper_2009_09271_amd as E
     announce("topk slow", offs[-1])
-    c = Case(offs, 0.01, tune={E.EF_TUNE_TOPK_SIGMA: -1e9})
+    c = Case(offs, 0.01, tune={E.EF_TUNE_TOPK_SIGMA: -1e9, E.EF_TUNE_TOPK_RETRY: 0})
     g, e = _inputs(c.d, 8)
     diag = _run_steps(c, "topk", [g, g], e)
     assert diag & E.DIAG_SLOW_PATH, "the slow path did not run"
+
+
+@pytest.mark.parametrize("offs", [[0, 100000], [0, 5, 50000, 120000], [0, 3, 40000, 40001, 90001],
+                                  [0, 1 << 21]],
+                         ids=["flat", "two-large", "mixed", "many-rows"])
+@pytest.mark.parametrize("scale", [1.0, 0.0], ids=["spread", "equal"])
+def test_topk_forced_retry(offs, scale):
+    """The same forced shortfall with the retry on: the sampled segments collect their candidates
+    again at a lower threshold over the whole device and must give the same result, without the
+    exact whole-segment path.  'equal' gives every element of a segment the same magnitude outside
+    a few large values, so the retry's list is all ties, ranked by index."""
+    import paper_2009_09271_amd as E
+    announce("topk retry", offs[-1], scale)
+    c = Case(offs, 0.01, tune={E.EF_TUNE_TOPK_SIGMA: -1e9})
+    rng = np.random.default_rng(12)
+    if scale:
+        g = (rng.standard_normal(c.d) * 10.0 ** rng.integers(-2, 1, c.d)).astype(np.float32)
+    else:
+        g = np.full(c.d, 0.75, np.float32)
+        g[rng.choice(c.d, size=c.d // 1000, replace=False)] = 1.0  # fewer than k: the rest are ties
+    e = np.zeros(c.d, np.float32)
+    diag = _run_steps(c, "topk", [g], e)
+    assert diag & E.DIAG_RETRY and not diag & E.DIAG_SLOW_PATH, f"diagnostics {diag:#x}"
 
 
 def test_randk_forced_slow_path():
