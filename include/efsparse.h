@@ -94,6 +94,12 @@ extern "C" {
 #define EF_TUNE_TOPK_RETRY 4   /* top-k: 1 (default) lets a segment whose sampled candidates fall
                                   short re-collect them at a lower threshold over the whole device;
                                   0 sends it straight to the exact whole-segment path */
+#define EF_TUNE_POOL 5         /* top-k / random-k workspace: scale (>= 0, default 1) of the
+                                  candidate overflow pool and of the candidate lists, whose default
+                                  sizes follow the expected candidate counts (O(K + rows), not
+                                  O(d)).  Smaller saves workspace and sends more segments to the
+                                  exact path; 0 keeps only each row's static slot.  A negative
+                                  value is EF_EINVAL. */
 
 typedef struct ef_layout ef_layout;
 
@@ -140,7 +146,13 @@ int ef_layout_bind(ef_layout* layout, void* dev_tables, size_t bytes, void* stre
  * decompress_aggregate_apply with W workers, EF_OP_AGG_SHARED for
  * decompress_aggregate_shared, EF_OP_RANDK_PREP for ef_randk_prepare and
  * ef_step_randk_prepared (W is ignored otherwise).  Random-block needs
- * none (returns 0).
+ * none (returns 0).  Top-k and random-k workspaces grow with K and the
+ * number of 4096-element rows (each row's static candidate slot, an overflow
+ * pool, candidate lists), not with d (ResNet-50 at 0.1 % density: 16 MiB,
+ * 0.65 bytes per element, in one segment); see EF_TUNE_POOL.  Their overflow counters are cleared by the
+ * step's last kernel (top-k: also by its first), so a fresh workspace
+ * needs no clearing (one holding garbage can send a random-k segment whose
+ * row overflows its slot down the exact path once: same result).
  * Returns 0 for a null layout or unknown op. */
 size_t ef_workspace_bytes(const ef_layout* layout, int op, int32_t W);
 
@@ -349,8 +361,8 @@ int ef_step_randk_prepared_batch(const ef_layout* layout, int32_t W, const void*
 
 /* Diagnostics: byte offset inside a top-k / random-k workspace of a uint32
  * word whose bit 1 is set when, for at least one segment, the candidates could
- * not contain the answer and the exact whole-segment path ran instead (a
- * slower path with the same result), bit 3 when a top-k segment's sampled
+ * not contain the answer, or did not fit the workspace, and the exact
+ * whole-segment path ran instead (a slower path with the same result), bit 3 when a top-k segment's sampled
  * candidates fell short and were collected again at a lower threshold (a few
  * microseconds more, same result), and whose bit 2 is set if the per-row
  * winner counts of a segment did not add up to k_l (an internal consistency

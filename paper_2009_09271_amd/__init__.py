@@ -23,7 +23,7 @@ EF_OK, EF_EINVAL, EF_ERANGE, EF_EWORKSPACE, EF_EHIP, EF_ENOMEM = range(6)
 EF_F32, EF_BF16 = 0, 1
 EF_OP_TOPK, EF_OP_RANDK, EF_OP_RANDBLOCK, EF_OP_AGG_SPARSE, EF_OP_AGG_BLOCK, EF_OP_AGG_SHARED, EF_OP_RANDK_PREP = range(7)
 EF_MSG_SPARSE, EF_MSG_BLOCK = 0, 1
-EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA, EF_TUNE_TOPK_RETRY = range(5)
+EF_TUNE_RANDK_SIGMA, EF_TUNE_RANDK_EXTRA, EF_TUNE_TOPK_SIGMA, EF_TUNE_TOPK_EXTRA, EF_TUNE_TOPK_RETRY, EF_TUNE_POOL = range(6)
 EF_PHASE_PREPARE, EF_PHASE_STREAM, EF_PHASE_FINISH, EF_PHASE_ALL = 1, 2, 4, 7
 DIAG_SLOW_PATH = 2
 DIAG_COUNT_MISMATCH = 4

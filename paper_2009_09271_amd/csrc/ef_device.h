@@ -7,6 +7,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace efs {
 
 constexpr int kNT = 256;                      // threads per workgroup of most kernels
@@ -43,6 +45,7 @@ enum : int {
   R_NEED = 8,   // winners still needed from bin R_B (retry: from the listed candidates)
   R_RETRY = 9,  // top-k: 1 when the segment's candidates fell short of k_l and are collected again
   R_A2 = 10,    // top-k retry: the lower threshold; keys in [R_A2, R_A) are the listed candidates
+  R_OVF = 11,   // top-k: candidates or listed entries did not fit the workspace (the exact path runs)
 };
 
 constexpr int kBtWords = 8;  // words per record of the block aggregate's (tile, segment) table
@@ -59,6 +62,8 @@ struct Tables {
   const int32_t* seg_ro;       // [L+1] first top-k sample run of each segment
   const uint64_t* seg_tau;     // [L]   random-k: Philox keys below tau are candidates
   const uint32_t* seg_ulo;     // [L]   random-k: keys below ulo are winners if at most k_l are
+  const uint64_t* seg_lbase;   // [L]   first entry of the segment's list region in the list arrays
+  const uint32_t* seg_lq;      // [L]   entries per sub-list in that region (min(kSubLists, rows) sub-lists)
   const int32_t* chunk_sf;     // [nchunks] first / last segment of each data tile
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row

@@ -44,14 +44,29 @@ struct WSel {
   uint32_t* counts;    // [nrows] candidates per row
   uint32_t* rcnt;      // [nrows] winners per row
   uint32_t* roff;      // [nrows] message position of each row's first winner
-  uint32_t* rtie;      // [nrows] top-k: candidates in the threshold bin when that bin is the key A
+  uint32_t* rtie;      // [nrows] top-k: elements equal to the key A (counted, not stored)
   uint32_t* lcnt;      // [L][kSubLists][kLineWords] sizes of the sub-lists, one cache line each
-  uint32_t* cand_idx;  // [nrows * kTile] per-row candidate slots, index order
-  float* cand_val;     // [nrows * kTile]
-  uint32_t* cand_key;  // [nrows * kTile] key' of each candidate
-  uint32_t* list_idx;  // [nrows * kTile] sub-lists of undecided candidates (see SubLists)
-  uint32_t* list_key;  // [nrows * kTile]
+  uint32_t* coff;      // [nrows] first entry of each row's candidates in the pool (kDropped: not
+                       //   stored); one segment: written only for rows beyond their static slot
+  uint32_t* pcnt;      // [kPools][kLineWords] fill counters of the overflow pool's parts
+  uint32_t* cand_idx;  // [pool0 + capB] candidate pool: each row's static slot (soff, S),
+  float* cand_val;     //   then the overflow pool for rows with more candidates (index order per row)
+  uint32_t* cand_key;  //   key' of each candidate
+  uint32_t* list_idx;  // sub-lists of undecided candidates, per segment (see SubLists)
+  uint32_t* list_key;
+  uint2* pairs;        // random-k, direct layouts: each row's undecided (key', index) pairs at its
+                       //   pool entries (the list arrays' memory)
+  const uint32_t* soff;  // [nrows+1] first entry of each row's static slot (several segments)
+  uint32_t S;          // one segment: static slot entries per row (row r's slot starts at r * S and
+                       //   holds min(S, the row's elements))
+  uint32_t pool0;      // first entry of the overflow pool (the static slots end there)
+  uint32_t capB;       // overflow pool entries, kPools equal parts (row r reserves in part r % kPools)
 };
+
+constexpr uint32_t kDropped = 0xFFFFFFFFu;  // coff of a row whose candidates did not fit
+constexpr uint32_t kAccRow = 0x80000000u;   // counts flag of a top-k row emitted from acc (winning
+                                            //   ties); the count is then the row's length
+constexpr int kPools = 16;                  // parts of the overflow pool, one counter each
 
 __device__ __forceinline__ uint32_t* res_of(const WSel& w, int l) { return w.res + (size_t)l * kResWords; }
 
@@ -85,47 +100,73 @@ __device__ __forceinline__ WSel ws_at(WSel w, uint64_t off) {
   w.roff = shifted(w.roff, off);
   w.rtie = shifted(w.rtie, off);
   w.lcnt = shifted(w.lcnt, off);
+  w.coff = shifted(w.coff, off);
+  w.pcnt = shifted(w.pcnt, off);
   w.cand_idx = shifted(w.cand_idx, off);
   w.cand_val = shifted(w.cand_val, off);
   w.cand_key = shifted(w.cand_key, off);
   w.list_idx = shifted(w.list_idx, off);
   w.list_key = shifted(w.list_key, off);
-  return w;
+  w.pairs = shifted(w.pairs, off);
+  return w;  // (soff is a layout table: not shifted)
 }
 
-// Random-k, direct lists: row r's undecided candidates as (key', index) pairs in the list_idx slot
-// of the row (kTile words hold kRowPairs pairs).
-constexpr uint32_t kRowPairs = kTile / 2;
-__device__ __forceinline__ uint2* row_pairs(const WSel& w, uint32_t row) {
-  return reinterpret_cast<uint2*>(w.list_idx + (size_t)row * kTile);
-}
 constexpr int kLineWords = 32;  // 128-byte L2 line: counters hit by many atomics get a line each
 __device__ __forceinline__ uint32_t* lcnt_of(const WSel& w, int l, uint32_t c) {
   return w.lcnt + ((size_t)l * kSubLists + c) * kLineWords;
 }
+__device__ __forceinline__ uint32_t* pcnt_of(const WSel& w, uint32_t part) { return w.pcnt + (size_t)part * kLineWords; }
 
-// Entry t of sub-list c of the segment whose rows start at r0 is stored in the slot of row
-// r0 + c + kSubLists * (t / kTile), at t % kTile.  Sub-list c only takes entries of the rows
-// r0 + c + kSubLists * j (at most kTile each), so it never runs past the segment's rows.
-__device__ __forceinline__ size_t sublist_pos(uint32_t r0, uint32_t c, uint32_t t) {
-  return (size_t)(r0 + c + kSubLists * (t / kTile)) * kTile + (t % kTile);
+// Reserves n pool entries for row `row` (more than its static slot holds) in part row % kPools of
+// the overflow pool; kDropped if the part is full.  One thread.
+__device__ __forceinline__ uint32_t pool_reserve(const WSel& w, uint32_t row, uint32_t n) {
+  const uint32_t part = row % kPools, q = w.capB / kPools;
+  const uint32_t at = atomicAdd(pcnt_of(w, part), n);
+  if (at > q || n > q - at) return kDropped;
+  return w.pool0 + part * q + at;
+}
+
+// The first pool entry of a row holding cnt candidates, given its coff word co: one segment: its
+// static slot unless they did not fit there.
+__device__ __forceinline__ uint32_t row_entry(const Tables& T, const WSel& w, uint32_t row, uint32_t cnt,
+                                              uint32_t co) {
+  if (T.L > 1) return co;
+  return cnt > min(w.S, (uint32_t)T.d - row * kTile) ? co : row * w.S;
+}
+
+// The static slot of a row: first entry and capacity.
+__device__ __forceinline__ void static_slot(const Tables& T, const WSel& w, uint32_t row, uint32_t& at, uint32_t& cap) {
+  if (T.L == 1) {  // every row but the last is a whole tile
+    at = row * w.S;
+    cap = min(w.S, (uint32_t)T.d - row * kTile);
+  } else {
+    at = w.soff[row];
+    cap = w.soff[row + 1] - at;
+  }
+}
+
+// First entry of sub-list c of segment l: sub-list c owns seg_lq[l] entries of the segment's region
+// (loaded once per row, ahead of the row's loop).
+__device__ __forceinline__ size_t sublist_base(const Tables& T, int l, uint32_t c) {
+  return (size_t)T.seg_lbase[l] + (size_t)c * (uint32_t)T.seg_lq[l];
 }
 
 // The sub-lists of one segment read as one array of M[kSubLists] entries (any order).
 struct SubLists {
   const uint32_t* arr;
-  uint32_t r0;
+  size_t base;  // the segment's list region
+  uint32_t q;   // entries per sub-list
   uint32_t M[kSubLists + 1];  // M[c]: entries in sub-lists before c
   __device__ __forceinline__ uint32_t operator[](uint32_t f) const {
-    uint32_t c = 0, base = 0;
+    uint32_t c = 0, b = 0;
 #pragma unroll
     for (int x = 1; x < kSubLists; ++x) {
       if (f >= M[x]) {
         c = (uint32_t)x;
-        base = M[x];
+        b = M[x];
       }
     }
-    return arr[sublist_pos(r0, c, f - base)];
+    return arr[base + (size_t)c * q + (f - b)];
   }
 };
 
@@ -1044,7 +1085,8 @@ __device__ __forceinline__ uint32_t block_max_u32(uint32_t v, uint32_t* lds) {
 
 // Position of the r-th (1-based) entry equal to x among keys[0, m), in position order.  Each
 // wave owns a contiguous share of the positions; `lds` holds kSelNT / 64 words.
-__device__ __forceinline__ uint32_t block_nth_equal(const uint32_t* keys, uint32_t m, uint32_t x, uint32_t r, uint32_t* lds) {
+template <typename K>
+__device__ __forceinline__ uint32_t block_nth_equal(const K& keys, uint32_t m, uint32_t x, uint32_t r, uint32_t* lds) {
   __shared__ uint32_t s_pos;
   constexpr int NW = kSelNT / 64;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -1116,6 +1158,25 @@ __device__ __forceinline__ uint32_t cand_bin(uint32_t key, uint32_t A, uint32_t 
   return key == A ? 0u : 1u + min((key - A - 1u) >> sh, (uint32_t)kHBins - 2u);
 }
 
+// Magnitude keys of acc read in place (a row's elements equal to A are counted, not stored).
+struct AccKeys {
+  const float* p;
+  __device__ __forceinline__ uint32_t operator[](uint32_t f) const { return mag_key(p[f]); }
+};
+
+// The first and one past the last element of a row.
+__device__ __forceinline__ void row_bounds(const Tables& T, uint32_t row, uint32_t& lo, uint32_t& hi) {
+  uint32_t o = 0, e_ = (uint32_t)T.d, tb = row * kTile;
+  if (T.L > 1) {
+    const uint4 rr = reinterpret_cast<const uint4*>(T.row_rec)[row];
+    o = rr.y;
+    e_ = rr.z;
+    tb = rr.w;
+  }
+  lo = max(o, tb);
+  hi = min(e_, tb + kTile);
+}
+
 // ---------------------------------------------------------------------------------------------
 // Top-k sample
 // ---------------------------------------------------------------------------------------------
@@ -1166,6 +1227,8 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
     i = o + a + __umulhi(x, b - a);  // uniform in [a, b): b > a because n > kSampleMax >= ns
     for (uint32_t h = sq; h < (uint32_t)(kHCopies * kHBins); h += ns) ws.hist[(size_t)l * kHCopies * kHBins + h] = 0u;
   }
+  // the overflow pool's counters start from zero (the first kernel of a top-k step)
+  if (r == 0 && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
   uint32_t key = 0;
   if (in) {
     float a;
@@ -1216,6 +1279,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
       R[R_IT] = it;
       R[R_MODE] = 1;
       R[R_SLOW] = 0;
+      R[R_OVF] = 0;
     }
     return;
   }
@@ -1261,6 +1325,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
     R[R_SH] = sh;
     R[R_MODE] = 0;
     R[R_SLOW] = 0;
+    R[R_OVF] = 0;
   }
 }
 
@@ -1286,17 +1351,25 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
   __shared__ uint32_t s_kk[KIND == 1 ? kTile : 1];  // random-k: the candidates' keys, by element
   __shared__ uint32_t wc[kStrW];  // random-k, direct lists: certain winners per wavefront
   __shared__ uint32_t s_und;         // random-k, direct lists: undecided candidates listed so far
+  __shared__ uint32_t s_tie[KIND == 0 ? kStrW : 1];  // top-k: elements equal to A per wavefront
+  __shared__ uint32_t s_cb;          // the row's first pool entry (a reservation in the overflow pool)
   const uint32_t row = blockIdx.x;
   // the row's segment and bounds: arithmetic on one segment, else one record load (the data loads
   // wait for the bounds only, not for a chain through the segment tables)
   int l = 0;
   uint32_t o = 0, e_ = (uint32_t)T.d, tb = row * kTile;
+  uint32_t cb, scap;  // the row's static slot (several segments: loaded with the row's record)
   if (T.L > 1) {
     const uint4 rr = reinterpret_cast<const uint4*>(T.row_rec)[row];
+    cb = ws.soff[row];
+    scap = ws.soff[row + 1];
     l = (int)rr.x;
     o = rr.y;
     e_ = rr.z;
     tb = rr.w;
+    scap -= cb;
+  } else {
+    static_slot(T, ws, row, cb, scap);
   }
   const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -1389,15 +1462,20 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
   uint32_t kk[kSR][4];
   uint32_t ncert = 0;  // random-k, direct lists: certain winners of this wavefront (uniform)
   uint32_t cbits = 0;  // random-k, direct lists: bit 4r+q marks a certain winner (key below ulo)
+  uint32_t ntie = 0;   // top-k, sampled segments: elements equal to A of this wavefront (uniform)
 #pragma unroll
   for (int r = 0; r < kSR; ++r) {
     const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
     uint32_t mk = 0;
     if constexpr (KIND == 0) {
+      // sampled segments: keys above A are stored, keys equal to A (the tie bin: exact zeros, say,
+      // which may be most of a segment) only counted; exact segments: the winner rule itself
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         kk[r][q] = mag_key(v[r][q]);
-        if (((vm[r] >> q) & 1u) && (kk[r][q] > A || (kk[r][q] == A && i0 + q < IA))) mk |= 1u << q;
+        const bool in = (vm[r] >> q) & 1u;
+        if (in && (kk[r][q] > A || (mode != 0 && kk[r][q] == A && i0 + q < IA))) mk |= 1u << q;
+        if (mode == 0) ntie += (uint32_t)__popcll(__ballot(in && kk[r][q] == A));
       }
     } else {
 #pragma unroll
@@ -1429,6 +1507,9 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     if (lane == 0) wc[wid] = ncert;
     if (threadIdx.x == 0) s_und = 0;
   }
+  if constexpr (KIND == 0) {
+    if (lane == 0) s_tie[wid] = ntie;
+  }
   if constexpr (FUSED && KIND == 1) {
     // random-k, direct lists: the residual is +0 at the certain winners (every one of them is sent
     // unless the segment takes the exact path, which puts their values back first), so the emit
@@ -1445,18 +1526,56 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     }
   }
   __syncthreads();
-  uint32_t base = 0;
-  uint32_t* cidx = ws.cand_idx + (size_t)row * kTile;
-  float* cval = ws.cand_val + (size_t)row * kTile;
-  uint32_t* ckey = ws.cand_key + (size_t)row * kTile;
+  // the row's candidates go to its static slot, or, when there are more than it holds, to entries
+  // reserved in the overflow pool; a row that does not fit is dropped and its segment takes the
+  // exact path (the histogram still counts its candidates)
+  // (the wavefront totals are read once: the row's total, and each group's first position for
+  // this wavefront; the total and the slot are uniform, kept in scalar registers)
+  uint32_t tot = 0, rbs[kSR];
 #pragma unroll
   for (int r = 0; r < kSR; ++r) {
-    uint32_t rb = base;
+    uint32_t pre = 0, all = 0;
 #pragma unroll
-    for (int w = 0; w < kStrW; ++w) rb += w < wid ? wt[r][w] : 0u;
-    if (mask[r]) {
+    for (int w = 0; w < kStrW; ++w) {
+      const uint32_t c = wt[r][w];
+      pre += w < wid ? c : 0u;
+      all += c;
+    }
+    rbs[r] = tot + pre;
+    tot += all;
+  }
+  tot = __builtin_amdgcn_readfirstlane(tot);
+  if (tot > scap) {
+    if (threadIdx.x == 0) s_cb = pool_reserve(ws, row, tot);
+    __syncthreads();
+    cb = __builtin_amdgcn_readfirstlane(s_cb);
+  }
+  const bool dropped = cb == kDropped;
+  if (threadIdx.x == 0 && (T.L > 1 || tot > scap)) ws.coff[row] = cb;
+  if (dropped) {
+    if constexpr (KIND == 0) {
+      if (threadIdx.x == 0) atomicOr(&R[R_OVF], 1u);
+    }
+    if constexpr (FUSED && KIND == 1) {
+      // random-k, direct lists: the certain winners' values were stored as +0 above; without the
+      // candidates the exact path cannot restore them, so they are stored again now
+      if (direct) {
+#pragma unroll
+        for (int r = 0; r < kSR; ++r) {
+          const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
+          store4m(acc_out, i0, vm[r], v[r]);
+        }
+      }
+    }
+  }
+  uint32_t* cidx = ws.cand_idx + cb;
+  float* cval = ws.cand_val + cb;
+  uint32_t* ckey = ws.cand_key + cb;
+#pragma unroll
+  for (int r = 0; r < kSR; ++r) {
+    if (mask[r] && !dropped) {
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
-      uint32_t pos = rb + lpre[r];
+      uint32_t pos = rbs[r] + lpre[r];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         if ((mask[r] >> q) & 1u) {
@@ -1469,17 +1588,16 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
           ++pos;
           if (direct && !((cbits >> (4 * r + q)) & 1u)) {
             // random-k, direct lists: an undecided candidate ([ulo, tau)) joins the row's list as
-            // a (key', index) pair; a row with more than kRowPairs of them sends the segment down
-            // the exact path (k_select sees the count)
+            // a (key', index) pair, at the row's pool entries in the pair array (fewer than its
+            // candidates)
             const uint32_t p = atomicAdd(&s_und, 1u);
-            if (p < kRowPairs) row_pairs(ws, row)[p] = make_uint2(key, i0 + q);
+            ws.pairs[(size_t)cb + p] = make_uint2(key, i0 + q);
           }
         }
       }
     }
-#pragma unroll
-    for (int w = 0; w < kStrW; ++w) base += wt[r][w];
   }
+  const uint32_t base = tot;  // the row's candidates
   if (threadIdx.x == 0) ws.counts[row] = base;
   if (direct && threadIdx.x == 0) {
     // random-k, direct lists: the row's certain winners (key below ulo)
@@ -1489,6 +1607,14 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     ws.rcnt[row] = c;
   }
   if constexpr (KIND == 0) {
+    if (mode == 0 && threadIdx.x == 0) {
+      // the ties are the histogram's bin 0
+      uint32_t t = 0;
+#pragma unroll
+      for (int w = 0; w < kStrW; ++w) t += s_tie[w];
+      ws.rtie[row] = t;
+      if (t) atomicAdd(&ws.hist[((size_t)l * kHCopies + (row % kHCopies)) * kHBins], t);
+    }
     if (mode == 0 && base) {
       uint32_t* gh = ws.hist + ((size_t)l * kHCopies + (row % kHCopies)) * kHBins;
       if (base > kHistDirect) {  // many candidates: count them in LDS, then one atomic per used bin
@@ -1527,7 +1653,7 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   // no histogram: its loads read the unused copies and are dropped)
   constexpr int kPer = kHBins / kSelNT;
   static_assert(kHBins % kSelNT == 0, "whole bins per thread");
-  const uint32_t mode = R[R_MODE];
+  const uint32_t mode = R[R_MODE], ovf = R[R_OVF];
   const uint32_t* gh = ws.hist + (size_t)l * kHCopies * kHBins;
   uint32_t c[kPer][kHCopies];
 #pragma unroll
@@ -1535,6 +1661,14 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 #pragma unroll
     for (int x = 0; x < kHCopies; ++x) c[u][x] = gh[x * kHBins + u * kSelNT + threadIdx.x];
   if (mode != 0) return;
+  if (ovf) {  // a row's candidates did not fit the workspace: the exact path
+    if (threadIdx.x == 0) {
+      R[R_SLOW] = 1;
+      R[R_RETRY] = 0;
+      atomicOr(ws.diag, kDiagSlowPath);
+    }
+    return;
+  }
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
     uint32_t sum = 0;
@@ -1558,8 +1692,8 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   // Fewer than k_l candidates: the sample misjudged the density above A.  The retry threshold A2
   // is read from the same sample, at the rank where the density actually found (N keys above A
   // against s sampled ones) predicts 4 k_l + 256 keys above it; its rows then collect every key
-  // >= A2 again (k_collect), and k_select falls back to the exact whole-segment path only if those
-  // are still fewer than k_l.
+  // above A2 again and count those equal to it (k_collect), and k_select falls back to the exact
+  // whole-segment path only if those are still fewer than k_l.
   uint32_t mine = 0;
 #pragma unroll
   for (int u = 0; u < kPer; ++u) mine += hist[u * kSelNT + threadIdx.x];
@@ -1579,10 +1713,11 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   uint32_t sA;
   (void)block_excl_scan<kSelNT>(above_a, lds, sA);  // its barriers also publish hist
   // (at least the rank where the sample alone predicts 4 k_l + 64 keys, in case its top was the
-  // only part it misjudged)
+  // only part it misjudged; only that rank when fewer than 8 sampled keys reach A: the scale
+  // N / s is then too noisy to use, and too large a threshold would overflow the candidate pool)
   const uint32_t n_seg = (uint32_t)T.seg_off[l + 1] - (uint32_t)T.seg_off[l];
   const uint64_t plain = (((uint64_t)4 * kl + 64u) * ns + n_seg - 1u) / n_seg;
-  const uint64_t want = ((uint64_t)4 * kl + 256u) * (uint64_t)(sA + 1u);
+  const uint64_t want = sA >= 8u ? ((uint64_t)4 * kl + 256u) * (uint64_t)sA : 0u;
   const uint64_t ratio = (want + max(N, 1u) - 1u) / max(N, 1u);
   const uint32_t r2 = (uint32_t)min<uint64_t>((uint64_t)ns, max(plain, ratio));
   uint32_t a2above;
@@ -1612,10 +1747,12 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 // candidate keys are loaded together; counts and list positions come from ballots, and each chunk
 // of 64 candidates reserves its list space with one atomic.
 // Top-k candidate retry, one wavefront per row: the row's keys are read again from acc and every
-// key >= A2 becomes a candidate in the row's slot, in index order; those >= A (the first
-// candidates) are certain winners, those in [A2, A) go to the segment's list.
+// key > A2 becomes a candidate, in index order, in the row's static slot or, if more, in entries
+// reserved in the overflow pool; those >= A (the first candidates) are certain winners, those in
+// (A2, A) go to the segment's list, and the keys equal to A2 are counted (ties, taken by index if
+// the list falls short).  A row or a list that does not fit marks the segment for the exact path.
 __device__ __forceinline__ void collect_retry(const Tables& T, const WSel& ws, const Batch& BT, uint32_t row, int l,
-                                              const uint32_t* R) {
+                                              uint32_t* R) {
   const uint32_t lane = threadIdx.x & 63;
   const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
   uint32_t o = 0, e_ = (uint32_t)T.d, tb = row * kTile;
@@ -1627,39 +1764,63 @@ __device__ __forceinline__ void collect_retry(const Tables& T, const WSel& ws, c
   }
   const uint32_t lo = max(o, tb), hi = min(e_, tb + kTile);
   const uint32_t A = R[R_A], A2 = R[R_A2];
-  const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
-  uint32_t* cidx = ws.cand_idx + (size_t)row * kTile;
-  float* cval = ws.cand_val + (size_t)row * kTile;
-  uint32_t* ckey = ws.cand_key + (size_t)row * kTile;
-  uint32_t n = 0, na = 0;
+  const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists, lq = T.seg_lq[l];
+  const size_t sb = sublist_base(T, l, c);
+  // pass 1: how many (above A2, and equal)
+  uint32_t n = 0, nt = 0;
+  for (uint32_t i0 = lo; i0 < hi; i0 += 64) {
+    const uint32_t i = i0 + lane;
+    const uint32_t k = i < hi ? mag_key(acc[i]) : 0u;
+    n += (uint32_t)__popcll(__ballot(i < hi && k > A2));
+    nt += (uint32_t)__popcll(__ballot(i < hi && k == A2));
+  }
+  if (lane == 0) ws.rtie[row] = nt;
+  uint32_t cb, scap;
+  static_slot(T, ws, row, cb, scap);
+  if (n > scap) {
+    uint32_t at = 0;
+    if (lane == 0) at = pool_reserve(ws, row, n);
+    cb = __shfl(at, 0, 64);
+  }
+  if (lane == 0) ws.coff[row] = cb;
+  if (cb == kDropped) {
+    if (lane == 0) atomicOr(&R[R_OVF], 1u);
+    return;
+  }
+  // pass 2: the candidates and the list
+  uint32_t* cidx = ws.cand_idx + cb;
+  float* cval = ws.cand_val + cb;
+  uint32_t* ckey = ws.cand_key + cb;
+  uint32_t m = 0, na = 0;
   for (uint32_t i0 = lo; i0 < hi; i0 += 64) {
     const uint32_t i = i0 + lane;
     const float v = i < hi ? acc[i] : 0.0f;
     const uint32_t key = mag_key(v);
-    const bool take = i < hi && key >= A2, cert = take && key >= A, lst = take && !cert;
+    const bool take = i < hi && key > A2, cert = take && key >= A, lst = take && !cert;
     const uint64_t bt = __ballot(take), bl = __ballot(lst);
     if (take) {
-      const uint32_t pos = n + lanes_below(bt);
+      const uint32_t pos = m + lanes_below(bt);
       cidx[pos] = i;
       cval[pos] = v;
       ckey[pos] = key;
     }
-    n += (uint32_t)__popcll(bt);
+    m += (uint32_t)__popcll(bt);
     na += (uint32_t)__popcll(__ballot(cert));
     const uint32_t nl = (uint32_t)__popcll(bl);
     if (nl) {
       uint32_t base = 0;
       if (lane == 0) base = atomicAdd(lcnt_of(ws, l, c), nl);
       base = __shfl(base, 0, 64);
-      if (lst) {
-        const size_t p = sublist_pos(r0, c, base + lanes_below(bl));
+      const uint32_t t = base + lanes_below(bl);
+      if (lst && t < lq) {  // a full sub-list is seen by k_select (its count exceeds lq)
+        const size_t p = sb + t;
         ws.list_key[p] = key;
         ws.list_idx[p] = i;
       }
     }
   }
   if (lane == 0) {
-    ws.counts[row] = n;
+    ws.counts[row] = m;
     ws.rcnt[row] = na;
   }
 }
@@ -1670,20 +1831,24 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * kCollectRows;
   int ls[kCollectRows];
-  uint32_t cnts[kCollectRows], k0[kCollectRows];
+  uint32_t cnts[kCollectRows], cofs[kCollectRows], k0[kCollectRows];
 #pragma unroll
   for (uint32_t r = 0; r < kCollectRows; ++r) {
     const uint32_t row = min(row0 + r, (uint32_t)T.nrows - 1u);
     ls[r] = T.L == 1 ? 0 : T.row_seg[row];  // one segment: no load before the segment's record
     cnts[r] = ws.counts[row];
-    k0[r] = ws.cand_key[(size_t)row * kTile + lane];  // the first 64 keys (past the count: unused)
+    cofs[r] = ws.coff[row];
+    // one segment: the first 64 keys from the row's static slot, in the same round trip (used if
+    // the row's candidates are there; past the count: unused, and not loaded past the slot)
+    const uint32_t cap0 = min(ws.S, (uint32_t)T.d - row * kTile);
+    k0[r] = T.L == 1 && lane < cap0 ? ws.cand_key[(size_t)row * ws.S + lane] : 0u;
   }
 #pragma unroll
   for (uint32_t r = 0; r < kCollectRows; ++r) {
     const uint32_t row = row0 + r;
     if (row >= (uint32_t)T.nrows) break;
     const int l = ls[r];
-    const uint32_t* R = res_of(ws, l);
+    uint32_t* R = res_of(ws, l);
     uint32_t A = 0, sh = 0, B = 0, ulo = 0;
     if constexpr (KIND == 0) {
       if (R[R_SLOW] || R[R_MODE]) continue;
@@ -1697,6 +1862,8 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
     } else {
       ulo = T.seg_ulo[l];
     }
+    const uint32_t co = row_entry(T, ws, row, cnts[r], cofs[r]);
+    if (co == kDropped) continue;  // the segment takes the exact path
     // class: 2 = certain winner, 1 = undecided (listed), 0 = loses
     auto cls = [&](uint32_t k) -> uint32_t {
       if constexpr (KIND == 0) {
@@ -1706,34 +1873,37 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
         return ~k < ulo ? 2u : 1u;
       }
     };
-    const bool tie_bin = KIND == 0 && B == 0;  // the threshold bin is the single key A: count, do not list
+    // tie bin (the threshold bin is the key A alone, whose elements the pass only counted): every
+    // stored candidate is a certain winner and nothing is listed
+    const bool tie_bin = KIND == 0 && B == 0;
     const uint32_t cnt = cnts[r];
-    const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
-    const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
-    const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists;
-    uint32_t na = 0, ne = 0;
+    const uint32_t* ck = ws.cand_key + co;
+    const uint32_t* ci = ws.cand_idx + co;
+    const bool k0_ok = T.L == 1 && co == row * ws.S;
+    const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists, lq = T.seg_lq[l];
+    const size_t sb = sublist_base(T, l, c);
+    uint32_t na = 0;
+    uint32_t kc = k0_ok ? k0[r] : (lane < cnt ? ck[lane] : 0u);
     for (uint32_t j0 = 0; j0 < cnt; j0 += 64) {
       const uint32_t j = j0 + lane;
-      const uint32_t k = j0 == 0 ? k0[r] : (j < cnt ? ck[j] : 0u);
-      const uint32_t cl = j < cnt ? cls(k) : 0u;
+      const uint32_t k = kc;
+      if (j0 + 64 < cnt) kc = j + 64 < cnt ? ck[j + 64] : 0u;  // the next chunk's keys, in flight
+      const uint32_t cl = j < cnt ? (tie_bin ? 2u : cls(k)) : 0u;
       na += (uint32_t)__popcll(__ballot(cl == 2u));
       const uint64_t bu = __ballot(cl == 1u);
       const uint32_t nu = (uint32_t)__popcll(bu);
-      ne += nu;
-      if (tie_bin || nu == 0) continue;
+      if (nu == 0) continue;
       uint32_t base = 0;
       if (lane == 0) base = atomicAdd(lcnt_of(ws, l, c), nu);
       base = __shfl(base, 0, 64);
-      if (cl == 1u) {
-        const size_t p = sublist_pos(r0, c, base + lanes_below(bu));
+      const uint32_t t = base + lanes_below(bu);
+      if (cl == 1u && t < lq) {  // a full sub-list is seen by k_select (its count exceeds lq)
+        const size_t p = sb + t;
         ws.list_key[p] = k;
         ws.list_idx[p] = ci[j];
       }
     }
-    if (lane == 0) {
-      ws.rcnt[row] = na;
-      if (tie_bin) ws.rtie[row] = ne;
-    }
+    if (lane == 0) ws.rcnt[row] = na;
   }
 }
 
@@ -1888,23 +2058,33 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   const uint32_t* cc = ws.counts + r0;
   // round trip 1: record, sub-list sizes, row counts
   bool slow = false, listed = true;
-  uint32_t need = 0, mU = 0, exU = 0;
+  uint32_t need = 0, mU = 0, exU = 0, ovf = 0;
   if constexpr (KIND == 0) {
     slow = R[R_SLOW] != 0;
     listed = R[R_MODE] == 0;
     need = R[R_NEED];
+    ovf = R[R_OVF];
   }
   const bool direct = KIND == 1 && T.rk_direct;
+  const uint32_t lq = T.seg_lq[l];
   uint32_t lc[kSubLists];
 #pragma unroll
   for (int c = 0; c < kSubLists; ++c) lc[c] = direct ? 0u : *lcnt_of(ws, l, (uint32_t)c);
+  bool lfull = false;  // a sub-list overflowed its region
+#pragma unroll
+  for (int c = 0; c < kSubLists; ++c) lfull |= lc[c] > lq;
+  // top-k candidate retry whose list holds fewer than the `need` winners: every listed candidate
+  // wins, and the rest are the first elements equal to A2 (counted per row, not stored)
+  bool retry_ties = false;
   if constexpr (KIND == 0) {
-    // a candidate retry whose list still cannot give the `need` winners: the exact path
-    if (!slow && listed && R[R_RETRY]) {
+    // a row or a sub-list that did not fit the workspace: the exact path
+    if (!slow) {
       uint32_t m = 0;
 #pragma unroll
       for (int c = 0; c < kSubLists; ++c) m += lc[c];
-      if (m < need) {
+      retry_ties = listed && R[R_RETRY] && m < need;
+      if (retry_ties) need -= m;
+      if (ovf || (listed && lfull)) {
         slow = true;
         __syncthreads();  // every thread has read R_SLOW before it is set
         if (threadIdx.x == 0) {
@@ -1918,31 +2098,48 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   // coalesced strided loads there, not in per-thread runs (one workgroup reading 244,141 rows in
   // runs of 238 per thread took 0.44 ms at 1e9 elements)
   const bool strided = KIND == 1 && !direct && BIG;
-  uint32_t cr[kPer], cn[kPer];
+  // random-k: the rows' first pool entries (one segment: the static slot, r * S, unless the row
+  // holds more candidates than it, so only those rows' entries are loaded)
+  const uint32_t* ro = ws.coff + r0;
+  auto first_entry = [&](uint32_t x, uint32_t cnt) -> uint32_t {
+    const uint32_t row = r0 + x;
+    return cnt > min(ws.S, (uint32_t)T.d - row * kTile) ? ro[x] : row * ws.S;
+  };
+  uint32_t cr[kPer], cn[kPer], co[kPer];
 #pragma unroll
   for (uint32_t x = 0; x < kPer; ++x) {
     cr[x] = !strided && a + x < b ? rc[a + x] : 0u;
     cn[x] = !strided && a + x < b ? cc[a + x] : 0u;
+    co[x] = KIND == 1 && T.L > 1 && !strided && a + x < b ? ro[a + x] : 0u;
+  }
+  if (KIND == 1 && T.L == 1 && !strided) {
+#pragma unroll
+    for (uint32_t x = 0; x < kPer; ++x)
+      if (a + x < b) co[x] = first_entry(a + x, cn[x]);
   }
   if constexpr (KIND == 1) {
     // random-k: the certain winners S (keys below ulo) and the candidates N decide whether the
-    // window [ulo, tau) holds the k_l-th smallest key
-    // (direct lists: also the rows whose undecided candidates overflowed their pair slot)
+    // window [ulo, tau) holds the k_l-th smallest key (also counted: rows whose candidates did not
+    // fit the workspace)
     uint32_t sv[3] = {0u, 0u, 0u};
     if (strided) {
       constexpr uint32_t kU = 8;
       for (uint32_t x0 = threadIdx.x; x0 < nr; x0 += kU * kSelNT) {
-        uint32_t ra[kU], ca[kU];
+        uint32_t ra[kU], ca[kU], oa[kU];
 #pragma unroll
         for (uint32_t u = 0; u < kU; ++u) {
           const uint32_t x = x0 + u * kSelNT;
           ra[u] = x < nr ? rc[x] : 0u;
           ca[u] = x < nr ? cc[x] : 0u;
+          oa[u] = x < nr && T.L > 1 ? ro[x] : 0u;
         }
 #pragma unroll
         for (uint32_t u = 0; u < kU; ++u) {
+          const uint32_t x = x0 + u * kSelNT;
+          if (T.L == 1 && x < nr) oa[u] = first_entry(x, ca[u]);
           sv[0] += ra[u];
           sv[1] += ca[u];
+          sv[2] += oa[u] == kDropped ? 1u : 0u;
         }
       }
     } else {
@@ -1950,18 +2147,21 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       for (uint32_t x = 0; x < kPer; ++x) {
         sv[0] += cr[x];
         sv[1] += cn[x];
-        sv[2] += cn[x] - cr[x] > kRowPairs ? 1u : 0u;
+        sv[2] += co[x] == kDropped ? 1u : 0u;
       }
       for (uint32_t x = a + kPer; x < b; ++x) {
+        const uint32_t c = cc[x];
         sv[0] += rc[x];
-        sv[1] += cc[x];
+        sv[1] += c;
+        sv[2] += (T.L == 1 ? first_entry(x, c) : ro[x]) == kDropped ? 1u : 0u;
       }
     }
     uint32_t ex[3], tot[3];
     block_excl_scan_n<kSelNT, 3>(sv, lds, ex, tot);
     const uint32_t S = tot[0], N = tot[1];
-    // direct lists: the rows' undecided candidates (counts - certain) must fit the LDS list
-    slow = S > kl || N < kl || (direct && (N - S > kListLds || tot[2] != 0));
+    // direct lists: the rows' undecided candidates (counts - certain) must fit the LDS list;
+    // collected lists: every sub-list its region
+    slow = S > kl || N < kl || tot[2] != 0 || (direct ? N - S > kListLds : lfull);
     need = kl - S;
     mU = N - S;
     exU = ex[1] - ex[0];
@@ -1975,10 +2175,13 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       if (direct && e_zero) {
         // the streaming pass stored +0 at the certain winners (keys below ulo); the exact path needs
         // acc there: every certain winner is a candidate, whose value its row slot keeps
+        // (a row whose candidates did not fit stored acc there itself)
         const uint32_t ulo = T.seg_ulo[l];
-        for (uint32_t x = a; x < b; ++x) {
-          const size_t sl = (size_t)(r0 + x) * kTile;
-          const uint32_t cnt = ws.counts[r0 + x];
+#pragma unroll
+        for (uint32_t x = 0; x < kPer; ++x) {
+          if (a + x >= b || co[x] == kDropped) continue;
+          const size_t sl = co[x];
+          const uint32_t cnt = cn[x];
           for (uint32_t j = 0; j < cnt; ++j)
             if (~ws.cand_key[sl + j] < ulo) e_zero[ws.cand_idx[sl + j]] = ws.cand_val[sl + j];
         }
@@ -1991,11 +2194,14 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   }
   const bool rows_lds = nr <= kRowsLds;
   bool tie = false;
-  if constexpr (KIND == 0) tie = listed && R[R_B] == 0;
+  if constexpr (KIND == 0) tie = listed && (R[R_B] == 0 || retry_ties);
   if (tie) {
-    // The threshold bin is the key A alone: the first `need` candidates equal to A, in index
-    // order, win.  Rows hold their candidates in index order, so a scan of the rows' tie counts
-    // finds the row of the last winner, and one pass over that row finds the winner itself.
+    // The threshold bin is the key A alone, whose elements the streaming pass counted per row but
+    // did not store (a retry: the key A2, counted by k_collect): every stored candidate wins, and
+    // the first `need` of the elements equal to it, in index order.  A scan of the rows' tie counts
+    // finds the row of the last winner, and one pass over that row's elements in acc the winner
+    // itself.  The rows with winning ties are emitted from acc (all their elements are scanned
+    // there: counts = the row's length, flagged kAccRow).
     __shared__ uint32_t s_row, s_rank;
     const uint32_t* rt = ws.rtie + r0;
     uint32_t tl[kPer], st = 0;
@@ -2007,13 +2213,32 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     for (uint32_t x = a + kPer; x < b; ++x) st += rt[x];
     uint32_t totT;
     uint32_t before = block_excl_scan<kSelNT>(st, lds, totT);
+    if (totT < need) {  // a retry with too few ties (the tie bin itself holds at least `need`)
+      if (threadIdx.x == 0) {
+        R[R_SLOW] = 1u;
+        atomicOr(ws.diag, kDiagSlowPath);
+      }
+      slow_select<KIND>(T, l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
+      return;
+    }
     uint32_t* rcw = ws.rcnt + r0;
+    if (retry_ties) {
+      // a retry counted only its certain winners per row: all the row's candidates win here
+#pragma unroll
+      for (uint32_t x = 0; x < kPer; ++x) cr[x] = cn[x];
+      for (uint32_t x = a + kPer; x < b; ++x) rcw[x] = cc[x];
+    }
     for (uint32_t x = a; x < b; ++x) {
       const uint32_t t = x - a < kPer ? tl[x - a] : rt[x];
       const uint32_t take = min(t, need > before ? need - before : 0u);
       if (before < need && need <= before + t) {
         s_row = x;
         s_rank = need - before;
+      }
+      if (take) {
+        uint32_t lo, hi;
+        row_bounds(T, r0 + x, lo, hi);
+        ws.counts[r0 + x] = (hi - lo) | kAccRow;
       }
       if (x - a < kPer) {
 #pragma unroll
@@ -2025,11 +2250,13 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       before += t;
     }
     __syncthreads();
-    const uint32_t row = r0 + s_row;
-    const uint32_t p = block_nth_equal(ws.cand_key + (size_t)row * kTile, ws.counts[row], R[R_A], s_rank, lds);
+    uint32_t lo, hi;
+    row_bounds(T, r0 + s_row, lo, hi);
+    const uint32_t A = retry_ties ? R[R_A2] : R[R_A];
+    const uint32_t p = block_nth_equal(AccKeys{data + lo}, hi - lo, A, s_rank, lds);
     if (threadIdx.x == 0) {
-      R[R_T] = R[R_A];
-      R[R_IT] = ws.cand_idx[(size_t)row * kTile + p] + 1u;
+      R[R_T] = A;
+      R[R_IT] = lo + p + 1u;
     }
   }
   if (listed && !tie) {
@@ -2037,7 +2264,8 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     SubLists lk, li;
     lk.arr = ws.list_key;
     li.arr = ws.list_idx;
-    lk.r0 = li.r0 = r0;
+    lk.base = li.base = T.seg_lbase[l];
+    lk.q = li.q = lq;
     uint32_t m = 0;
 #pragma unroll
     for (int c = 0; c < kSubLists; ++c) {
@@ -2049,13 +2277,13 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     const bool in_lds = m <= kListLds;
     if (direct) {
       // round trip 2 (direct lists; every row of the segment is one of kPer per thread): each
-      // thread notes (row, slot) of its rows' undecided candidates at their list positions, then
-      // the pairs are fetched, all loads in flight together
+      // thread notes the pool entries of its rows' undecided candidates at their list positions,
+      // then the pairs are fetched, all loads in flight together
       uint32_t f = exU;
 #pragma unroll
       for (uint32_t x = 0; x < kPer; ++x) {
         if (a + x < b)
-          for (uint32_t t = 0; t < cn[x] - cr[x]; ++t) s_key[f++] = ((a + x) << 12) | t;
+          for (uint32_t t = 0; t < cn[x] - cr[x]; ++t) s_key[f++] = co[x] + t;
       }
       __syncthreads();
       for (uint32_t f0 = 0; f0 < m; f0 += (uint32_t)kSelNT * 4u) {
@@ -2065,8 +2293,8 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
           const uint32_t fu = f0 + (uint32_t)u * kSelNT + threadIdx.x;
           pr[u] = make_uint2(0u, 0u);
           if (fu < m) {
-            const uint32_t rs = s_key[fu];
-            pr[u] = row_pairs(ws, r0 + (rs >> 12))[rs & 0xFFFu];
+            const uint32_t at = s_key[fu];
+            pr[u] = ws.pairs[at];
           }
         }
 #pragma unroll
@@ -2166,15 +2394,26 @@ __global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws0, Batch BT) 
   const int l = T.L == 1 ? 0 : T.row_seg[row];
   const uint32_t* R = res_of(ws, l);
   if (R[R_SLOW]) return;
-  const uint32_t cnt = ws.counts[row];
+  const uint32_t cw = ws.counts[row], cnt = cw & ~kAccRow;
+  const uint32_t co = row_entry(T, ws, row, cnt, ws.coff[row]);
   uint32_t won = 0;
   if (KIND == 1 || R[R_MODE] == 0) {
     const uint32_t Tk = R[R_T], IT = R[R_IT];
-    const uint32_t* ck = ws.cand_key + (size_t)row * kTile;
-    const uint32_t* ci = ws.cand_idx + (size_t)row * kTile;
-    for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
-      const uint32_t k = ck[j];
-      won += (k > Tk || (k == Tk && ci[j] < IT)) ? 1u : 0u;
+    if (KIND == 0 && (cw & kAccRow)) {  // winning ties: the row's elements in acc
+      const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
+      uint32_t lo, hi;
+      row_bounds(T, row, lo, hi);
+      for (uint32_t i = lo + threadIdx.x; i < hi; i += kNT) {
+        const uint32_t k = mag_key(acc[i]);
+        won += (k > Tk || (k == Tk && i < IT)) ? 1u : 0u;
+      }
+    } else {
+      const uint32_t* ck = ws.cand_key + co;
+      const uint32_t* ci = ws.cand_idx + co;
+      for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
+        const uint32_t k = ck[j];
+        won += (k > Tk || (k == Tk && ci[j] < IT)) ? 1u : 0u;
+      }
     }
   } else {
     won = threadIdx.x == 0 ? cnt : 0u;
@@ -2244,8 +2483,10 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
 // the current one is written.  A winner's position is its row's offset plus the row's winners
 // before it: earlier passes (kept by the row's lane) and a ballot count over the row's lanes in
 // this pass.  RW = 16 for random-k (a few candidates per row); for top-k, whose rows in the layers
-// of largest magnitude hold hundreds, 1 for one or a few workers and 4 for a batch.
-template <uint32_t RW>
+// of largest magnitude hold hundreds, 1 for one or a few workers and 4 for a batch.  A top-k row
+// with winning ties (flagged kAccRow) takes its elements in acc as its candidates.  The step's
+// last kernel, it also clears the overflow pool's counters for the next step.
+template <uint32_t RW, bool ACC_ROWS>
 __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT,
                                               int certain_zeroed) {
   static_assert(RW >= 1 && RW <= 64 && (RW & (RW - 1)) == 0, "one lane per row, a power of two");
@@ -2257,86 +2498,107 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
   const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * RW;
   if (row0 >= (uint32_t)T.nrows) return;
   // lane j < RW: row row0 + j (rows past the end and rows of exact-path segments count 0)
+  if (blockIdx.x == 0 && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
   const uint32_t myrow = row0 + lane;
   const bool has_row = lane < RW && myrow < (uint32_t)T.nrows;
-  uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, ulo = 0;
+  uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, ulo = 0, co = 0, in_acc = 0;
   if (has_row) {
     const int l = T.L == 1 ? 0 : T.row_seg[myrow];  // one segment: no load before the record
     const uint32_t* R = res_of(ws, l);
     cnt = ws.counts[myrow];
+    co = ws.coff[myrow];
     off = ws.roff[myrow];
     pend = (uint32_t)T.seg_P[l + 1];
     ulo = certain_zeroed ? T.seg_ulo[l] : 0u;
-    if (R[R_SLOW]) cnt = 0;
     Tk = R[R_T];
     IT = R[R_IT];
+    if (ACC_ROWS && (cnt & kAccRow)) {  // the row's first element in acc
+      uint32_t hi;
+      row_bounds(T, myrow, co, hi);
+      cnt &= ~kAccRow;
+      in_acc = 1u;
+    } else {
+      co = row_entry(T, ws, myrow, cnt, co);
+    }
+    if (R[R_SLOW]) cnt = 0;
   }
+  const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
   const uint32_t incl = wave_incl_scan(cnt);
   const uint32_t total = __shfl(incl, 63, 64);
   const uint32_t pre = incl - cnt;  // this lane's row: first flattened candidate
-  // flattened candidate f -> its row lane r (the last row lane with pre_r <= f; for f < total that
-  // row's count is nonzero, so f lies inside it) and its slot
-  auto locate = [&](uint32_t f, uint32_t& r, size_t& sl) {
-    r = 0;
+  // The wave's loop; the form that tests for rows emitted from acc runs only in a wave holding one.
+  auto run = [&](auto acc_rows) {
+    constexpr bool AR = decltype(acc_rows)::value;
+    // flattened candidate f -> its row lane r (the last row lane with pre_r <= f; for f < total that
+    // row's count is nonzero, so f lies inside it) and its entry: a pool entry, or an element of acc
+    auto locate = [&](uint32_t f, uint32_t& r, uint32_t& sl, bool& ia) {
+      r = 0;
 #pragma unroll
-    for (uint32_t step = RW / 2; step >= 1; step >>= 1) {
-      const uint32_t p = __shfl(pre, (int)(r + step), 64);
-      if (f < total && p <= f) r += step;
-    }
-    sl = (size_t)(row0 + r) * kTile + (f - __shfl(pre, (int)r, 64));
-  };
-  uint32_t done = 0;  // this lane's row: winners emitted in earlier passes
-  uint32_t r;
-  size_t sl;
-  locate(lane, r, sl);
-  uint32_t k = 0, i = 0;
-  float v = 0.0f;
-  if (lane < total) {
-    k = ws.cand_key[sl];
-    i = ws.cand_idx[sl];
-    v = ws.cand_val[sl];
-  }
-  for (uint32_t f0 = 0; f0 < total; f0 += 64) {
-    const uint32_t f = f0 + lane;
-    const bool in = f < total;
-    const uint32_t rpre = __shfl(pre, (int)r, 64);
-    const uint32_t rTk = __shfl(Tk, (int)r, 64), rIT = __shfl(IT, (int)r, 64);
-    const uint32_t roffr = __shfl(off, (int)r, 64) + __shfl(done, (int)r, 64);
-    const uint32_t rpend = __shfl(pend, (int)r, 64), rulo = __shfl(ulo, (int)r, 64);
-    const uint32_t ck = k, ci = i;
-    const float cv = v;
-    // the next pass's candidates, in flight while this pass is written
-    uint32_t rn = 0;
-    size_t sn = 0;
-    locate(f + 64, rn, sn);
-    if (f + 64 < total) {
-      k = ws.cand_key[sn];
-      i = ws.cand_idx[sn];
-      v = ws.cand_val[sn];
-    }
-    const bool win = in && (ck > rTk || (ck == rTk && ci < rIT));
-    const uint64_t bw = __ballot(win);
-    // this pass's lanes of row r before this lane: [lo_r, lane)
-    const uint32_t lo_r = rpre > f0 ? rpre - f0 : 0u;
-    const uint64_t below = (lane ? (~0ull >> (64 - lane)) : 0ull) & ~((lo_r ? (~0ull >> (64 - lo_r)) : 0ull));
-    const uint32_t pos = roffr + (uint32_t)__popcll(bw & below);
-    if (win && pos < rpend) {
-      out_idx[pos] = ci;
-      if (out_val) out_val[pos] = cv;
-      // random-k, direct lists: the streaming pass already zeroed e at the certain winners (key' of
-      // a key below ulo)
-      if (e_zero && !(~ck < rulo)) e_zero[ci] = 0.0f;
-    }
-    // each row lane adds its winners of this pass
-    if (has_row) {
-      const uint32_t a = pre > f0 ? pre - f0 : 0u, z = incl > f0 ? min(incl - f0, 64u) : 0u;
-      if (z > a) {
-        const uint64_t m = (z == 64 ? ~0ull : (~0ull >> (64 - z))) & ~(a ? (~0ull >> (64 - a)) : 0ull);
-        done += (uint32_t)__popcll(bw & m);
+      for (uint32_t step = RW / 2; step >= 1; step >>= 1) {
+        const uint32_t p = __shfl(pre, (int)(r + step), 64);
+        if (f < total && p <= f) r += step;
       }
+      sl = __shfl(co, (int)r, 64) + (f - __shfl(pre, (int)r, 64));
+      ia = AR && __shfl(in_acc, (int)r, 64) != 0u;
+    };
+    auto fetch = [&](uint32_t sl, bool ia, uint32_t& k, uint32_t& i, float& v) {
+      if (AR && ia) {
+        v = acc[sl];
+        k = mag_key(v);
+        i = sl;
+      } else {
+        k = ws.cand_key[sl];
+        i = ws.cand_idx[sl];
+        v = ws.cand_val[sl];
+      }
+    };
+    uint32_t done = 0;  // this lane's row: winners emitted in earlier passes
+    uint32_t r, sl;
+    bool ia;
+    locate(lane, r, sl, ia);
+    uint32_t k = 0, i = 0;
+    float v = 0.0f;
+    if (lane < total) fetch(sl, ia, k, i, v);
+    for (uint32_t f0 = 0; f0 < total; f0 += 64) {
+      const uint32_t f = f0 + lane;
+      const bool in = f < total;
+      const uint32_t rpre = __shfl(pre, (int)r, 64);
+      const uint32_t rTk = __shfl(Tk, (int)r, 64), rIT = __shfl(IT, (int)r, 64);
+      const uint32_t roffr = __shfl(off, (int)r, 64) + __shfl(done, (int)r, 64);
+      const uint32_t rpend = __shfl(pend, (int)r, 64), rulo = __shfl(ulo, (int)r, 64);
+      const uint32_t ck = k, ci = i;
+      const float cv = v;
+      // the next pass's candidates, in flight while this pass is written
+      uint32_t rn = 0, sn = 0;
+      bool ian = false;
+      locate(f + 64, rn, sn, ian);
+      if (f + 64 < total) fetch(sn, ian, k, i, v);
+      const bool win = in && (ck > rTk || (ck == rTk && ci < rIT));
+      const uint64_t bw = __ballot(win);
+      // this pass's lanes of row r before this lane: [lo_r, lane)
+      const uint32_t lo_r = rpre > f0 ? rpre - f0 : 0u;
+      const uint64_t below = (lane ? (~0ull >> (64 - lane)) : 0ull) & ~((lo_r ? (~0ull >> (64 - lo_r)) : 0ull));
+      const uint32_t pos = roffr + (uint32_t)__popcll(bw & below);
+      if (win && pos < rpend) {
+        out_idx[pos] = ci;
+        if (out_val) out_val[pos] = cv;
+        // random-k, direct lists: the streaming pass already zeroed e at the certain winners (key' of
+        // a key below ulo)
+        if (e_zero && !(~ck < rulo)) e_zero[ci] = 0.0f;
+      }
+      // each row lane adds its winners of this pass
+      if (has_row) {
+        const uint32_t a = pre > f0 ? pre - f0 : 0u, z = incl > f0 ? min(incl - f0, 64u) : 0u;
+        if (z > a) {
+          const uint64_t m = (z == 64 ? ~0ull : (~0ull >> (64 - z))) & ~(a ? (~0ull >> (64 - a)) : 0ull);
+          done += (uint32_t)__popcll(bw & m);
+        }
+      }
+      r = rn;
     }
-    r = rn;
-  }
+  };
+  if (ACC_ROWS && __ballot(in_acc != 0u)) run(std::true_type{});
+  else run(std::false_type{});
 }
 
 }  // namespace efs

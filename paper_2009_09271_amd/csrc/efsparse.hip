@@ -47,8 +47,9 @@ struct Blob {
 };
 
 struct WsLayout {
-  size_t diag = 0, res = 0, hist = 0, samp = 0, counts = 0, rcnt = 0, roff = 0, rtie = 0, lcnt = 0, cand_idx = 0, cand_val = 0,
-         cand_key = 0, list_idx = 0, list_key = 0, total = 0;
+  size_t diag = 0, res = 0, hist = 0, samp = 0, counts = 0, rcnt = 0, roff = 0, rtie = 0, lcnt = 0, coff = 0, pcnt = 0,
+         cand_idx = 0, cand_val = 0, cand_key = 0, list_idx = 0, list_key = 0, total = 0;
+  uint32_t S = 0, capB = 0;
 };
 
 }  // namespace
@@ -59,13 +60,19 @@ struct ef_layout {
   double density = 0;
   int64_t block = 1;
   std::vector<int64_t> off64;
-  double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0, tk_retry = 1.0;
+  double rk_sigma = 6.0, rk_extra = 32.0, tk_sigma = 6.0, tk_extra = 8.0, tk_retry = 1.0, pool = 1.0;
 
   std::vector<int32_t> off, k, P, bl, nb, srank, urank, cbase, ro, csf, csl, rseg, runseg;
   std::vector<uint32_t> btile;  // block aggregate, multi-segment: (data tile, segment) pairs
   std::vector<uint32_t> rrec;   // multi-segment: per row (segment, its offset and end, tile base)
   std::vector<uint64_t> tau;
   std::vector<uint32_t> ulo;
+  std::vector<uint64_t> lbase;      // per segment: list region
+  std::vector<uint32_t> lq;         // entries per sub-list
+  std::vector<uint32_t> soff[2];    // per op (0 top-k, 1 random-k), per row: static slot start
+  uint32_t S[2] = {64, 64};         // per op, one segment: static slot entries per row (at most)
+  const uint32_t* dsoff[2] = {nullptr, nullptr};  // soff in the bound device tables
+  uint64_t pB[2] = {0, 0}, lists = 0;  // overflow pool entries per op (0 top-k, 1 random-k), list entries
   int64_t K = 0;
   int32_t nchunks = 0, nrows = 0, nruns = 0;
   bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
@@ -74,7 +81,7 @@ struct ef_layout {
 
   Blob blob;
   size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_runseg,
-      o_btile, o_rrec;
+      o_btile, o_rrec, o_lbase, o_lq, o_soff[2];
   Tables T{};
   bool bound = false;
   bool valid = false;  // build() completed (host memory for the tables was available)
@@ -166,6 +173,72 @@ void ef_layout::build() {
   }
   nrows = cbase[n];
   nruns = ro[n];
+  // Candidate pools.  Each row keeps up to S_l candidates in a static slot (S_l: the expected
+  // candidates of one of segment l's rows, plus a margin); a row with more reserves its entries in
+  // the overflow pool.  The pool is sized by the candidate bound of each segment,
+  // plus slack for the whole layout: top-k: the winners (exact segments) or the expected count
+  // above the sampled threshold, twice, plus eight k_l for a retry (which aims at 4 k_l + 256
+  // candidates); random-k: the binomial bound.  A row that does not fit sends its segment to the
+  // exact path (same result, slower).
+  {
+    uint64_t bt = 0, br = 0, lsum = 0;
+    std::vector<uint32_t> slot[2];  // per op, per segment: static slot entries per row
+    slot[0].assign(n, 64);
+    slot[1].assign(n, 64);
+    lbase.assign(n, 0);
+    lq.assign(n, 0);
+    for (int l = 0; l < n; ++l) {
+      const double dl = (double)(off64[l + 1] - off64[l]), kl = (double)k[l];
+      double et;
+      if (dl <= kSampleMax) {
+        et = kl;
+      } else {
+        const double ns = (double)((ro[l + 1] - ro[l]) * kSampleRun);
+        et = (double)srank[l] * dl / ns;
+      }
+      const uint64_t ct = dl <= kSampleMax ? (uint64_t)kl : (uint64_t)std::min(dl, std::ceil(2.0 * et + 8.0 * kl + 256.0));
+      const double mu = (double)tau[l] / 4294967296.0 * dl;
+      const uint64_t cr = (uint64_t)std::min(dl, std::ceil(mu + 8.0 * std::sqrt(mu) + 64.0));
+      // slots: mu + 4 sqrt(mu) + 32 for top-k's mean mu per row (its candidates above the sampled
+      // threshold, or the winners), mu + 8 sqrt(mu) + 32 for random-k's binomial count; multiples of
+      // 32 entries, at most a tile
+      const double nrl = (double)(cbase[l + 1] - cbase[l]);
+      auto round_slot = [](double x) {
+        return (uint32_t)std::min<double>(kTile, std::max(32.0, std::ceil(x / 32.0) * 32.0));
+      };
+      const double mt = (dl <= kSampleMax ? kl : std::min(dl, et)) / nrl;
+      const double mr = (double)tau[l] / 4294967296.0 * std::min(dl, (double)kTile);
+      slot[0][l] = round_slot(mt + 4.0 * std::sqrt(mt) + 32.0);
+      slot[1][l] = round_slot(mr + 8.0 * std::sqrt(mr) + 32.0);
+      bt += ct;
+      br += cr;
+      // lists: sub-list c takes the entries of the segment's rows c, c + 16, ...; each of the
+      // min(16, rows) sub-lists in use holds the segment's bound (up to 16 rows: one row each, at
+      // most a tile) or an eighth of it, at most the elements of its rows; a sub-list that
+      // overflows sends the segment to the exact path
+      // (scaled by the pool knob)
+      const uint64_t bl = std::max(ct, cr), nr = (uint64_t)(cbase[l + 1] - cbase[l]);
+      const uint64_t rows_cap = (nr + kSubLists - 1) / kSubLists * kTile;
+      const uint64_t q0 = nr <= kSubLists ? std::min<uint64_t>(bl, kTile) : std::min<uint64_t>(bl, (bl + 7) / 8 + 64);
+      const uint64_t q = std::min<uint64_t>(rows_cap, (uint64_t)std::ceil((double)q0 * pool));
+      lbase[l] = lsum;
+      lq[l] = (uint32_t)q;
+      lsum += q * std::min<uint64_t>(nr, kSubLists);
+    }
+    for (int o = 0; o < 2; ++o) {
+      S[o] = slot[o][0];
+      soff[o].assign(nrows + 1, 0);
+      for (int l = 0; l < n; ++l)
+        for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) {
+          const int64_t tb = (off64[l] / kTile + (r - cbase[l])) * kTile;
+          const int64_t len = std::min<int64_t>(off64[l + 1], tb + kTile) - std::max<int64_t>(off64[l], tb);
+          soff[o][r + 1] = soff[o][r] + (uint32_t)std::min<int64_t>(slot[o][l], len);
+        }
+    }
+    pB[0] = (uint64_t)std::ceil((double)(bt + 49152 + kPools * 4096) * pool / kPools) * kPools;
+    pB[1] = (uint64_t)std::ceil((double)(br + 49152 + kPools * 4096) * pool / kPools) * kPools;
+    lists = lsum;
+  }
   rseg.resize(nrows);
   for (int l = 0; l < n; ++l)
     for (int32_t r = cbase[l]; r < cbase[l + 1]; ++r) rseg[r] = l;
@@ -227,6 +300,10 @@ void ef_layout::build() {
   o_runseg = blob.add(runseg);
   o_btile = blob.add(btile);
   o_rrec = blob.add(rrec);
+  o_lbase = blob.add(lbase);
+  o_lq = blob.add(lq);
+  o_soff[0] = blob.add(soff[0]);
+  o_soff[1] = blob.add(soff[1]);
   bound = false;
 }
 
@@ -238,7 +315,17 @@ WsLayout ef_layout::ws_layout(int op) const {
     at = align_up(at + bytes, kAlign);
     return a;
   };
-  const size_t rows = (size_t)nrows, slots = rows * kTile;
+  const size_t rows = (size_t)nrows;
+  const int o = op == EF_OP_TOPK ? 0 : 1;
+  w.S = soff[o][rows];  // the static slots' total: the overflow pool starts there
+  // at most every element once more (a pass whose rows all overflow their static slots); entry
+  // positions are 32-bit: the pool ends below 2^32
+  const uint64_t every = ((uint64_t)d + kPools * 4096 + kPools - 1) / kPools * kPools;
+  w.capB = (uint32_t)std::min<uint64_t>({pB[o], every, (0xFFFFFFFEull - w.S) / kPools * kPools});
+  const size_t slots = (size_t)w.S + w.capB;  // candidate pool entries
+  // the segments' sub-lists; random-k's direct lists instead: a (key', index) pair for each pool
+  // entry, in the list_idx memory
+  const bool pairs = o == 1 && rk_direct;
   w.diag = take(16);
   w.res = take((size_t)L * kResWords * 4);
   w.hist = take((size_t)L * kHCopies * kHBins * 4);
@@ -248,11 +335,13 @@ WsLayout ef_layout::ws_layout(int op) const {
   w.roff = take(rows * 4);
   w.rtie = take(rows * 4);
   w.lcnt = take((size_t)L * kSubLists * kLineWords * 4);
+  w.coff = take(rows * 4);
+  w.pcnt = take((size_t)kPools * kLineWords * 4);
   w.cand_idx = take(slots * 4);
   w.cand_val = take(slots * 4);
   w.cand_key = take(slots * 4);
-  w.list_idx = take(slots * 4);
-  w.list_key = take(slots * 4);
+  w.list_idx = take(pairs ? slots * 8 : (size_t)lists * 4);
+  w.list_key = take(pairs ? 0 : (size_t)lists * 4);
   w.total = at;
   return w;
 }
@@ -271,11 +360,16 @@ WSel make_ws(const WsLayout& l, void* base) {
   w.roff = reinterpret_cast<uint32_t*>(b + l.roff);
   w.rtie = reinterpret_cast<uint32_t*>(b + l.rtie);
   w.lcnt = reinterpret_cast<uint32_t*>(b + l.lcnt);
+  w.coff = reinterpret_cast<uint32_t*>(b + l.coff);
+  w.pcnt = reinterpret_cast<uint32_t*>(b + l.pcnt);
+  w.pool0 = l.S;
+  w.capB = l.capB;
   w.cand_idx = reinterpret_cast<uint32_t*>(b + l.cand_idx);
   w.cand_val = reinterpret_cast<float*>(b + l.cand_val);
   w.cand_key = reinterpret_cast<uint32_t*>(b + l.cand_key);
   w.list_idx = reinterpret_cast<uint32_t*>(b + l.list_idx);
   w.list_key = reinterpret_cast<uint32_t*>(b + l.list_key);
+  w.pairs = reinterpret_cast<uint2*>(b + l.list_idx);
   return w;
 }
 
@@ -411,7 +505,12 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
   const dim3 blk(kNT), sblk(kSelNT), pblk(kSampleRun);
   auto g_at = [&](int w) -> const void* { return P.g ? P.g[w] : nullptr; };
   auto e_at = [&](int w) -> float* { return P.e ? P.e[w] : nullptr; };
-  auto ws_of = [&](int w) { return make_ws(wl, P.ws + (uint64_t)w * P.ws_stride); };
+  auto ws_of = [&](int w) {
+    WSel s = make_ws(wl, P.ws + (uint64_t)w * P.ws_stride);
+    s.soff = L->dsoff[KIND];
+    s.S = L->S[KIND];
+    return s;
+  };
   // the kernel-argument table of workers [c0, c0 + nw)
   auto batch_of = [&](int c0, int nw) {
     Batch b{};
@@ -497,9 +596,10 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     }
     EF_TRY(launched());
     const int cz = KIND == 1 && L->rk_direct && P.e ? 1 : 0;
-    if (emit_rw == 16u) EF_LAUNCH(k_emit<16>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
-    else if (emit_rw == 4u) EF_LAUNCH(k_emit<4>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
-    else EF_LAUNCH(k_emit<1>, egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    // (top-k rows with winning ties are emitted from acc)
+    if (emit_rw == 16u) EF_LAUNCH((k_emit<16, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else if (emit_rw == 4u) EF_LAUNCH((k_emit<4, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else EF_LAUNCH((k_emit<1, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
     EF_TRY(launched());
   }
   return EF_OK;
@@ -667,6 +767,10 @@ int ef_layout_tune(ef_layout* layout, int knob, double value) {
     case EF_TUNE_TOPK_SIGMA: layout->tk_sigma = value; break;
     case EF_TUNE_TOPK_EXTRA: layout->tk_extra = value; break;
     case EF_TUNE_TOPK_RETRY: layout->tk_retry = value; break;
+    case EF_TUNE_POOL:
+      if (value < 0.0) return EF_EINVAL;
+      layout->pool = value;
+      break;
     default: return EF_EINVAL;
   }
   // a failed rebuild leaves the layout unusable (every later call on it returns EF_EINVAL)
@@ -707,6 +811,10 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.row_rec = reinterpret_cast<const uint32_t*>(b + L->o_rrec);
   T.seg_tau = reinterpret_cast<const uint64_t*>(b + L->o_tau);
   T.seg_ulo = reinterpret_cast<const uint32_t*>(b + L->o_ulo);
+  T.seg_lbase = reinterpret_cast<const uint64_t*>(b + L->o_lbase);
+  T.seg_lq = reinterpret_cast<const uint32_t*>(b + L->o_lq);
+  L->dsoff[0] = reinterpret_cast<const uint32_t*>(b + L->o_soff[0]);
+  L->dsoff[1] = reinterpret_cast<const uint32_t*>(b + L->o_soff[1]);
   T.chunk_sf = reinterpret_cast<const int32_t*>(b + L->o_csf);
   T.chunk_sl = reinterpret_cast<const int32_t*>(b + L->o_csl);
   T.btile = reinterpret_cast<const uint32_t*>(b + L->o_btile);

@@ -107,8 +107,10 @@ def test_workspace_sizes():
     assert L.workspace_bytes(E.EF_OP_AGG_SPARSE, 8) >= 8 * (L.d // 8192 + 1) * 4
     assert L.workspace_bytes(E.EF_OP_AGG_SPARSE, 0) == 0
     assert L.workspace_bytes(99) == 0
-    # candidate slots cover every element
-    assert L.workspace_bytes(E.EF_OP_TOPK) >= 8 * L.d
+    # candidate pools sized by k and the rows, not by d: well under 2 bytes per element at 0.1 %
+    big = E.Layout(1 << 26, None, 0.001)
+    assert 0 < big.workspace_bytes(E.EF_OP_TOPK) < 2 * big.d
+    assert 0 < big.workspace_bytes(E.EF_OP_RANDK) < 2 * big.d
     assert E.lib().ef_workspace_diag_offset(L.handle, E.EF_OP_TOPK) == 0
     assert E.lib().ef_workspace_diag_offset(L.handle, E.EF_OP_RANDBLOCK) == ctypes.c_size_t(-1).value
 
@@ -119,6 +121,18 @@ def test_tune_rejects_bad_knobs():
     assert E.lib().ef_layout_tune(L.handle, 0, float("inf")) == E.EF_EINVAL
     assert E.lib().ef_layout_tune(L.handle, 0, 5.0) == E.EF_OK
     assert E.lib().ef_layout_tune(L.handle, E.EF_TUNE_TOPK_RETRY, 0.0) == E.EF_OK
+    assert E.lib().ef_layout_tune(L.handle, E.EF_TUNE_POOL, -1.0) == E.EF_EINVAL
+
+
+def test_pool_knob_scales_the_workspace():
+    """The candidate pool and lists follow the pool knob; 0 leaves the rows' static slots."""
+    sizes = []
+    for scale in (0.0, 1.0, 2.0):
+        L = E.Layout(1 << 24, [0, 1 << 20, 1 << 24], 0.01, tune={E.EF_TUNE_POOL: scale})
+        sizes.append((L.workspace_bytes(E.EF_OP_TOPK), L.workspace_bytes(E.EF_OP_RANDK)))
+    for op in range(2):
+        assert sizes[0][op] < sizes[1][op] < sizes[2][op]
+    assert sizes[0][0] < 2 * (1 << 24)  # static slots of 128 entries per 4096-element row, 12 B each
 
 
 def test_status_strings():

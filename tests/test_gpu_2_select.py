@@ -130,15 +130,45 @@ def test_randk_forced_slow_path():
 
 
 @pytest.mark.parametrize("offs", [[0, 4096], [0, 3, 4099, 9000]], ids=["one-row", "ragged"])
-def test_randk_row_list_overflow_takes_exact_path(offs):
-    """A window margin of 2000 around k_l = d_l / 2 makes every element of a 4096-element segment
-    undecided: more than a row's list slot holds, so the segment must take the exact path."""
+def test_randk_rows_wholly_undecided(offs):
+    """A window margin of 2000 around k_l = d_l / 2 makes nearly every element of a 4096-element
+    segment undecided: each row lists all of them from its own candidate entries, and the
+    selection over that list must be exact without the whole-segment path."""
     import paper_2009_09271_amd as E
-    announce("randk row list overflow", offs)
+    announce("randk rows wholly undecided", offs)
     c = Case(offs, 0.5, tune={E.EF_TUNE_RANDK_EXTRA: 2000.0})
     g, e = _inputs(c.d, 12)
     diag = _run_steps(c, "randk", [g, g], e, seed=79)
-    assert diag & E.DIAG_SLOW_PATH, "the exact path did not run"
+    assert not diag & E.DIAG_SLOW_PATH, f"diagnostics {diag:#x}"
+
+
+def _front_loaded(d, seed):
+    """Magnitudes 100x larger in the first quarter: its rows hold all of top-k's candidates."""
+    rng = np.random.default_rng(seed)
+    g = rng.standard_normal(d).astype(np.float32)
+    g[: d // 4] *= np.float32(100.0)
+    return g
+
+
+@pytest.mark.parametrize("kind,offs,rho,tune", [
+    ("topk", [0, 100000], 0.05, {}),
+    ("topk", [0, 5, 50000, 120000], 0.05, {}),
+    ("topk", [0, 3, 40000, 40001, 90001], 0.01, {"TOPK_SIGMA": -1e9}),
+    ("randk", [0, 1000000], 0.3, {"RANDK_EXTRA": 5000.0}),
+], ids=["topk-flat", "topk-two-large", "topk-retry", "randk-lists"])
+def test_pool_overflow_takes_exact_path(kind, offs, rho, tune):
+    """With the candidate pool and lists tuned to nothing, a row with more candidates than its
+    static slot (top-k: the pass or the retry) or any listed candidate (random-k, wide windows)
+    does not fit the workspace: its segment takes the exact whole-segment path, same result."""
+    import paper_2009_09271_amd as E
+    announce("pool overflow", kind, offs[-1], rho, tune)
+    t = {getattr(E, "EF_TUNE_" + k): v for k, v in tune.items()}
+    t[E.EF_TUNE_POOL] = 0.0
+    c = Case(offs, rho, tune=t)
+    assert c.L.workspace_bytes(E.EF_OP_TOPK if kind == "topk" else E.EF_OP_RANDK) < 12 * c.d
+    g = _front_loaded(c.d, 13)
+    diag = _run_steps(c, kind, [g, g * np.float32(0.5)], np.zeros(c.d, np.float32), seed=81)
+    assert diag & E.DIAG_SLOW_PATH, f"diagnostics {diag:#x}"
 
 
 def test_randk_every_element_a_candidate():
