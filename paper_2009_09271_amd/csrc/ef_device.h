@@ -44,8 +44,10 @@ enum : int {
   R_B = 7,      // candidate histogram: bin holding the k_l-th best candidate
   R_NEED = 8,   // winners still needed from bin R_B (retry: from the listed candidates)
   R_RETRY = 9,  // top-k: 1 when the segment's candidates fell short of k_l and are collected again
-  R_A2 = 10,    // top-k retry: the lower threshold; keys in [R_A2, R_A) are the listed candidates
-  R_OVF = 11,   // top-k: candidates or listed entries did not fit the workspace (the exact path runs)
+  R_A2 = 10,    // top-k retry: the lower threshold; keys in (R_A2, R_A) are the listed candidates,
+                //   keys equal to it are counted
+  R_OVF = 11,   // top-k: candidates did not fit the workspace (a retry collects them again, else the
+                //   exact path runs)
 };
 
 constexpr int kBtWords = 8;  // words per record of the block aggregate's (tile, segment) table

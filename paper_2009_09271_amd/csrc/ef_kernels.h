@@ -1348,12 +1348,14 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   __syncthreads();
   kmax = block_max_u32(kmax, lds);
   // Key edge of the rank-th largest sampled key: the lower (or upper) edge of its top-11-bit bin,
-  // refined by the next 11 bits when that bin holds many sampled keys (concentrated values).
+  // refined by the next 11 bits when that bin holds more than 64 sampled keys (concentrated
+  // values: an unrefined edge could take up to the whole bin's keys as candidates beyond the
+  // rank, which the candidate pool is not sized for).
   auto rank_edge = [&](uint32_t rank, bool upper) -> uint32_t {
     uint32_t above;
     const int bin = block_resolve<kSelNT>(hist, kHBins, rank, lds, above);
     if (bin < 0) return 0u;
-    if (hist[bin] <= ns / 8) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
+    if (hist[bin] <= 64u) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
     for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist2[b] = 0;
     __syncthreads();
     for_keys(sk, ns, [&](uint32_t, uint32_t k) {
@@ -1714,14 +1716,6 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
 #pragma unroll
     for (int x = 0; x < kHCopies; ++x) c[u][x] = gh[x * kHBins + u * kSelNT + threadIdx.x];
   if (mode != 0) return;
-  if (ovf) {  // a row's candidates did not fit the workspace: the exact path
-    if (threadIdx.x == 0) {
-      R[R_SLOW] = 1;
-      R[R_RETRY] = 0;
-      atomicOr(ws.diag, kDiagSlowPath);
-    }
-    return;
-  }
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
     uint32_t sum = 0;
@@ -1734,6 +1728,34 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
   uint32_t above;
   const int bin = block_resolve<kSelNT>(hist, kHBins, kl, lds, above);
   if (threadIdx.x < kSubLists) *lcnt_of(ws, l, threadIdx.x) = 0;
+  if (ovf) {
+    // A row's candidates did not fit the workspace (the sample put A far below the k_l-th key), but
+    // the histogram counted them all: the rows collect again the keys of bins >= B only (those
+    // above bin B are certain, bin B's are listed), as a retry (below) does.  With one segment the
+    // pool's parts start again from empty (every row is collected again).  The threshold bin being
+    // the key A itself, or the retry switched off: the exact path.
+    const uint32_t A = R[R_A], sh = R[R_SH];
+    if (bin < 1 || !T.tk_retry) {
+      if (threadIdx.x == 0) {
+        R[R_SLOW] = 1;
+        R[R_RETRY] = 0;
+        atomicOr(ws.diag, kDiagSlowPath);
+      }
+      return;
+    }
+    if (T.L == 1 && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
+    if (threadIdx.x == 0) {
+      const uint32_t b = (uint32_t)bin;
+      R[R_A2] = A + ((b - 1u) << sh);  // keys above it: bins >= B
+      R[R_A] = b < (uint32_t)kHBins - 1u ? A + 1u + (b << sh) : 0xFFFFFFFFu;  // first key of bin B + 1
+      R[R_NEED] = kl - above;
+      R[R_B] = 1u;  // not the tie bin: the listed candidates are ranked
+      R[R_RETRY] = 1u;
+      R[R_OVF] = 0u;
+      atomicOr(ws.diag, kDiagRetry);
+    }
+    return;
+  }
   if (bin >= 0) {
     if (threadIdx.x == 0) {
       R[R_B] = (uint32_t)bin;

@@ -171,6 +171,25 @@ def test_pool_overflow_takes_exact_path(kind, offs, rho, tune):
     assert diag & E.DIAG_SLOW_PATH, f"diagnostics {diag:#x}"
 
 
+def test_topk_pool_overflow_retries():
+    """Candidates crowded into a few rows overflow a small pool in the streaming pass; the
+    histogram still counted them all, so the rows collect again only the keys of the threshold bin
+    and above, which fit.  Each pool size must give the oracle's result; at least one of them must
+    take that retry without the exact path (the exact whole-segment path costs ~0.3 s at 1e8)."""
+    import paper_2009_09271_amd as E
+    d = 1 << 20
+    rng = np.random.default_rng(14)
+    g = rng.standard_normal(d).astype(np.float32)
+    g[: d // 16] *= np.float32(100.0)  # the winners lie in the first 16 rows
+    retried = []
+    for scale in (0.04, 0.06, 0.08, 0.1):
+        announce("topk pool overflow retry", scale)
+        c = Case([0, d], 0.01, tune={E.EF_TUNE_POOL: scale})
+        diag = _run_steps(c, "topk", [g], np.zeros(d, np.float32))
+        retried.append((scale, diag))
+    assert any(dg & E.DIAG_RETRY and not dg & E.DIAG_SLOW_PATH for _, dg in retried), retried
+
+
 def test_randk_every_element_a_candidate():
     import paper_2009_09271_amd as E
     announce("randk all candidates")
