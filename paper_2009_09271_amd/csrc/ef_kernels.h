@@ -1022,6 +1022,10 @@ constexpr uint32_t kSelPer = 8;        // rows per k_select thread held in regis
 constexpr uint32_t kHistDirect = 32;   // rows with more candidates histogram them in LDS first
 constexpr int kHCopies = 16;           // copies of each candidate histogram (row r adds to copy r % 16)
 constexpr uint32_t kDiagCount = 4u;    // diagnostics: the row counts of a segment did not add up to k_l
+// R_IT of a top-k segment on a many-row layout whose threshold key T is shared by more listed
+// candidates than win: k_rowcount counts each row's keys equal to T, k_rowscan finds the last
+// winner among them (R_NEED of them win, in index order) and writes the real R_IT.
+constexpr uint32_t kTieRows = 0xFFFFFFFEu;
 
 // Workgroup-wide AND and OR of per-thread values; `lds` holds 2 * kSelNT / 64 words.
 __device__ __forceinline__ void block_and_or(uint32_t& a, uint32_t& o, uint32_t* lds) {
@@ -1254,7 +1258,8 @@ struct LocalPos {
 template <typename K, typename I>
 __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
                                                   uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
-                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out);
+                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out,
+                                                  uint32_t* defer_need = nullptr);
 template <int GDT, bool FUSED>
 __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
@@ -2026,7 +2031,8 @@ __device__ __forceinline__ void rank_select(const uint32_t* sk, const uint32_t* 
 template <typename K, typename I>
 __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
                                                   uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
-                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out) {
+                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out,
+                                                  uint32_t* defer_need) {
   __shared__ uint32_t s_n;
   if (m <= kRankList) {
     for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
@@ -2080,15 +2086,23 @@ __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, ui
     rank_select(gk, gi, cnt, need, T_out, IT_out);
     return;
   }
-  // more than kRankList entries share the full key': ties ordered by index
+  // more than kRankList entries share the full key': ties ordered by index (with defer_need, the
+  // caller resolves them: IT_out = kTieRows, *defer_need = how many of them win)
   T_out = prefix;
-  IT_out = need >= cnt ? 0xFFFFFFFFu : block_nth_smallest_tie(key, idx, m, prefix, need, hist, lds) + 1u;
+  if (need >= cnt) {
+    IT_out = 0xFFFFFFFFu;
+  } else if (defer_need) {
+    IT_out = kTieRows;
+    *defer_need = need;
+  } else {
+    IT_out = block_nth_smallest_tie(key, idx, m, prefix, need, hist, lds) + 1u;
+  }
 }
 
 template <typename K>
 __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint32_t m, uint32_t need,
                                                uint32_t* hist, uint32_t* lds, uint32_t* gk, uint32_t* gi,
-                                               uint32_t& T_out, uint32_t& IT_out) {
+                                               uint32_t& T_out, uint32_t& IT_out, uint32_t* defer_need = nullptr) {
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
   if (m > kRankList) {
     for_keys(key, m, [&](uint32_t, uint32_t k) {
@@ -2097,7 +2111,7 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
     });
     block_and_or(kand, kor, lds);
   }
-  list_threshold_ao(key, idx, m, need, kand, kor, hist, lds, gk, gi, T_out, IT_out);
+  list_threshold_ao(key, idx, m, need, kand, kor, hist, lds, gk, gi, T_out, IT_out, defer_need);
 }
 
 // Per segment: the exact threshold among the listed candidates, then every row's message offset;
@@ -2316,9 +2330,15 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
         ws.counts[r0 + x] = (hi - lo) | kAccRow;
       }
       if (x - a < kPer) {
+        uint32_t now = 0;
 #pragma unroll
         for (uint32_t y = 0; y < kPer; ++y)
-          if (y == x - a) cr[y] += take;
+          if (y == x - a) {
+            cr[y] += take;
+            now = cr[y];
+          }
+        // (many-row layouts: k_rowcount keeps the winner count of a row emitted from acc)
+        if (take) rcw[x] = now;
       } else {
         rcw[x] += take;  // re-read by this thread below
       }
@@ -2406,9 +2426,13 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     __syncthreads();
     // need == 0 (random-k only): the certain winners, keys below ulo, are all the winners
     uint32_t Tk = KIND == 1 ? ~T.seg_ulo[l] : 0u, IT = 0;
+    // many-row top-k layouts: ties at the threshold key are ordered by index through the rows
+    // (a list of millions of equal keys, as bf16 gradients give, took one workgroup 7-14 ms)
+    uint32_t tneed = 0;
+    uint32_t* defer = KIND == 0 && BIG ? &tneed : nullptr;
     if (need > 0) {
-      if (in_lds) list_threshold(s_key, s_idx, m, need, hist, lds, s_gk, s_gi, Tk, IT);
-      else list_threshold(lk, li, m, need, hist, lds, s_gk, s_gi, Tk, IT);
+      if (in_lds) list_threshold(s_key, s_idx, m, need, hist, lds, s_gk, s_gi, Tk, IT, defer);
+      else list_threshold(lk, li, m, need, hist, lds, s_gk, s_gi, Tk, IT, defer);
       // the list's winners join their rows' counts
       const uint32_t c0 = o / kTile;
       for (uint32_t j = threadIdx.x; j < (BIG ? 0u : m); j += kSelNT) {
@@ -2423,6 +2447,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     if (threadIdx.x == 0) {
       R[R_T] = Tk;
       R[R_IT] = IT;
+      if (IT == kTieRows) R[R_NEED] = tneed;
     }
     if (!BIG && !rows_lds) {
       // the additions went to global memory: order them before re-reading the counts
@@ -2470,25 +2495,21 @@ __global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws0, Batch BT) 
   const uint32_t* R = res_of(ws, l);
   if (R[R_SLOW]) return;
   const uint32_t cw = ws.counts[row], cnt = cw & ~kAccRow;
+  // a row emitted from acc (winning ties): k_select wrote its winner count (its stored candidates,
+  // which all win, and the ties it takes)
+  if (KIND == 0 && (cw & kAccRow)) return;
   const uint32_t co = row_entry(T, ws, row, cnt, ws.coff[row]);
-  uint32_t won = 0;
+  uint32_t won = 0, tie = 0;
+  bool defer = false;  // ties at T resolved by k_rowscan: count them apart
   if (KIND == 1 || R[R_MODE] == 0) {
     const uint32_t Tk = R[R_T], IT = R[R_IT];
-    if (KIND == 0 && (cw & kAccRow)) {  // winning ties: the row's elements in acc
-      const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
-      uint32_t lo, hi;
-      row_bounds(T, row, lo, hi);
-      for (uint32_t i = lo + threadIdx.x; i < hi; i += kNT) {
-        const uint32_t k = mag_key(acc[i]);
-        won += (k > Tk || (k == Tk && i < IT)) ? 1u : 0u;
-      }
-    } else {
-      const uint32_t* ck = ws.cand_key + co;
-      const uint32_t* ci = ws.cand_idx + co;
-      for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
-        const uint32_t k = ck[j];
-        won += (k > Tk || (k == Tk && ci[j] < IT)) ? 1u : 0u;
-      }
+    defer = KIND == 0 && IT == kTieRows;
+    const uint32_t* ck = ws.cand_key + co;
+    const uint32_t* ci = ws.cand_idx + co;
+    for (uint32_t j = threadIdx.x; j < cnt; j += kNT) {
+      const uint32_t k = ck[j];
+      won += (k > Tk || (!defer && k == Tk && ci[j] < IT)) ? 1u : 0u;
+      tie += defer && k == Tk ? 1u : 0u;
     }
   } else {
     won = threadIdx.x == 0 ? cnt : 0u;
@@ -2496,11 +2517,19 @@ __global__ __launch_bounds__(kNT) void k_rowcount(Tables T, WSel ws0, Batch BT) 
   uint32_t tot;
   (void)block_excl_scan<kNT>(won, lds, tot);
   if (threadIdx.x == 0) ws.rcnt[row] = tot;
+  if (defer) {  // uniform
+    (void)block_excl_scan<kNT>(tie, lds, tot);
+    if (threadIdx.x == 0) ws.rtie[row] = tot;
+  }
 }
 
 // Large layouts, per segment: message offset of every row (exclusive scan of the winner counts),
 // in tiles of kSelNT * 8 rows: coalesced loads into LDS, eight consecutive rows per thread, a
-// workgroup scan, coalesced stores.
+// workgroup scan, coalesced stores.  A top-k segment whose threshold key T is shared by more
+// candidates than win (R_IT = kTieRows) first scans the rows' counts of keys equal to T the same
+// way: the row where the R_NEED-th falls, then that tie inside the row's candidates (stored in
+// index order) give R_IT, and the rows before it add all their ties to their winners, the row
+// itself the ties up to that one.
 __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT) {
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   constexpr uint32_t kU = 8, kTl = kSelNT * kU;
@@ -2512,14 +2541,66 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
   if (R[R_SLOW]) return;
   const uint32_t r0 = (uint32_t)T.seg_cbase[l], nr = (uint32_t)T.seg_cbase[l + 1] - r0;
   const uint32_t* cnt = ws.rcnt + r0;
+  const uint32_t* rt = ws.rtie + r0;
   uint32_t* roff = ws.roff + r0;
+  const bool defer = R[R_IT] == kTieRows;  // uniform
+  __shared__ uint32_t s_row, s_rank;
+  if (defer) {
+    const uint32_t need = R[R_NEED];
+    if (threadIdx.x == 0) {
+      s_row = nr;
+      s_rank = 0;
+    }
+    uint32_t before = 0;  // ties in earlier tiles
+    for (uint32_t t0 = 0; t0 < nr; t0 += kTl) {
+      uint32_t v[kU];
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        const uint32_t x = t0 + u * kSelNT + threadIdx.x;
+        v[u] = x < nr ? rt[x] : 0u;
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) s_c[pad(u * kSelNT + threadIdx.x)] = v[u];
+      __syncthreads();
+      uint32_t sum = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        v[u] = s_c[pad(threadIdx.x * kU + u)];
+        sum += v[u];
+      }
+      uint32_t tot;
+      uint32_t run = before + block_excl_scan<kSelNT>(sum, lds, tot);
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        if (run < need && need <= run + v[u]) {
+          s_row = t0 + threadIdx.x * kU + u;
+          s_rank = need - run;
+        }
+        run += v[u];
+      }
+      before += tot;
+      __syncthreads();
+    }
+    __syncthreads();
+    // the s_rank-th key equal to T among the row's candidates (index order): the last winner
+    const uint32_t sr = s_row;
+    if (sr < nr) {
+      const uint32_t row = r0 + sr, c = ws.counts[row];
+      const uint32_t co = row_entry(T, ws, row, c, ws.coff[row]);
+      const uint32_t p = block_nth_equal(ws.cand_key + co, c, R[R_T], s_rank, lds);
+      if (threadIdx.x == 0) res_of(ws, l)[R_IT] = ws.cand_idx[co + p] + 1u;
+    }
+  }
+  const uint32_t srow = defer ? s_row : 0u, srank = defer ? s_rank : 0u;  // no ties to add: none
   uint32_t carry = (uint32_t)T.seg_P[l], total = 0;
   for (uint32_t t0 = 0; t0 < nr; t0 += kTl) {
     uint32_t v[kU];
 #pragma unroll
     for (uint32_t u = 0; u < kU; ++u) {
       const uint32_t x = t0 + u * kSelNT + threadIdx.x;
-      v[u] = x < nr ? cnt[x] : 0u;
+      // (ties at T: all of a row before srow win, srank of row srow)
+      const uint32_t tk = x < srow ? rt[x] : (x == srow ? srank : 0u);
+      v[u] = x < nr ? cnt[x] + tk : 0u;
     }
 #pragma unroll
     for (uint32_t u = 0; u < kU; ++u) s_c[pad(u * kSelNT + threadIdx.x)] = v[u];
