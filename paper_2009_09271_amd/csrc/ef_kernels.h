@@ -1498,8 +1498,8 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
-      // random-k, direct lists: stored below, once the certain winners are known
-      if (!(KIND == 1 && direct)) store4m(acc_out, i0, vm[r], v[r]);
+      // random-k: stored below, once the candidates are known
+      if constexpr (KIND == 0) store4m(acc_out, i0, vm[r], v[r]);
     }
   } else if (KIND == 1 && !src) {
     // random-k without data (a selection prepared ahead of the step): keys and positions only
@@ -1571,18 +1571,18 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     if (lane == 0) s_tie[wid] = ntie;
   }
   if constexpr (FUSED && KIND == 1) {
-    // random-k, direct lists: the residual is +0 at the certain winners (every one of them is sent
-    // unless the segment takes the exact path, which puts their values back first), so the emit
-    // kernel only zeroes the winners from the undecided window
-    if (direct) {
+    // random-k: the residual is stored as +0 at every candidate; the emit kernel puts the value
+    // back at the few candidates that do not win (the window's losers, about 6 sqrt(k_l) + 32 of a
+    // segment), and the exact path puts them all back first.  Zeroing the winners afterwards
+    // instead wrote single words into lines long evicted from the caches: 1e9 elements at 10 %,
+    // 1.9 of the emission's 2.3 ms.
 #pragma unroll
-      for (int r = 0; r < kSR; ++r) {
-        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
-        float o[4];
+    for (int r = 0; r < kSR; ++r) {
+      const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
+      float o[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = ((cbits >> (4 * r + q)) & 1u) ? 0.0f : v[r][q];
-        store4m(acc_out, i0, vm[r], o);
-      }
+      for (int q = 0; q < 4; ++q) o[q] = ((mask[r] >> q) & 1u) ? 0.0f : v[r][q];
+      store4m(acc_out, i0, vm[r], o);
     }
   }
   __syncthreads();
@@ -1617,14 +1617,12 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       if (threadIdx.x == 0) atomicOr(&R[R_OVF], 1u);
     }
     if constexpr (FUSED && KIND == 1) {
-      // random-k, direct lists: the certain winners' values were stored as +0 above; without the
-      // candidates the exact path cannot restore them, so they are stored again now
-      if (direct) {
+      // random-k: the candidates' values were stored as +0 above; without the candidates the exact
+      // path cannot restore them, so they are stored again now
 #pragma unroll
-        for (int r = 0; r < kSR; ++r) {
-          const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
-          store4m(acc_out, i0, vm[r], v[r]);
-        }
+      for (int r = 0; r < kSR; ++r) {
+        const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
+        store4m(acc_out, i0, vm[r], v[r]);
       }
     }
   }
@@ -2261,18 +2259,14 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   }
   if (slow) {
     if constexpr (KIND == 1) {
-      if (direct && e_zero) {
-        // the streaming pass stored +0 at the certain winners (keys below ulo); the exact path needs
-        // acc there: every certain winner is a candidate, whose value its row slot keeps
-        // (a row whose candidates did not fit stored acc there itself)
-        const uint32_t ulo = T.seg_ulo[l];
-#pragma unroll
-        for (uint32_t x = 0; x < kPer; ++x) {
-          if (a + x >= b || co[x] == kDropped) continue;
-          const size_t sl = co[x];
-          const uint32_t cnt = cn[x];
-          for (uint32_t j = 0; j < cnt; ++j)
-            if (~ws.cand_key[sl + j] < ulo) e_zero[ws.cand_idx[sl + j]] = ws.cand_val[sl + j];
+      if (e_zero) {
+        // the streaming pass stored +0 at every candidate; the exact path needs acc there, which
+        // the candidates keep (a row whose candidates did not fit stored acc there itself)
+        for (uint32_t x = a; x < b; ++x) {
+          const uint32_t cnt = cc[x];
+          const uint32_t sl = T.L == 1 ? first_entry(x, cnt) : ro[x];
+          if (sl == kDropped) continue;
+          for (uint32_t j = 0; j < cnt; ++j) e_zero[ws.cand_idx[(size_t)sl + j]] = ws.cand_val[(size_t)sl + j];
         }
         __threadfence();
         __syncthreads();
@@ -2591,43 +2585,49 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
       if (threadIdx.x == 0) res_of(ws, l)[R_IT] = ws.cand_idx[co + p] + 1u;
     }
   }
-  const uint32_t srow = defer ? s_row : 0u, srank = defer ? s_rank : 0u;  // no ties to add: none
   uint32_t carry = (uint32_t)T.seg_P[l], total = 0;
-  for (uint32_t t0 = 0; t0 < nr; t0 += kTl) {
-    uint32_t v[kU];
+  // the offsets pass, with the ties of the rows up to s_row added to their winners or without
+  auto offsets = [&](auto with_ties) {
+    constexpr bool TI = decltype(with_ties)::value;
+    const uint32_t srow = TI ? s_row : 0u, srank = TI ? s_rank : 0u;
+    for (uint32_t t0 = 0; t0 < nr; t0 += kTl) {
+      uint32_t v[kU];
 #pragma unroll
-    for (uint32_t u = 0; u < kU; ++u) {
-      const uint32_t x = t0 + u * kSelNT + threadIdx.x;
-      // (ties at T: all of a row before srow win, srank of row srow)
-      const uint32_t tk = x < srow ? rt[x] : (x == srow ? srank : 0u);
-      v[u] = x < nr ? cnt[x] + tk : 0u;
+      for (uint32_t u = 0; u < kU; ++u) {
+        const uint32_t x = t0 + u * kSelNT + threadIdx.x;
+        uint32_t tk = 0;  // ties at T: all of a row before srow win, srank of row srow
+        if constexpr (TI) tk = x < srow ? rt[x] : (x == srow ? srank : 0u);
+        v[u] = x < nr ? cnt[x] + tk : 0u;
+      }
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) s_c[pad(u * kSelNT + threadIdx.x)] = v[u];
+      __syncthreads();
+      uint32_t sum = 0;
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        v[u] = s_c[pad(threadIdx.x * kU + u)];
+        sum += v[u];
+      }
+      uint32_t tot;
+      uint32_t run = carry + block_excl_scan<kSelNT>(sum, lds, tot);
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        s_c[pad(threadIdx.x * kU + u)] = run;
+        run += v[u];
+      }
+      __syncthreads();
+#pragma unroll
+      for (uint32_t u = 0; u < kU; ++u) {
+        const uint32_t x = t0 + u * kSelNT + threadIdx.x;
+        if (x < nr) roff[x] = s_c[pad(u * kSelNT + threadIdx.x)];
+      }
+      __syncthreads();
+      carry += tot;
+      total += tot;
     }
-#pragma unroll
-    for (uint32_t u = 0; u < kU; ++u) s_c[pad(u * kSelNT + threadIdx.x)] = v[u];
-    __syncthreads();
-    uint32_t sum = 0;
-#pragma unroll
-    for (uint32_t u = 0; u < kU; ++u) {
-      v[u] = s_c[pad(threadIdx.x * kU + u)];
-      sum += v[u];
-    }
-    uint32_t tot;
-    uint32_t run = carry + block_excl_scan<kSelNT>(sum, lds, tot);
-#pragma unroll
-    for (uint32_t u = 0; u < kU; ++u) {
-      s_c[pad(threadIdx.x * kU + u)] = run;
-      run += v[u];
-    }
-    __syncthreads();
-#pragma unroll
-    for (uint32_t u = 0; u < kU; ++u) {
-      const uint32_t x = t0 + u * kSelNT + threadIdx.x;
-      if (x < nr) roff[x] = s_c[pad(u * kSelNT + threadIdx.x)];
-    }
-    __syncthreads();
-    carry += tot;
-    total += tot;
-  }
+  };
+  if (defer) offsets(std::true_type{});
+  else offsets(std::false_type{});
   if (threadIdx.x == 0 && total != (uint32_t)T.seg_k[l]) atomicOr(ws.diag, kDiagCount);
 }
 
@@ -2644,7 +2644,7 @@ __global__ __launch_bounds__(kSelNT) void k_rowscan(Tables T, WSel ws0, Batch BT
 // last kernel, it also clears the overflow pool's counters for the next step.
 template <uint32_t RW, bool ACC_ROWS>
 __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_idx, float* out_val, Batch BT,
-                                              int certain_zeroed) {
+                                              int cand_zeroed) {
   static_assert(RW >= 1 && RW <= 64 && (RW & (RW - 1)) == 0, "one lane per row, a power of two");
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   float* e_zero = BT.e[blockIdx.y];
@@ -2657,7 +2657,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
   if (blockIdx.x == 0 && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
   const uint32_t myrow = row0 + lane;
   const bool has_row = lane < RW && myrow < (uint32_t)T.nrows;
-  uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, ulo = 0, co = 0, in_acc = 0;
+  uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, co = 0, in_acc = 0;
   if (has_row) {
     const int l = T.L == 1 ? 0 : T.row_seg[myrow];  // one segment: no load before the record
     const uint32_t* R = res_of(ws, l);
@@ -2665,7 +2665,6 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
     co = ws.coff[myrow];
     off = ws.roff[myrow];
     pend = (uint32_t)T.seg_P[l + 1];
-    ulo = certain_zeroed ? T.seg_ulo[l] : 0u;
     Tk = R[R_T];
     IT = R[R_IT];
     if (ACC_ROWS && (cnt & kAccRow)) {  // the row's first element in acc
@@ -2721,7 +2720,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
       const uint32_t rpre = __shfl(pre, (int)r, 64);
       const uint32_t rTk = __shfl(Tk, (int)r, 64), rIT = __shfl(IT, (int)r, 64);
       const uint32_t roffr = __shfl(off, (int)r, 64) + __shfl(done, (int)r, 64);
-      const uint32_t rpend = __shfl(pend, (int)r, 64), rulo = __shfl(ulo, (int)r, 64);
+      const uint32_t rpend = __shfl(pend, (int)r, 64);
       const uint32_t ck = k, ci = i;
       const float cv = v;
       // the next pass's candidates, in flight while this pass is written
@@ -2738,10 +2737,10 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
       if (win && pos < rpend) {
         out_idx[pos] = ci;
         if (out_val) out_val[pos] = cv;
-        // random-k, direct lists: the streaming pass already zeroed e at the certain winners (key' of
-        // a key below ulo)
-        if (e_zero && !(~ck < rulo)) e_zero[ci] = 0.0f;
+        if (e_zero && !cand_zeroed) e_zero[ci] = 0.0f;
       }
+      // random-k: the streaming pass stored +0 at every candidate: a losing one gets its value back
+      if (e_zero && cand_zeroed && in && !win) e_zero[ci] = cv;
       // each row lane adds its winners of this pass
       if (has_row) {
         const uint32_t a = pre > f0 ? pre - f0 : 0u, z = incl > f0 ? min(incl - f0, 64u) : 0u;

@@ -78,6 +78,7 @@ struct ef_layout {
   bool all_exact = false;  // top-k: every segment fits the sample, so the threshold is exact
   bool big = false;        // some k_l is large: row winners are counted by many workgroups
   bool rk_direct = false;  // random-k: every segment's rows and expected window fit k_select's LDS
+  uint32_t rk_emit_rw = 16;  // random-k emission: rows per wavefront
 
   Blob blob;
   size_t o_off, o_k, o_P, o_bl, o_nb, o_srank, o_urank, o_cbase, o_ro, o_tau, o_ulo, o_csf, o_csl, o_rseg, o_runseg,
@@ -183,6 +184,7 @@ void ef_layout::build() {
   {
     uint64_t bt = 0, br = 0, lsum = 0;
     std::vector<uint32_t> slot[2];  // per op, per segment: static slot entries per row
+    double musum = 0.0;             // random-k: expected candidates of the whole layout
     slot[0].assign(n, 64);
     slot[1].assign(n, 64);
     lbase.assign(n, 0);
@@ -210,6 +212,7 @@ void ef_layout::build() {
       const double mr = (double)tau[l] / 4294967296.0 * std::min(dl, (double)kTile);
       slot[0][l] = round_slot(mt + 4.0 * std::sqrt(mt) + 32.0);
       slot[1][l] = round_slot(mr + 8.0 * std::sqrt(mr) + 32.0);
+      musum += mu;
       bt += ct;
       br += cr;
       // lists: sub-list c takes the entries of the segment's rows c, c + 16, ...; each of the
@@ -235,6 +238,10 @@ void ef_layout::build() {
           soff[o][r + 1] = soff[o][r] + (uint32_t)std::min<int64_t>(slot[o][l], len);
         }
     }
+    // random-k emission: about 96 candidates per wavefront on average (16 rows of a few at low
+    // density; at 1 % a wavefront of 16 rows walked ~650 candidates in turn)
+    rk_emit_rw = 16;
+    while (rk_emit_rw > 1 && (double)rk_emit_rw * musum / (double)std::max(nrows, 1) > 96.0) rk_emit_rw /= 2;
     pB[0] = (uint64_t)std::ceil((double)(bt + 49152 + kPools * 4096) * pool / kPools) * kPools;
     pB[1] = (uint64_t)std::ceil((double)(br + 49152 + kPools * 4096) * pool / kPools) * kPools;
     lists = lsum;
@@ -567,9 +574,10 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     // candidates, so one row per wavefront for one or a few workers (the most parallel form) and,
     // for a batch, two (collection) or four (emission) for fewer, fuller wavefronts (measured on
     // 16 workers: collection 23.7 us with two, 25.8 with four; emission the same with two or
-    // four); random-k rows hold a few, 16 per wavefront
+    // four); random-k rows hold a few at low density, 16 per wavefront there, fewer as the density
+    // grows (rk_emit_rw)
     const bool wide = nw >= kWideBatch;
-    const uint32_t emit_rw = KIND == 1 ? 16u : wide ? 4u : 1u;
+    const uint32_t emit_rw = KIND == 1 ? L->rk_emit_rw : wide ? 4u : 1u;
     const uint32_t emit_rows = (kNT / 64) * emit_rw;
     const dim3 egrid((unsigned)((L->nrows + emit_rows - 1) / emit_rows), nw);
     uint32_t* idx = P.idx + (uint64_t)c0 * K;
@@ -595,10 +603,12 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
       EF_LAUNCH((k_select<KIND, false>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
     }
     EF_TRY(launched());
-    const int cz = KIND == 1 && L->rk_direct && P.e ? 1 : 0;
+    const int cz = KIND == 1 && P.e ? 1 : 0;  // random-k, fused: the candidates were stored as +0
     // (top-k rows with winning ties are emitted from acc)
     if (emit_rw == 16u) EF_LAUNCH((k_emit<16, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else if (emit_rw == 8u) EF_LAUNCH((k_emit<8, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
     else if (emit_rw == 4u) EF_LAUNCH((k_emit<4, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
+    else if (emit_rw == 2u) EF_LAUNCH((k_emit<2, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
     else EF_LAUNCH((k_emit<1, KIND == 0>), egrid, blk, 0, st, T, w, idx, val, bt, cz);
     EF_TRY(launched());
   }
