@@ -66,6 +66,7 @@ struct Tables {
   const uint32_t* seg_ulo;     // [L]   random-k: keys below ulo are winners if at most k_l are
   const uint64_t* seg_lbase;   // [L]   first entry of the segment's list region in the list arrays
   const uint32_t* seg_lq;      // [L]   entries per sub-list in that region (min(kSubLists, rows) sub-lists)
+  const uint32_t* seg_zc;      // [L]   top-k: 1 when the fused pass stores +0 at the candidates
   const int32_t* chunk_sf;     // [nchunks] first / last segment of each data tile
   const int32_t* chunk_sl;
   const int32_t* row_seg;      // [nrows] segment of each row

@@ -1402,7 +1402,8 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
 constexpr int kStrNT = 512;
 constexpr int kStrW = kStrNT / 64;     // its wavefronts
 
-template <int KIND, int GDT, bool FUSED>
+// ZC: some top-k segment of the layout has seg_zc (the form without it has no such test).
+template <int KIND, int GDT, bool FUSED, bool ZC = false>
 __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, const float* src, float* acc_out,
                                                     uint32_t s0, uint32_t s1, uint32_t step, WSel ws) {
   constexpr int kSR = (int)kTile / (4 * kStrNT);  // float4 groups per thread
@@ -1437,11 +1438,13 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
   uint32_t mode = 1, A = 0, IA = 0, sh = 0, ulo = 0;
   uint64_t tau = 0;
   const bool direct = KIND == 1 && T.rk_direct;
+  bool zc = false;  // top-k, fused: +0 stored at the candidates, not acc
   if constexpr (KIND == 0) {
     mode = R[R_MODE];
     A = R[R_A];
     IA = R[R_IA];
     sh = R[R_SH];
+    zc = ZC && FUSED && T.seg_zc[l] != 0u;
   } else {
     tau = T.seg_tau[l];
     ulo = T.seg_ulo[l];
@@ -1498,8 +1501,21 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
 #pragma unroll
       for (int q = 0; q < 4; ++q) v[r][q] = gv[r][q] + v[r][q];
-      // random-k: stored below, once the candidates are known
-      if constexpr (KIND == 0) store4m(acc_out, i0, vm[r], v[r]);
+      // top-k: stored at once (+0 at the candidates where seg_zc asks for it: the candidate rule
+      // needs only the key); random-k: stored below, once the candidates are known
+      if constexpr (KIND == 0) {
+        if (zc) {
+          float o[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint32_t k = mag_key(v[r][q]);
+            o[q] = k > A || (mode != 0 && k == A && i0 + q < IA) ? 0.0f : v[r][q];
+          }
+          store4m(acc_out, i0, vm[r], o);
+        } else {
+          store4m(acc_out, i0, vm[r], v[r]);
+        }
+      }
     }
   } else if (KIND == 1 && !src) {
     // random-k without data (a selection prepared ahead of the step): keys and positions only
@@ -1571,11 +1587,11 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     if (lane == 0) s_tie[wid] = ntie;
   }
   if constexpr (FUSED && KIND == 1) {
-    // random-k: the residual is stored as +0 at every candidate; the emit kernel puts the value
-    // back at the few candidates that do not win (the window's losers, about 6 sqrt(k_l) + 32 of a
-    // segment), and the exact path puts them all back first.  Zeroing the winners afterwards
-    // instead wrote single words into lines long evicted from the caches: 1e9 elements at 10 %,
-    // 1.9 of the emission's 2.3 ms.
+    // random-k (as top-k segments with seg_zc, above): the residual is stored as +0 at every
+    // candidate; the emit kernel puts the value back at the few candidates that do not win (the
+    // window's losers, about 6 sqrt(k_l) + 32 of a segment), and the exact path puts them all back
+    // first.  Zeroing the winners afterwards instead wrote single words into lines long evicted
+    // from the caches: 1e9 elements at 10 %, 1.9 of the emission's 2.3 ms.
 #pragma unroll
     for (int r = 0; r < kSR; ++r) {
       const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
@@ -1616,9 +1632,9 @@ __global__ __launch_bounds__(kStrNT) void k_stream_sel(Tables T, const void* g, 
     if constexpr (KIND == 0) {
       if (threadIdx.x == 0) atomicOr(&R[R_OVF], 1u);
     }
-    if constexpr (FUSED && KIND == 1) {
-      // random-k: the candidates' values were stored as +0 above; without the candidates the exact
-      // path cannot restore them, so they are stored again now
+    if (FUSED && (KIND == 1 || zc)) {
+      // the candidates' values were stored as +0 above; without the candidates the exact path
+      // cannot restore them, so they are stored again now
 #pragma unroll
       for (int r = 0; r < kSR; ++r) {
         const uint32_t i0 = tb + (uint32_t)(r * kStrNT + threadIdx.x) * 4u;
@@ -1735,8 +1751,10 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
     // A row's candidates did not fit the workspace (the sample put A far below the k_l-th key), but
     // the histogram counted them all: the rows collect again the keys of bins >= B only (those
     // above bin B are certain, bin B's are listed), as a retry (below) does.  With one segment the
-    // pool's parts start again from empty (every row is collected again).  The threshold bin being
-    // the key A itself, or the retry switched off: the exact path.
+    // pool's parts start again from empty (every row is collected again), unless the pass stored
+    // +0 at the candidates: the rows then read their old candidates to put them back into acc, so
+    // those must stay where they are.  The threshold bin being the key A itself, or the retry
+    // switched off: the exact path.
     const uint32_t A = R[R_A], sh = R[R_SH];
     if (bin < 1 || !T.tk_retry) {
       if (threadIdx.x == 0) {
@@ -1746,7 +1764,7 @@ __global__ __launch_bounds__(kSelNT) void k_resolve(Tables T, WSel ws0, Batch BT
       }
       return;
     }
-    if (T.L == 1 && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
+    if (T.L == 1 && !T.seg_zc[l] && threadIdx.x < (unsigned)kPools) *pcnt_of(ws, threadIdx.x) = 0u;
     if (threadIdx.x == 0) {
       const uint32_t b = (uint32_t)bin;
       R[R_A2] = A + ((b - 1u) << sh);  // keys above it: bins >= B
@@ -1844,6 +1862,16 @@ __device__ __forceinline__ void collect_retry(const Tables& T, const WSel& ws, c
   const uint32_t A = R[R_A], A2 = R[R_A2];
   const uint32_t r0 = (uint32_t)T.seg_cbase[l], c = (row - r0) % kSubLists, lq = T.seg_lq[l];
   const size_t sb = sublist_base(T, l, c);
+  if (BT.g[blockIdx.y] && T.seg_zc[l]) {
+    // the pass stored +0 at the row's candidates: their values go back into acc first (a dropped
+    // row's pass stored acc itself), made visible to this wavefront's reads below
+    float* accw = BT.e[blockIdx.y];
+    const uint32_t oc = ws.counts[row];
+    const uint32_t oco = row_entry(T, ws, row, oc, ws.coff[row]);
+    if (oco != kDropped)
+      for (uint32_t j = lane; j < oc; j += 64) accw[ws.cand_idx[(size_t)oco + j]] = ws.cand_val[(size_t)oco + j];
+    __threadfence();
+  }
   // pass 1: how many (above A2, and equal)
   uint32_t n = 0, nt = 0;
   for (uint32_t i0 = lo; i0 < hi; i0 += 64) {
@@ -2257,21 +2285,22 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       if (slow) atomicOr(ws.diag, kDiagSlowPath);
     }
   }
-  if (slow) {
-    if constexpr (KIND == 1) {
-      if (e_zero) {
-        // the streaming pass stored +0 at every candidate; the exact path needs acc there, which
-        // the candidates keep (a row whose candidates did not fit stored acc there itself)
-        for (uint32_t x = a; x < b; ++x) {
-          const uint32_t cnt = cc[x];
-          const uint32_t sl = T.L == 1 ? first_entry(x, cnt) : ro[x];
-          if (sl == kDropped) continue;
-          for (uint32_t j = 0; j < cnt; ++j) e_zero[ws.cand_idx[(size_t)sl + j]] = ws.cand_val[(size_t)sl + j];
-        }
-        __threadfence();
-        __syncthreads();
-      }
+  // The streaming pass stored +0 at every candidate (random-k; top-k segments with seg_zc): the
+  // exact path needs acc there, which the candidates keep (a row whose candidates did not fit
+  // stored acc there itself).  Uniform.
+  auto restore_candidates = [&]() {
+    if (!e_zero || (KIND == 0 && !T.seg_zc[l])) return;
+    for (uint32_t x = a; x < b; ++x) {
+      const uint32_t cnt = cc[x];
+      const uint32_t sl = T.L == 1 ? first_entry(x, cnt) : ro[x];
+      if (sl == kDropped) continue;
+      for (uint32_t j = 0; j < cnt; ++j) e_zero[ws.cand_idx[(size_t)sl + j]] = ws.cand_val[(size_t)sl + j];
     }
+    __threadfence();
+    __syncthreads();
+  };
+  if (slow) {
+    restore_candidates();
     slow_select<KIND>(T, l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
     return;
   }
@@ -2301,6 +2330,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
         R[R_SLOW] = 1u;
         atomicOr(ws.diag, kDiagSlowPath);
       }
+      restore_candidates();
       slow_select<KIND>(T, l, data, e_zero, out_idx, out_val, s0, s1, step, hist, lds);
       return;
     }
@@ -2321,6 +2351,16 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       if (take) {
         uint32_t lo, hi;
         row_bounds(T, r0 + x, lo, hi);
+        // the row's own candidate count moves to rtie (the emission finds its candidates with it)
+        uint32_t oc = 0;
+        if (x - a < kPer) {
+#pragma unroll
+          for (uint32_t y = 0; y < kPer; ++y)
+            if (y == x - a) oc = cn[y];
+        } else {
+          oc = cc[x];
+        }
+        ws.rtie[r0 + x] = oc;
         ws.counts[r0 + x] = (hi - lo) | kAccRow;
       }
       if (x - a < kPer) {
@@ -2342,6 +2382,16 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
     uint32_t lo, hi;
     row_bounds(T, r0 + s_row, lo, hi);
     const uint32_t A = retry_ties ? R[R_A2] : R[R_A];
+    if (e_zero && T.seg_zc[l] && !R[R_RETRY]) {
+      // the pass stored +0 at this row's candidates: back to acc before its elements are searched
+      // (+0 has the key of a tie at A = 0)
+      const uint32_t row = r0 + s_row, oc = ws.rtie[row];
+      const uint32_t co = row_entry(T, ws, row, oc, ws.coff[row]);
+      if (co != kDropped)
+        for (uint32_t j = threadIdx.x; j < oc; j += kSelNT) e_zero[ws.cand_idx[(size_t)co + j]] = ws.cand_val[(size_t)co + j];
+      __threadfence();
+      __syncthreads();
+    }
     const uint32_t p = block_nth_equal(AccKeys{data + lo}, hi - lo, A, s_rank, lds);
     if (threadIdx.x == 0) {
       R[R_T] = A;
@@ -2658,6 +2708,11 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
   const uint32_t myrow = row0 + lane;
   const bool has_row = lane < RW && myrow < (uint32_t)T.nrows;
   uint32_t cnt = 0, off = 0, Tk = 0, IT = 0, pend = 0, co = 0, in_acc = 0;
+  // rl: the pass stored +0 at this row's candidates (random-k, fused; top-k segments with seg_zc
+  // unless a candidate retry put acc back): losers get their values back, winners are left;
+  // otherwise winners get +0.  A row emitted from acc whose candidates are +0 first puts them
+  // back (rst, ocnt and oco: its own candidates).
+  uint32_t rl = 0, rst = 0, ocnt = 0, oco = 0;
   if (has_row) {
     const int l = T.L == 1 ? 0 : T.row_seg[myrow];  // one segment: no load before the record
     const uint32_t* R = res_of(ws, l);
@@ -2667,17 +2722,35 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
     pend = (uint32_t)T.seg_P[l + 1];
     Tk = R[R_T];
     IT = R[R_IT];
+    const bool zrow = e_zero && (cand_zeroed || (ACC_ROWS && T.seg_zc[l] && !R[R_RETRY]));
     if (ACC_ROWS && (cnt & kAccRow)) {  // the row's first element in acc
+      if (zrow) {
+        ocnt = ws.rtie[myrow];
+        oco = row_entry(T, ws, myrow, ocnt, co);
+        rst = oco != kDropped ? 1u : 0u;
+      }
       uint32_t hi;
       row_bounds(T, myrow, co, hi);
       cnt &= ~kAccRow;
       in_acc = 1u;
     } else {
       co = row_entry(T, ws, myrow, cnt, co);
+      rl = zrow ? 1u : 0u;
     }
-    if (R[R_SLOW]) cnt = 0;
+    if (R[R_SLOW]) {
+      cnt = 0;
+      rst = 0;
+    }
   }
   const float* acc = BT.g[blockIdx.y] ? BT.e[blockIdx.y] : BT.src[blockIdx.y];
+  if (ACC_ROWS && __ballot(rst != 0u)) {  // wave-uniform
+    for (uint32_t u = 0; u < RW; ++u) {
+      const uint32_t n = __shfl(rst, (int)u, 64) ? __shfl(ocnt, (int)u, 64) : 0u;
+      const uint32_t b0 = __shfl(oco, (int)u, 64);
+      for (uint32_t j = lane; j < n; j += 64) e_zero[ws.cand_idx[(size_t)b0 + j]] = ws.cand_val[(size_t)b0 + j];
+    }
+    __threadfence();  // before the rows' elements are read from acc
+  }
   const uint32_t incl = wave_incl_scan(cnt);
   const uint32_t total = __shfl(incl, 63, 64);
   const uint32_t pre = incl - cnt;  // this lane's row: first flattened candidate
@@ -2720,7 +2793,7 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
       const uint32_t rpre = __shfl(pre, (int)r, 64);
       const uint32_t rTk = __shfl(Tk, (int)r, 64), rIT = __shfl(IT, (int)r, 64);
       const uint32_t roffr = __shfl(off, (int)r, 64) + __shfl(done, (int)r, 64);
-      const uint32_t rpend = __shfl(pend, (int)r, 64);
+      const uint32_t rpend = __shfl(pend, (int)r, 64), rrl = __shfl(rl, (int)r, 64);
       const uint32_t ck = k, ci = i;
       const float cv = v;
       // the next pass's candidates, in flight while this pass is written
@@ -2737,10 +2810,9 @@ __global__ __launch_bounds__(kNT) void k_emit(Tables T, WSel ws0, uint32_t* out_
       if (win && pos < rpend) {
         out_idx[pos] = ci;
         if (out_val) out_val[pos] = cv;
-        if (e_zero && !cand_zeroed) e_zero[ci] = 0.0f;
+        if (e_zero && !rrl) e_zero[ci] = 0.0f;
       }
-      // random-k: the streaming pass stored +0 at every candidate: a losing one gets its value back
-      if (e_zero && cand_zeroed && in && !win) e_zero[ci] = cv;
+      if (e_zero && rrl && in && !win) e_zero[ci] = cv;  // a losing candidate stored as +0: its value
       // each row lane adds its winners of this pass
       if (has_row) {
         const uint32_t a = pre > f0 ? pre - f0 : 0u, z = incl > f0 ? min(incl - f0, 64u) : 0u;

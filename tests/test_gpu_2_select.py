@@ -171,23 +171,31 @@ def test_pool_overflow_takes_exact_path(kind, offs, rho, tune):
     assert diag & E.DIAG_SLOW_PATH, f"diagnostics {diag:#x}"
 
 
-def test_topk_pool_overflow_retries():
+@pytest.mark.parametrize("rho,scales,must_retry", [
+    (0.001, (0.006, 0.01, 0.015, 0.02), True),
+    (0.01, (0.04, 0.06, 0.08, 0.1), False),
+], ids=["sparse", "dense"])
+def test_topk_pool_overflow_retries(rho, scales, must_retry):
     """Candidates crowded into a few rows overflow a small pool in the streaming pass; the
     histogram still counted them all, so the rows collect again only the keys of the threshold bin
-    and above, which fit.  Each pool size must give the oracle's result; at least one of them must
-    take that retry without the exact path (the exact whole-segment path costs ~0.3 s at 1e8)."""
+    and above.  Each pool size must give the oracle's result.  At 0.1 % (the residual is +0 at the
+    winners) the pool starts again from empty and at least one size must take that retry without
+    the exact path (which costs ~0.3 s at 1e8); at 1 % the pass stored +0 at the candidates, whose
+    rows put them back first, so the pool keeps them and a retry that does not fit ends on the
+    exact path."""
     import paper_2009_09271_amd as E
     d = 1 << 20
     rng = np.random.default_rng(14)
     g = rng.standard_normal(d).astype(np.float32)
     g[: d // 16] *= np.float32(100.0)  # the winners lie in the first 16 rows
     retried = []
-    for scale in (0.04, 0.06, 0.08, 0.1):
-        announce("topk pool overflow retry", scale)
-        c = Case([0, d], 0.01, tune={E.EF_TUNE_POOL: scale})
+    for scale in scales:
+        announce("topk pool overflow retry", rho, scale)
+        c = Case([0, d], rho, tune={E.EF_TUNE_POOL: scale})
         diag = _run_steps(c, "topk", [g], np.zeros(d, np.float32))
         retried.append((scale, diag))
-    assert any(dg & E.DIAG_RETRY and not dg & E.DIAG_SLOW_PATH for _, dg in retried), retried
+    if must_retry:
+        assert any(dg & E.DIAG_RETRY and not dg & E.DIAG_SLOW_PATH for _, dg in retried), retried
 
 
 def test_randk_every_element_a_candidate():
