@@ -21,6 +21,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import statistics
 import sys
 import time
 
@@ -357,7 +358,8 @@ def measure_flat1g(args, E, torch, dev, reps=20):
     of each compressor (fp32 and bf16 gradient) and the aggregate of W = 32 workers' messages; for
     the block sizes 2^8 ... 2^20 at 1 %, the block-random-k step and its aggregate.  Messages come
     from 32 workers' own gradients (drawn on the device one after another); the timed steps use
-    worker 0's gradient.  Back-to-back repetitions on one stream, timed with events."""
+    worker 0's gradient.  Back-to-back repetitions on one stream, each timed with events; the
+    median repetition is reported."""
     from workloads import WORKLOADS, worker_seed
     wl = WORKLOADS["flat1g"]
     d, W = wl.d, args.workers or wl.W
@@ -365,17 +367,19 @@ def measure_flat1g(args, E, torch, dev, reps=20):
     gen = torch.Generator(device=dev)
 
     def timed(fn):
+        # the median of the repetitions' own durations (an event between each two): a one-off
+        # stall of several ms inside one repetition moved a mean of 20 by 0.5 ms
         torch.cuda.synchronize()  # work enqueued on other streams first
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
         with torch.cuda.stream(st):
             for _ in range(3):
                 fn()
-            a.record(st)
-            for _ in range(reps):
+            ev[0].record(st)
+            for r in range(reps):
                 fn()
-            b.record(st)
+                ev[r + 1].record(st)
         torch.cuda.synchronize()
-        return a.elapsed_time(b) * 1e3 / reps
+        return statistics.median(ev[r].elapsed_time(ev[r + 1]) for r in range(reps)) * 1e3
 
     def split(fn):
         torch.cuda.synchronize()
