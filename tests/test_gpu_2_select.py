@@ -316,6 +316,27 @@ def test_topk_threshold_on_a_repeated_value():
     _run_steps(c, "topk", [g, g], np.zeros(d, np.float32))
 
 
+@pytest.mark.parametrize("d,rho,big_frac,tie_frac", [(1_000_000, 0.08, 0.07, 0.02), (1 << 22, 0.26, 0.25, 0.02)],
+                         ids=["k-below-2^20", "k-above-2^20"])
+def test_topk_list_of_equal_keys_beyond_lds(d, rho, big_frac, tie_frac):
+    """A magnitude repeated tens of thousands of times strictly inside a histogram bin, right at the
+    threshold (quantised or bf16 gradients): the listed candidates outgrow the select kernel's LDS
+    list (8192 entries) and are swept from the sub-lists in global memory; the second step, with
+    the residual carried, puts the threshold on another such value.  Without the exact path."""
+    announce("topk list beyond LDS", d, rho)
+    rng = np.random.default_rng(26)
+    u = rng.random(d)
+    sign = np.where(rng.random(d) < 0.5, np.float32(-1.0), np.float32(1.0))
+    g = (0.01 * rng.standard_normal(d)).astype(np.float32)
+    g[u < big_frac] = 1.5
+    g[(u >= big_frac) & (u < big_frac + tie_frac)] = 0.7
+    g = np.where(u < big_frac + tie_frac, g * sign, g).astype(np.float32)
+    c = Case([0, d], rho)
+    assert c.K > (d * big_frac) and c.K < d * (big_frac + tie_frac)  # the threshold is the tie value
+    diag = _run_steps(c, "topk", [g, g], np.zeros(d, np.float32), composed=False)
+    assert not diag & c.E.DIAG_SLOW_PATH, "exact whole-segment path taken"
+
+
 @pytest.mark.parametrize("offs", [[0, 3000000], [0, 5, 1234567, 1234570, 3000000]], ids=["flat", "ragged"])
 @pytest.mark.parametrize("kind", ["topk", "randk"])
 @pytest.mark.parametrize("ties", [False, True], ids=["smooth", "ties"])
