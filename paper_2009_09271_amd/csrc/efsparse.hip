@@ -514,6 +514,7 @@ struct Steps {
 // every other kernel once per kBatchMax workers (the worker is the grid's second dimension), so
 // the short latency-bound selection kernels are paid once for the batch.
 constexpr int kWideBatch = 8;  // batches of at least this many workers take the batch forms
+constexpr uint64_t kWideRows = 131072;  // ... and so do sparse calls with this many rows in all
 
 template <int KIND>
 int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream) {
@@ -586,14 +587,17 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     const unsigned nw = (unsigned)std::min(kBatchMax, P.W - c0);
     const WSel w = ws_of(c0);
     const Batch bt = batch_of(c0, (int)nw);
-    const dim3 rgrid((unsigned)L->nrows, nw), sgrid((unsigned)L->L, nw);
+    const dim3 sgrid((unsigned)L->L, nw);
     // rows per wavefront of the collection and of the emission: top-k rows hold hundreds of
     // candidates, so one row per wavefront for one or a few workers (the most parallel form) and,
     // for a batch, two (collection) or four (emission) for fewer, fuller wavefronts (measured on
     // 16 workers: collection 23.7 us with two, 25.8 with four; emission the same with two or
     // four); random-k rows hold a few at low density, 16 per wavefront there, fewer as the density
     // grows (rk_emit_rw)
-    const bool wide = nw >= kWideBatch;
+    // (one worker on a very large, sparse layout as well: 1e9 elements at 0.01-0.1 %, top-k
+    // emission 79-87 -> 28-39 us; at 1-10 %, with hundreds of candidates a row, it was slower)
+    const bool wide = nw >= kWideBatch ||
+                      ((uint64_t)nw * L->nrows >= kWideRows && (uint64_t)L->K <= 16ull * L->nrows);
     const uint32_t emit_rw = KIND == 1 ? L->rk_emit_rw : wide ? 4u : 1u;
     const uint32_t emit_rows = (kNT / 64) * emit_rw;
     const dim3 egrid((unsigned)((L->nrows + emit_rows - 1) / emit_rows), nw);
@@ -613,7 +617,8 @@ int run_select(const ef_layout* L, const Steps& P, unsigned phases, void* stream
     if (L->big) {
       EF_LAUNCH((k_select<KIND, true>), sgrid, sblk, 0, st, T, w, idx, val, P.step, bt);
       EF_TRY(launched());
-      EF_LAUNCH(k_rowcount<KIND>, rgrid, blk, 0, st, T, w, bt);
+      const dim3 cgrid1((unsigned)((L->nrows + kNT / 64 - 1) / (kNT / 64)), nw);  // a row per wavefront
+      EF_LAUNCH(k_rowcount<KIND>, cgrid1, blk, 0, st, T, w, bt);
       EF_TRY(launched());
       EF_LAUNCH(k_rowscan, sgrid, sblk, 0, st, T, w, bt);
     } else {
