@@ -77,6 +77,7 @@ struct Tables {
                                // (1024-element data tile, segment) pair with an element in common:
                                // tile, segment, its offset, size, k and message offset, 0, 0
   int32_t d, L, nchunks, nrows, nruns, nbtiles;
+  int32_t K;                   // the sum of the k_l (one segment: its k)
   int32_t rk_direct;           // random-k: k_stream_sel counts the certain winners and lists the
                                // undecided candidates of every row; k_select gathers the lists
   int32_t tk_retry;            // top-k: the candidate retry is enabled

@@ -856,6 +856,7 @@ int ef_layout_bind(ef_layout* L, void* dev, size_t bytes, void* stream) {
   T.L = L->L;
   T.nchunks = L->nchunks;
   T.nrows = L->nrows;
+  T.K = (int32_t)L->K;
   T.nruns = L->nruns;
   T.rk_direct = L->rk_direct ? 1 : 0;
   T.tk_retry = L->tk_retry != 0.0 ? 1 : 0;
