@@ -22,8 +22,12 @@
 //   k_select         per segment: the exact threshold among the listed candidates, then the
 //                    message offset of every row.  Layouts with a very large k_l instead count
 //                    and scan the rows' winners in k_rowcount and k_rowscan.
-//   k_emit           per row: the winners in index order to the message, e = +0 there.
-// A segment with fewer than k_l candidates is resolved exactly over all of its elements by
+//   k_emit           per row: the winners in index order to the message and e = +0 there (where
+//                    the pass already stored +0 at every candidate, random-k and dense top-k
+//                    segments, the losing candidates get their values back instead).
+// A top-k segment with fewer than k_l candidates, or whose candidates do not fit the workspace, is
+// collected again at a lower threshold (k_resolve sets it, k_collect re-reads the rows); only if
+// that falls short too, or for random-k, is it resolved exactly over all of its elements by
 // k_select.  Random-k's selection can also run without data, ahead of the step (the keys depend
 // only on seed, step and position); the step is then one streaming pass (k_randk_apply).
 // Block-random-k is one fused streaming pass (k_randblock_step).  The aggregates (Algorithm 1) sum
