@@ -21,6 +21,8 @@ constexpr int kSubLists = 16;                // a segment's list of undecided ca
 constexpr int kSampleMax = 32768;             // top-k threshold sample size (keys held in LDS)
 constexpr int kSampleRun = 256;               // samples per sample run (one workgroup each)
 constexpr int kSampleTotal = 16384;           // top-k: samples shared by a layout's sampled segments
+constexpr int kSampleSpacing = 16384;         // top-k, very large layouts: one sample per this many elements
+constexpr int kSampleCap = 65536;             // ... up to this many
 constexpr int kSampleMinRuns = 4;             // top-k: at least this many runs per sampled segment
 
 constexpr uint32_t kRandkTag = 0x01000000u;

@@ -1275,7 +1275,7 @@ __device__ __forceinline__ void row_bounds(const Tables& T, uint32_t row, uint32
 // ---------------------------------------------------------------------------------------------
 // One workgroup of kSampleRun threads per run: a segment of up to kSampleMax elements is sampled
 // whole (runs of consecutive positions).  A larger one, given s = runs * kSampleRun samples by the
-// layout (a share of kSampleTotal in proportion to its size, at least kSampleMinRuns runs), is
+// layout (a share of its samples in proportion to its size, at least kSampleMinRuns runs), is
 // split into s strata of equal length (to within one element) and sampled once in each, at a
 // pseudo-random position inside the stratum (stratified sampling): every part of the segment, a
 // small tensor of large values inside a flat gradient included, is represented in proportion to
