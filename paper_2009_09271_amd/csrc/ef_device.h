@@ -21,8 +21,7 @@ constexpr int kSubLists = 16;                // a segment's list of undecided ca
 constexpr int kSampleMax = 32768;             // top-k threshold sample size (keys held in LDS)
 constexpr int kSampleRun = 256;               // samples per sample run (one workgroup each)
 constexpr int kSampleTotal = 16384;           // top-k: samples shared by a layout's sampled segments
-constexpr int kSampleSpacing = 16384;         // top-k, very large layouts: one sample per this many elements
-constexpr int kSampleCap = 65536;             // ... up to this many
+constexpr int kSampleCap = 65536;             // ... or this many where the margin would hold many candidates
 constexpr int kSampleMinRuns = 4;             // top-k: at least this many runs per sampled segment
 
 constexpr uint32_t kRandkTag = 0x01000000u;

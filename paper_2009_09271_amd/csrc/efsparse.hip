@@ -109,15 +109,28 @@ void ef_layout::build() {
   ro.assign(n + 1, 0);
   all_exact = true;
   // top-k threshold sample: segments of more than kSampleMax elements share the layout's samples in
-  // proportion to their sizes (at least kSampleMinRuns runs each): kSampleTotal of them, or, on very
-  // large layouts at a density of 0.5 % or more, one per kSampleSpacing elements (up to kSampleCap).
-  // A larger sample narrows the candidate margin, and every candidate beyond k_l is a loser whose
-  // value the emission writes back into e, one scattered word each (1e9 elements: step 2.85 ->
-  // 2.67 ms at 1 %, 4.23 -> 3.99 ms at 10 %; at 0.01-0.1 % the longer sample phase cost more than
-  // the few candidates saved).
+  // proportion to their sizes (at least kSampleMinRuns runs each): kSampleTotal of them, or
+  // kSampleCap at a density of 0.5 % or more when kSampleTotal would leave more than 10^6
+  // candidates beyond the k_l (the margins of the sampled segments with 64 or more expected sampled
+  // keys above their threshold, in elements).  A larger sample narrows the margin, and at such
+  // densities every candidate beyond k_l is a loser whose value the emission writes back into e,
+  // one scattered word each (1e9 elements: step 2.86 -> 2.67 ms at 1 %, 4.21 -> 3.93 ms at 10 %;
+  // BERT flat at 10 %: 526 -> 510 us; where the margin holds few candidates, the longer sample
+  // phase costs more than it saves).
   double dbig = 0.0;
   for (int l = 0; l < n; ++l)
     if (off64[l + 1] - off64[l] > kSampleMax) dbig += (double)(off64[l + 1] - off64[l]);
+  double excess = 0.0;
+  for (int l = 0; l < n; ++l) {
+    const double dl = (double)(off64[l + 1] - off64[l]);
+    if (dl <= kSampleMax) continue;
+    const double nsl = (double)kSampleTotal * dl / dbig, mus = nsl * density;
+    // (segments with few sampled keys above the threshold: the constant part of the margin
+    // dominates there, and the excess candidates of a layer-wise layout are mostly not losers
+    // written back: BERT per layer at 1 %, 384 -> 403 us with the larger sample)
+    if (mus >= 64.0) excess += (tk_sigma * std::sqrt(mus) + tk_extra) * dl / nsl;
+  }
+  const double sample_total = density >= 0.005 && excess > 1e6 ? (double)kSampleCap : (double)kSampleTotal;
   for (int l = 0; l < n; ++l) {
     const int64_t dl = off64[l + 1] - off64[l];
     // k per segment: round-half-up of density * d_l in double, clamped to [1, d_l]
@@ -131,10 +144,7 @@ void ef_layout::build() {
     // top-k sample runs: the whole segment when it fits the sample, else its share of the samples
     int64_t runs = (dl + kSampleRun - 1) / kSampleRun;
     if (dl > kSampleMax) {
-      const double total = density >= 0.005
-                               ? std::min<double>(kSampleCap, std::max<double>(kSampleTotal, dbig / kSampleSpacing))
-                               : (double)kSampleTotal;
-      const double want = std::ceil(total * (double)dl / dbig / kSampleRun);
+      const double want = std::ceil(sample_total * (double)dl / dbig / kSampleRun);
       runs = (int64_t)std::min<double>(std::max<double>(want, kSampleMinRuns), kSampleCap / kSampleRun);
     }
     const double ns = (double)(runs * kSampleRun);
