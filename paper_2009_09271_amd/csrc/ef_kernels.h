@@ -738,13 +738,19 @@ __device__ __forceinline__ void agg_add_workers(AggLds& S, int nw, int w0, int32
 }
 
 // Workgroup b -> tile: workgroups are dispatched to the 8 XCDs in turn (b mod 8), so XCD x is
-// given the contiguous tiles [x q + min(x, r), ...) (q = n / 8, r = n mod 8; a bijection for any
-// n).  Neighbouring tiles share the cache lines of the range table and of the messages, and now
-// share an L2 as well.
+// given chunks of kXcdChunk contiguous tiles in turn (chunks x, x + 8, ...), and the tiles past
+// the last whole round of chunks in one contiguous part (a bijection for any n).  Neighbouring
+// tiles share the cache lines of the range table and of the messages, and, within a chunk, an L2;
+// the chunks spread a cluster of crowded tiles (top-k messages) over all the XCDs, where one
+// contiguous eighth of the tiles per XCD left one XCD with most of the work.
 constexpr uint32_t kXcds = 8;
+constexpr uint32_t kXcdChunk = 32;
 __device__ __forceinline__ uint32_t xcd_tile(uint32_t b, uint32_t n) {
-  const uint32_t x = b % kXcds, j = b / kXcds, q = n / kXcds, r = n % kXcds;
-  return x * q + min(x, r) + j;
+  const uint32_t x = b % kXcds, j = b / kXcds;
+  const uint32_t full = n / (kXcds * kXcdChunk) * kXcdChunk;  // each XCD's workgroups in whole rounds
+  if (j < full) return ((j / kXcdChunk) * kXcds + x) * kXcdChunk + j % kXcdChunk;
+  const uint32_t base = full * kXcds, rn = n - base, q = rn / kXcds, r = rn % kXcds;
+  return base + x * q + min(x, r) + (j - full);
 }
 
 __global__ __launch_bounds__(64) void k_agg_sparse(int32_t d, int32_t W, int32_t K, int32_t nt,
