@@ -370,4 +370,53 @@ __device__ __forceinline__ int block_resolve(const uint32_t* hist, int nb, uint3
   return bin;
 }
 
+// block_resolve for two counts at once (one scan of the histogram): the bins where the running
+// count from the top reaches need_a and need_b (a need of 0 finds nothing: bin -1).
+template <int NT>
+__device__ __forceinline__ void block_resolve2(const uint32_t* hist, int nb, uint32_t need_a, uint32_t need_b,
+                                               uint32_t* lds, int& bin_a, uint32_t& above_a, int& bin_b,
+                                               uint32_t& above_b) {
+  __shared__ int s_bin2[2];
+  __shared__ uint32_t s_above2[2];
+  constexpr int kMaxPer = (kHBins + NT - 1) / NT;
+  const int per = (nb + NT - 1) / NT;
+  const int top = nb - 1 - per * (int)threadIdx.x;
+  uint32_t h[kMaxPer];
+  uint32_t local = 0;
+#pragma unroll
+  for (int j = 0; j < kMaxPer; ++j) {
+    const int b = top - j;
+    h[j] = (j < per && b >= 0) ? hist[b] : 0u;
+    local += h[j];
+  }
+  if (threadIdx.x == 0) {
+    s_bin2[0] = s_bin2[1] = -1;
+    s_above2[0] = s_above2[1] = 0;
+  }
+  uint32_t total;
+  const uint32_t excl = block_excl_scan<NT>(local, lds, total);
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const uint32_t need = q == 0 ? need_a : need_b;
+    if (excl < need && need <= excl + local) {
+      uint32_t run = excl;
+#pragma unroll
+      for (int j = 0; j < kMaxPer; ++j) {
+        if (j < per && run + h[j] >= need) {
+          s_bin2[q] = top - j;
+          s_above2[q] = run;
+          break;
+        }
+        run += h[j];
+      }
+    }
+  }
+  __syncthreads();
+  bin_a = s_bin2[0];
+  above_a = s_above2[0];
+  bin_b = s_bin2[1];
+  above_b = s_above2[1];
+  __syncthreads();
+}
+
 }  // namespace efs

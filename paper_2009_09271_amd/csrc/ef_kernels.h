@@ -1412,10 +1412,13 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   // Key edge of the rank-th largest sampled key: the lower (or upper) edge of its top-11-bit bin,
   // refined by the next 11 bits when that bin holds more than 64 sampled keys (concentrated
   // values: an unrefined edge could take up to the whole bin's keys as candidates beyond the
-  // rank, which the candidate pool is not sized for).
-  auto rank_edge = [&](uint32_t rank, bool upper) -> uint32_t {
-    uint32_t above;
-    const int bin = block_resolve<kSelNT>(hist, kHBins, rank, lds, above);
+  // rank, which the candidate pool is not sized for).  Both ranks' bins come from one scan of
+  // the histogram.
+  const uint32_t rank = (uint32_t)T.seg_srank[l], urank = (uint32_t)T.seg_urank[l];
+  int bin_t, bin_u;
+  uint32_t above_t, above_u;
+  block_resolve2<kSelNT>(hist, kHBins, rank < ns ? rank : 0u, urank, lds, bin_t, above_t, bin_u, above_u);
+  auto rank_edge = [&](int bin, uint32_t above, uint32_t rk, bool upper) -> uint32_t {
     if (bin < 0) return 0u;
     if (hist[bin] <= 64u) return ((uint32_t)bin + (upper ? 1u : 0u)) << 20;
     for (int b = threadIdx.x; b < kHBins; b += kSelNT) hist2[b] = 0;
@@ -1425,14 +1428,13 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
     });
     __syncthreads();
     uint32_t above2;
-    const int bin2 = block_resolve<kSelNT>(hist2, kHBins, rank - above, lds, above2);
+    const int bin2 = block_resolve<kSelNT>(hist2, kHBins, rk - above, lds, above2);
     return ((uint32_t)bin << 20) + (((uint32_t)max(bin2, 0) + (upper ? 1u : 0u)) << 9);
   };
-  const uint32_t rank = (uint32_t)T.seg_srank[l], urank = (uint32_t)T.seg_urank[l];
   // rank >= sample size: every element is a candidate
-  const uint32_t thr = rank < ns ? rank_edge(rank, false) : 0u;
+  const uint32_t thr = rank < ns ? rank_edge(bin_t, above_t, rank, false) : 0u;
   // the bins resolve the range up to the upper edge of where the k-th key very likely lies
-  uint32_t top = rank_edge(urank, true);
+  uint32_t top = rank_edge(bin_u, above_u, urank, true);
   if (top <= thr || top > kmax) top = kmax;
   const uint32_t span = top - thr;
   const uint32_t sh = span < 1024u ? 0u : (uint32_t)(32 - __clz(span)) - 10u;
