@@ -1302,7 +1302,7 @@ __device__ __forceinline__ void hist_add_peel(uint32_t* h, uint32_t b) {
 // the runs of a sampled segment also clear its candidate histogram (kHCopies * kHBins words).
 static_assert(kHCopies * kHBins == kSampleMax, "a sampled segment's histogram is cleared by its samples");
 constexpr int kSampleKeysPer = kSampleMax / kSelNT;  // sample keys per thread, loaded in one round trip
-static_assert(2 * kRankList <= kHBins, "the ranked entries of an exact segment fit a histogram array");
+static_assert(2 * kRankList <= kHBins, "the ranked entries (64-bit words) of an exact segment fit a histogram array");
 
 // Positions 0, 1, ... as the indices of keys held in position order.
 struct LocalPos {
@@ -1311,7 +1311,7 @@ struct LocalPos {
 template <typename K, typename I>
 __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
                                                   uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
-                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out,
+                                                  uint64_t* g, uint32_t& T_out, uint32_t& IT_out,
                                                   uint32_t* defer_need = nullptr);
 template <int GDT, bool FUSED>
 __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0, Batch BT) {
@@ -1364,7 +1364,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   const WSel ws = ws_at(ws0, (uint64_t)blockIdx.y * BT.ws);
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[kHBins];
-  __shared__ uint32_t hist2[kHBins];
+  __shared__ __align__(8) uint32_t hist2[kHBins];
   __shared__ uint32_t lds[2 * kSelNT / 64];
   const int l = blockIdx.x;
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
@@ -1380,8 +1380,8 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
     block_and_or(kand, kor, lds);  // its barriers also publish keys[]
     // the k_l best of the segment's keys (positions as indices): hist2 holds the ranked entries
     uint32_t Tk, IT;
-    list_threshold_ao(keys, LocalPos{}, n, (uint32_t)T.seg_k[l], kand, kor, hist, lds, hist2, hist2 + kRankList,
-                      Tk, IT);
+    list_threshold_ao(keys, LocalPos{}, n, (uint32_t)T.seg_k[l], kand, kor, hist, lds,
+                      reinterpret_cast<uint64_t*>(hist2), Tk, IT);
     const uint32_t it = IT == 0xFFFFFFFFu ? IT : o + IT;  // every tie wins, or one past the last
     if (threadIdx.x == 0) {
       R[R_A] = Tk;
@@ -2091,41 +2091,48 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   }
 }
 
-// The need-th best (key' descending, then index ascending; 1 <= need <= m <= kRankList) of m
-// entries held in LDS, by counting for every entry the entries that beat it: four threads share an
-// entry, each comparing against every fourth entry.  Gives its key' and one past its index.
-__device__ __forceinline__ void rank_select(const uint32_t* sk, const uint32_t* si, uint32_t m, uint32_t need,
-                                            uint32_t& T_out, uint32_t& IT_out) {
+// An entry to be ranked as one 64-bit word: key' in the high half and the complement of the index
+// in the low half, so that one unsigned comparison orders entries by key' descending, then index
+// ascending.  The word 0 (key' 0 with index 2^32 - 1, which no element has) beats no entry; it
+// pads a ranked list to rank_pad(m) words, the stride of the ranking loop.
+__device__ __forceinline__ uint64_t rank_word(uint32_t key, uint32_t idx) {
+  return ((uint64_t)key << 32) | (uint64_t)(~idx);
+}
+__device__ __forceinline__ uint32_t rank_pad(uint32_t m) { return (m + 63u) & ~63u; }
+
+// The need-th best (1 <= need <= m <= kRankList) of m entries held in LDS as rank words, padded
+// with zero words up to rank_pad(m): every entry counts the entries that beat it.  An entry is
+// shared by 4, 8 or 16 threads (as many as the workgroup's threads allow for m entries), each
+// comparing against every 4th, 8th or 16th entry, four loads in flight per pass.  Gives its key'
+// and one past its index.
+__device__ __forceinline__ void rank_select(const uint64_t* g, uint32_t m, uint32_t need, uint32_t& T_out,
+                                            uint32_t& IT_out) {
+  static_assert(kRankList * 4 <= kSelNT, "four threads per ranked entry");
   __shared__ uint32_t s_t, s_it;
-  const uint32_t e = threadIdx.x >> 2, part = threadIdx.x & 3u;
-  uint32_t rank = 0, k = 0, i = 0;
+  const uint32_t lg = m <= kSelNT / 16 ? 4u : (m <= kSelNT / 8 ? 3u : 2u);  // log2 threads per entry
+  const uint32_t tpe = 1u << lg;
+  const uint32_t e = threadIdx.x >> lg, part = threadIdx.x & (tpe - 1u);
+  uint32_t rank = 0;
+  uint64_t v = 0;
   if (e < m) {
-    k = sk[e];
-    i = si[e];
-    // every load in bounds (j clamped to m - 1) and the tests without branches, so that a pass's
-    // eight loads are in flight together (short-circuit tests made each wait for the one before:
-    // 179 entries took 4.3 us)
-    for (uint32_t j0 = part; j0 < m; j0 += 16u) {
-      uint32_t kj[4], ij[4];
+    v = g[e];
+    // j0 + 3 tpe stays below m rounded up to 4 tpe, which divides 64: inside the padding
+    for (uint32_t j0 = part; j0 < m; j0 += 4u * tpe) {
+      uint64_t w[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t j = min(j0 + 4u * (uint32_t)u, m - 1u);
-        kj[u] = sk[j];
-        ij[u] = si[j];
-      }
+      for (int u = 0; u < 4; ++u) w[u] = g[j0 + (uint32_t)u * tpe];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t in = j0 + 4u * (uint32_t)u < m ? 1u : 0u;
-        const uint32_t gt = kj[u] > k ? 1u : 0u, eq = kj[u] == k ? 1u : 0u, lt = ij[u] < i ? 1u : 0u;
-        rank += in & (gt | (eq & lt));
-      }
+      for (int u = 0; u < 4; ++u) rank += w[u] > v ? 1u : 0u;
     }
   }
+  // the entry's threads are adjacent lanes of one wavefront
   rank += __shfl_xor(rank, 1, 64);
   rank += __shfl_xor(rank, 2, 64);
+  if (lg >= 3u) rank += __shfl_xor(rank, 4, 64);
+  if (lg >= 4u) rank += __shfl_xor(rank, 8, 64);
   if (e < m && part == 0 && rank == need - 1) {
-    s_t = k;
-    s_it = i + 1u;
+    s_t = (uint32_t)(v >> 32);
+    s_it = ~(uint32_t)v + 1u;
   }
   __syncthreads();
   T_out = s_t;
@@ -2141,16 +2148,13 @@ __device__ __forceinline__ void rank_select(const uint32_t* sk, const uint32_t* 
 template <typename K, typename I>
 __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, uint32_t m, uint32_t need,
                                                   uint32_t kand, uint32_t kor, uint32_t* hist, uint32_t* lds,
-                                                  uint32_t* gk, uint32_t* gi, uint32_t& T_out, uint32_t& IT_out,
+                                                  uint64_t* g, uint32_t& T_out, uint32_t& IT_out,
                                                   uint32_t* defer_need) {
   __shared__ uint32_t s_n;
   if (m <= kRankList) {
-    for (uint32_t j = threadIdx.x; j < m; j += kSelNT) {
-      gk[j] = key[j];
-      gi[j] = idx[j];
-    }
+    for (uint32_t j = threadIdx.x; j < rank_pad(m); j += kSelNT) g[j] = j < m ? rank_word(key[j], idx[j]) : 0ull;
     __syncthreads();
-    rank_select(gk, gi, m, need, T_out, IT_out);
+    rank_select(g, m, need, T_out, IT_out);
     return;
   }
   const uint32_t diff = kand ^ kor;
@@ -2184,16 +2188,16 @@ __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, ui
     const uint32_t pmask = known == 0 ? 0u : (known >= 32 ? 0xFFFFFFFFu : (0xFFFFFFFFu << (32 - known)));
     const uint32_t want = prefix & pmask;
     if (threadIdx.x == 0) s_n = 0;
+    for (uint32_t j = cnt + threadIdx.x; j < rank_pad(cnt); j += kSelNT) g[j] = 0ull;  // the gather fills [0, cnt)
     __syncthreads();
     for_keys(key, m, [&](uint32_t f, uint32_t k) {
       if ((k & pmask) == want) {
         const uint32_t p = atomicAdd(&s_n, 1u);
-        gk[p] = k;
-        gi[p] = idx[f];
+        g[p] = rank_word(k, idx[f]);
       }
     });
     __syncthreads();
-    rank_select(gk, gi, cnt, need, T_out, IT_out);
+    rank_select(g, cnt, need, T_out, IT_out);
     return;
   }
   // more than kRankList entries share the full key': ties ordered by index (with defer_need, the
@@ -2211,7 +2215,7 @@ __device__ __forceinline__ void list_threshold_ao(const K& key, const I& idx, ui
 
 template <typename K>
 __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint32_t m, uint32_t need,
-                                               uint32_t* hist, uint32_t* lds, uint32_t* gk, uint32_t* gi,
+                                               uint32_t* hist, uint32_t* lds, uint64_t* g,
                                                uint32_t& T_out, uint32_t& IT_out, uint32_t* defer_need = nullptr) {
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
   if (m > kRankList) {
@@ -2221,7 +2225,7 @@ __device__ __forceinline__ void list_threshold(const K& key, const K& idx, uint3
     });
     block_and_or(kand, kor, lds);
   }
-  list_threshold_ao(key, idx, m, need, kand, kor, hist, lds, gk, gi, T_out, IT_out, defer_need);
+  list_threshold_ao(key, idx, m, need, kand, kor, hist, lds, g, T_out, IT_out, defer_need);
 }
 
 // Per segment: the exact threshold among the listed candidates, then every row's message offset;
@@ -2245,8 +2249,7 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
   __shared__ uint32_t s_key[kListLds];
   __shared__ uint32_t s_idx[kListLds];
   __shared__ uint32_t s_add[kRowsLds];
-  __shared__ uint32_t s_gk[kRankList];
-  __shared__ uint32_t s_gi[kRankList];
+  __shared__ uint64_t s_g[kRankList];
   const int l = blockIdx.x;
   uint32_t* R = res_of(ws, l);
   // (one segment: no table loads before the rows' loads)
@@ -2428,7 +2431,14 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
       for (uint32_t x = a + kPer; x < b; ++x) rcw[x] = cc[x];
     }
     for (uint32_t x = a; x < b; ++x) {
-      const uint32_t t = x - a < kPer ? tl[x - a] : rt[x];
+      uint32_t t = 0;  // tl[x - a] by unrolled selects (a dynamic index would put tl in scratch)
+      if (x - a < kPer) {
+#pragma unroll
+        for (uint32_t y = 0; y < kPer; ++y)
+          if (y == x - a) t = tl[y];
+      } else {
+        t = rt[x];
+      }
       const uint32_t take = min(t, need > before ? need - before : 0u);
       if (before < need && need <= before + t) {
         s_row = x;
@@ -2570,14 +2580,14 @@ __global__ __launch_bounds__(kSelNT) void k_select(Tables T, WSel ws0, uint32_t*
         // in which ~(tau - 1) and ~ulo differ are theirs: the prefix the AND / OR sweep over the
         // list finds (1.2 us on ResNet-50 flat) comes from the window itself
         const uint32_t klo = ~(uint32_t)(T.seg_tau[l] - 1u), khi = ~T.seg_ulo[l];
-        if (in_lds) list_threshold_ao(s_key, s_idx, m, need, klo, khi, hist, lds, s_gk, s_gi, Tk, IT, defer);
-        else list_threshold_ao(lk, li, m, need, klo, khi, hist, lds, s_gk, s_gi, Tk, IT, defer);
+        if (in_lds) list_threshold_ao(s_key, s_idx, m, need, klo, khi, hist, lds, s_g, Tk, IT, defer);
+        else list_threshold_ao(lk, li, m, need, klo, khi, hist, lds, s_g, Tk, IT, defer);
       } else if (in_lds) {
         // (the AND / OR taken while staging the list spares a sweep over it: 1.1 us on ResNet-50)
         if (m > kRankList) block_and_or(sand, sor, lds);
-        list_threshold_ao(s_key, s_idx, m, need, sand, sor, hist, lds, s_gk, s_gi, Tk, IT, defer);
+        list_threshold_ao(s_key, s_idx, m, need, sand, sor, hist, lds, s_g, Tk, IT, defer);
       } else {
-        list_threshold(lk, li, m, need, hist, lds, s_gk, s_gi, Tk, IT, defer);
+        list_threshold(lk, li, m, need, hist, lds, s_g, Tk, IT, defer);
       }
       // the list's winners join their rows' counts
       const uint32_t c0 = o / kTile;
