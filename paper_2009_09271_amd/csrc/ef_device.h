@@ -19,6 +19,7 @@ constexpr int kResWords = 16;                // per-segment selection record (ui
 constexpr int kSubLists = 16;                // a segment's list of undecided candidates is kept as 16
                                               // sub-lists (row r appends to sub-list r % 16)
 constexpr int kSampleMax = 32768;             // top-k threshold sample size (keys held in LDS)
+constexpr int kExactMax = 4096;               // top-k: segments up to this size are sampled whole (exact rule)
 constexpr int kSampleRun = 256;               // samples per sample run (one workgroup each)
 constexpr int kSampleTotal = 16384;           // top-k: samples shared by a layout's sampled segments
 constexpr int kSampleCap = 65536;             // ... or this many where the margin would hold many candidates

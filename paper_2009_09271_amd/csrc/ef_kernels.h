@@ -7,7 +7,7 @@
 //
 // Top-k and random-k (Section 3) share one pipeline; no kernel synchronises across workgroups:
 //   k_sample_gather  top-k only: the keys of a sample per segment (the whole segment when it has
-//   k_sample_select  at most kSampleMax elements, else runs spread over it); per segment either
+//   k_sample_select  at most kExactMax elements, else runs spread over it); per segment either
 //                    the exact winner rule (small segments) or a candidate threshold set so that
 //                    the candidates very likely number at least k_l.
 //   k_stream_sel     per row: fused accumulate (acc = g + e, written to e), candidate test (top-k:
@@ -1290,7 +1290,7 @@ __device__ __forceinline__ void hist_add_peel(uint32_t* h, uint32_t b) {
 // ---------------------------------------------------------------------------------------------
 // Top-k sample
 // ---------------------------------------------------------------------------------------------
-// One workgroup of kSampleRun threads per run: a segment of up to kSampleMax elements is sampled
+// One workgroup of kSampleRun threads per run: a segment of up to kExactMax elements is sampled
 // whole (runs of consecutive positions).  A larger one, given s = runs * kSampleRun samples by the
 // layout (a share of its samples in proportion to its size, at least kSampleMinRuns runs), is
 // split into s strata of equal length (to within one element) and sampled once in each, at a
@@ -1301,6 +1301,7 @@ __device__ __forceinline__ void hist_add_peel(uint32_t* h, uint32_t b) {
 // tensor is either missed or over-represented many times).  Sample q = run * kSampleRun + thread;
 // the runs of a sampled segment also clear its candidate histogram (kHCopies * kHBins words).
 static_assert(kHCopies * kHBins == kSampleMax, "a sampled segment's histogram is cleared by its samples");
+static_assert(kExactMax <= kSampleMax, "a segment sampled whole fits the sample keys held in LDS");
 constexpr int kSampleKeysPer = kSampleMax / kSelNT;  // sample keys per thread, loaded in one round trip
 static_assert(2 * kRankList <= kHBins, "the ranked entries (64-bit words) of an exact segment fit a histogram array");
 
@@ -1325,7 +1326,7 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
   const uint32_t q = r - (uint32_t)T.seg_ro[l];
   uint32_t i;
   bool in = true;
-  if (n <= (uint32_t)kSampleMax) {
+  if (n <= (uint32_t)kExactMax) {
     const uint32_t j = q * kSampleRun + threadIdx.x;
     in = j < n;
     i = o + j;
@@ -1335,7 +1336,7 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
     const uint32_t a = (uint32_t)(((uint64_t)sq * n) / ns);
     const uint32_t b = (uint32_t)(((uint64_t)(sq + 1u) * n) / ns);
     const uint32_t x = philox(make_uint4(sq, 0u, 0u, kSampleTag | (uint32_t)l), 0u, 0u).x;
-    i = o + a + __umulhi(x, b - a);  // uniform in [a, b): b > a because n > kSampleMax >= ns
+    i = o + a + __umulhi(x, b - a);  // uniform in [a, b): b > a because ns <= n (runs <= n / kSampleRun)
     for (uint32_t h = sq; h < (uint32_t)(kHCopies * kHBins); h += ns) ws.hist[(size_t)l * kHCopies * kHBins + h] = 0u;
   }
   // the overflow pool's counters start from zero (the first kernel of a top-k step)
@@ -1351,7 +1352,7 @@ __global__ __launch_bounds__(kSampleRun) void k_sample_gather(Tables T, WSel ws0
 }
 
 // Per segment (one workgroup) the candidate rule of the streaming pass:
-//  * at most kSampleMax elements: the exact k_l-th largest key T over the whole segment and the
+//  * at most kExactMax elements: the exact k_l-th largest key T over the whole segment and the
 //    bound I (one past the index of the last tie sent; ties go to lower indices); the candidates
 //    are then exactly the winners (mode 1).
 //  * larger segments: A = the lower edge of the bin of the top 11 key bits that holds the
@@ -1370,7 +1371,7 @@ __global__ __launch_bounds__(kSelNT) void k_sample_select(Tables T, WSel ws0, Ba
   const uint32_t o = (uint32_t)T.seg_off[l], n = (uint32_t)T.seg_off[l + 1] - o;
   const uint32_t* sk = ws.samp + (size_t)T.seg_ro[l] * kSampleRun;
   uint32_t* R = res_of(ws, l);
-  if (n <= (uint32_t)kSampleMax) {
+  if (n <= (uint32_t)kExactMax) {
     uint32_t kand = 0xFFFFFFFFu, kor = 0u;
     for_keys<kSampleKeysPer>(sk, n, [&](uint32_t f, uint32_t k) {
       keys[f] = k;

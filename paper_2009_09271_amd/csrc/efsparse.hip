@@ -108,7 +108,7 @@ void ef_layout::build() {
   cbase.assign(n + 1, 0);
   ro.assign(n + 1, 0);
   all_exact = true;
-  // top-k threshold sample: segments of more than kSampleMax elements share the layout's samples in
+  // top-k threshold sample: segments of more than kExactMax elements share the layout's samples in
   // proportion to their sizes (at least kSampleMinRuns runs each): kSampleTotal of them, or
   // kSampleCap at a density of 0.5 % or more when kSampleTotal would leave more than 10^6
   // candidates beyond the k_l (the margins of the sampled segments with 64 or more expected sampled
@@ -119,11 +119,11 @@ void ef_layout::build() {
   // phase costs more than it saves).
   double dbig = 0.0;
   for (int l = 0; l < n; ++l)
-    if (off64[l + 1] - off64[l] > kSampleMax) dbig += (double)(off64[l + 1] - off64[l]);
+    if (off64[l + 1] - off64[l] > kExactMax) dbig += (double)(off64[l + 1] - off64[l]);
   double excess = 0.0;
   for (int l = 0; l < n; ++l) {
     const double dl = (double)(off64[l + 1] - off64[l]);
-    if (dl <= kSampleMax) continue;
+    if (dl <= kExactMax) continue;
     const double nsl = (double)kSampleTotal * dl / dbig, mus = nsl * density;
     // (segments with few sampled keys above the threshold: the constant part of the margin
     // dominates there, and the excess candidates of a layer-wise layout are mostly not losers
@@ -143,9 +143,10 @@ void ef_layout::build() {
     nb[l] = (int32_t)((dl + b - 1) / b);
     // top-k sample runs: the whole segment when it fits the sample, else its share of the samples
     int64_t runs = (dl + kSampleRun - 1) / kSampleRun;
-    if (dl > kSampleMax) {
+    if (dl > kExactMax) {
       const double want = std::ceil(sample_total * (double)dl / dbig / kSampleRun);
       runs = (int64_t)std::min<double>(std::max<double>(want, kSampleMinRuns), kSampleCap / kSampleRun);
+      runs = std::min<int64_t>(runs, dl / kSampleRun);  // strata of one element or more
     }
     const double ns = (double)(runs * kSampleRun);
     // top-k: rank of the candidate threshold inside the segment's sample of ns keys, so that the
@@ -174,7 +175,7 @@ void ef_layout::build() {
     const int64_t c0 = off64[l] / kTile, c1 = (off64[l + 1] - 1) / kTile;
     cbase[l + 1] = cbase[l] + (int32_t)(c1 - c0 + 1);
     ro[l + 1] = ro[l] + (int32_t)runs;
-    if (dl > kSampleMax) all_exact = false;
+    if (dl > kExactMax) all_exact = false;
   }
   K = P[n];
   // many-workgroup row counting: a very large k_l, or a segment with more rows than k_select's
@@ -213,13 +214,13 @@ void ef_layout::build() {
     for (int l = 0; l < n; ++l) {
       const double dl = (double)(off64[l + 1] - off64[l]), kl = (double)k[l];
       double et;
-      if (dl <= kSampleMax) {
+      if (dl <= kExactMax) {
         et = kl;
       } else {
         const double ns = (double)((ro[l + 1] - ro[l]) * kSampleRun);
         et = (double)srank[l] * dl / ns;
       }
-      const uint64_t ct = dl <= kSampleMax ? (uint64_t)kl : (uint64_t)std::min(dl, std::ceil(2.0 * et + 8.0 * kl + 256.0));
+      const uint64_t ct = dl <= kExactMax ? (uint64_t)kl : (uint64_t)std::min(dl, std::ceil(2.0 * et + 8.0 * kl + 256.0));
       // top-k residual: +0 stored at the candidates by the pass (their losers restored by the
       // emission) on dense segments (k_l >= 0.5 % of d_l, at least a row) whose candidates are
       // the winners (exact segments) or not many more than them (under 1.8 k_l expected), else +0
@@ -227,7 +228,7 @@ void ef_layout::build() {
       // line read and a line write each, so whichever set is smaller is written (on sparse or
       // small segments the winners are few either way, and a layout with no such segment keeps
       // the pass without the test: ResNet-50 per layer, 57.6 against 61.9 us)
-      zc[l] = dl >= kTile && kl >= 0.005 * dl && (dl <= kSampleMax || et <= 1.8 * kl) ? 1u : 0u;
+      zc[l] = dl >= kTile && kl >= 0.005 * dl && (dl <= kExactMax || et <= 1.8 * kl) ? 1u : 0u;
       const double mu = (double)tau[l] / 4294967296.0 * dl;
       const uint64_t cr = (uint64_t)std::min(dl, std::ceil(mu + 8.0 * std::sqrt(mu) + 64.0));
       // slots: mu + 4 sqrt(mu) + 32 for top-k's mean mu per row (its candidates above the sampled
@@ -237,7 +238,7 @@ void ef_layout::build() {
       auto round_slot = [](double x) {
         return (uint32_t)std::min<double>(kTile, std::max(32.0, std::ceil(x / 32.0) * 32.0));
       };
-      const double mt = (dl <= kSampleMax ? kl : std::min(dl, et)) / nrl;
+      const double mt = (dl <= kExactMax ? kl : std::min(dl, et)) / nrl;
       const double mr = (double)tau[l] / 4294967296.0 * std::min(dl, (double)kTile);
       slot[0][l] = round_slot(mt + 4.0 * std::sqrt(mt) + 32.0);
       slot[1][l] = round_slot(mr + 8.0 * std::sqrt(mr) + 32.0);
