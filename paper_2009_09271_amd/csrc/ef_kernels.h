@@ -2000,17 +2000,31 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
   const uint32_t lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const uint32_t row0 = (blockIdx.x * (kNT / 64) + (threadIdx.x >> 6)) * kCollectRows;
   int ls[kCollectRows];
-  uint32_t cnts[kCollectRows], cofs[kCollectRows], k0[kCollectRows];
+  uint32_t cnts[kCollectRows], cofs[kCollectRows], k0[kCollectRows], i0[kCollectRows];
+  // one segment: its record read once, in the first round trip (k_collect does not write it; read
+  // per row, each row's fields waited for again after the previous row's list stores)
+  uint32_t r_skip = 0, r_retry = 0, r_A = 0, r_sh = 0, r_B = 0;
+  if (KIND == 0 && T.L == 1) {
+    const uint32_t* R0 = res_of(ws, 0);
+    r_skip = R0[R_SLOW] | R0[R_MODE];
+    r_retry = R0[R_RETRY];
+    r_A = R0[R_A];
+    r_sh = R0[R_SH];
+    r_B = R0[R_B];
+  }
 #pragma unroll
   for (uint32_t r = 0; r < kCollectRows; ++r) {
     const uint32_t row = min(row0 + r, (uint32_t)T.nrows - 1u);
     ls[r] = T.L == 1 ? 0 : T.row_seg[row];  // one segment: no load before the segment's record
     cnts[r] = ws.counts[row];
     cofs[r] = ws.coff[row];
-    // one segment: the first 64 keys from the row's static slot, in the same round trip (used if
-    // the row's candidates are there; past the count: unused, and not loaded past the slot)
+    // one segment: the first 64 keys and indices from the row's static slot, in the same round
+    // trip (used if the row's candidates are there; past the count: unused, and not loaded past
+    // the slot)
     const uint32_t cap0 = min(ws.S, (uint32_t)T.d - row * kTile);
-    k0[r] = T.L == 1 && lane < cap0 ? ws.cand_key[(size_t)row * ws.S + lane] : 0u;
+    const bool in0 = T.L == 1 && lane < cap0;
+    k0[r] = in0 ? ws.cand_key[(size_t)row * ws.S + lane] : 0u;
+    i0[r] = in0 ? ws.cand_idx[(size_t)row * ws.S + lane] : 0u;
   }
 #pragma unroll
   for (uint32_t r = 0; r < kCollectRows; ++r) {
@@ -2020,14 +2034,15 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
     uint32_t* R = res_of(ws, l);
     uint32_t A = 0, sh = 0, B = 0, ulo = 0;
     if constexpr (KIND == 0) {
-      if (R[R_SLOW] || R[R_MODE]) continue;
-      if (R[R_RETRY]) {
+      const bool one = T.L == 1;
+      if (one ? r_skip != 0 : (R[R_SLOW] || R[R_MODE])) continue;
+      if (one ? r_retry != 0 : R[R_RETRY] != 0) {
         collect_retry(T, ws, BT, row, l, R);
         continue;
       }
-      A = R[R_A];
-      sh = R[R_SH];
-      B = R[R_B];
+      A = one ? r_A : R[R_A];
+      sh = one ? r_sh : R[R_SH];
+      B = one ? r_B : R[R_B];
     } else {
       ulo = T.seg_ulo[l];
     }
@@ -2083,7 +2098,7 @@ __global__ __launch_bounds__(kNT) void k_collect(Tables T, WSel ws0, Batch BT) {
       if (cl == 1u) {
         const uint32_t x = nb + lanes_below(bu);
         s_lk[wv][x] = k;
-        s_li[wv][x] = ci[j];
+        s_li[wv][x] = k0_ok && j0 == 0 ? i0[r] : ci[j];
       }
       nb += nu;
     }
