@@ -981,32 +981,41 @@ __global__ __launch_bounds__(kNT) void k_shared_sum(int32_t W, int32_t K, const 
 }
 
 // Standard SGD's exchange (no compression): out = (sum over workers in order, from +0.0) / W of
-// the dense gradients g[W][d].  One float4 group per thread; the loads of kDenseBatch workers are
-// in flight together.
-constexpr int kDenseBatch = 8;
+// the dense gradients g[W][d].  Two float4 groups per thread, one in each half of the groups, and
+// the loads of kDenseBatch workers in flight together (16 workers on ResNet-50's d: 287 us, 76 %
+// of 8 TB/s, against 305 us with one group and 8 loads in flight, 296 us with one group and 16).
+constexpr int kDenseBatch = 16;
 __global__ __launch_bounds__(kNT) void k_dense_average(int32_t d, int32_t W, const float* g, int average,
                                                        float* out) {
-  const uint32_t i0 = (blockIdx.x * kNT + threadIdx.x) * 4u;
-  if (i0 >= (uint32_t)d) return;
-  const int nv = (int)min(4u, (uint32_t)d - i0);
-  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int w0 = 0; w0 < W; w0 += kDenseBatch) {
-    float v[kDenseBatch][4];
+  const uint32_t ngr = ((uint32_t)d + 3u) / 4u;
+  const uint32_t half = (ngr + 1u) / 2u;
+  const uint32_t t = blockIdx.x * kNT + threadIdx.x;
+  if (t >= half) return;
 #pragma unroll
-    for (int u = 0; u < kDenseBatch; ++u)
-      if (w0 + u < W) load4(g + (size_t)(w0 + u) * d, i0, nv, v[u]);
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t gi = t + (uint32_t)h * half;
+    if (gi >= ngr) break;
+    const uint32_t i0 = gi * 4u;
+    const int nv = (int)min(4u, (uint32_t)d - i0);
+    float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int w0 = 0; w0 < W; w0 += kDenseBatch) {
+      float v[kDenseBatch][4];
 #pragma unroll
-    for (int u = 0; u < kDenseBatch; ++u)
-      if (w0 + u < W)
+      for (int u = 0; u < kDenseBatch; ++u)
+        if (w0 + u < W) load4(g + (size_t)(w0 + u) * d, i0, nv, v[u]);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) s[q] += v[u][q];
+      for (int u = 0; u < kDenseBatch; ++u)
+        if (w0 + u < W)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s[q] += v[u][q];
+    }
+    const bool pow2 = (W & (W - 1)) == 0;
+    const float inv = 1.0f / (float)W;
+    float o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = average ? agg_scale(s[q], W, pow2, inv) : s[q];
+    store4(out, i0, nv, o);
   }
-  const bool pow2 = (W & (W - 1)) == 0;
-  const float inv = 1.0f / (float)W;
-  float o[4];
-#pragma unroll
-  for (int q = 0; q < 4; ++q) o[q] = average ? agg_scale(s[q], W, pow2, inv) : s[q];
-  store4(out, i0, nv, o);
 }
 
 // ---------------------------------------------------------------------------------------------

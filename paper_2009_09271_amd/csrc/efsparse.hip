@@ -1281,7 +1281,7 @@ int ef_dense_average(const ef_layout* L, int32_t W, const float* g, int average,
   if (W < 1 || W > 65535) return EF_ERANGE;
   if (!vec_ok(g) || !vec_ok(out)) return EF_EINVAL;
   const size_t groups = ((size_t)L->d + 3) / 4;
-  EF_LAUNCH(k_dense_average, dim3((unsigned)((groups + kNT - 1) / kNT)), dim3(kNT), 0, S(stream), L->T.d, W, g,
+  EF_LAUNCH(k_dense_average, dim3((unsigned)(((groups + 1) / 2 + kNT - 1) / kNT)), dim3(kNT), 0, S(stream), L->T.d, W, g,
             average ? 1 : 0, out);
   return launched();
 }
