@@ -74,6 +74,22 @@ def test_topk_ties_and_signed_zeros(rho, offs):
     _run_steps(c, "topk", [g, g], e)
 
 
+# Segments sampled whole are ranked directly when they hold at most 256 keys, with 16, 8 or 4
+# threads per key (up to 64, 128 and 256 keys) over a list padded to a multiple of 64 words; the
+# sizes fall on both sides of each width and of the largest segment sampled whole (4096).
+RANK_SIZES = [1, 63, 64, 65, 127, 128, 129, 255, 256, 257, 4096, 4097]
+
+
+@pytest.mark.parametrize("rho", [0.02, 0.5, 1.0])
+@pytest.mark.parametrize("ties", [False, True], ids=["smooth", "ties"])
+def test_topk_segments_at_the_ranking_widths(rho, ties):
+    offs = np.concatenate([[0], np.cumsum(RANK_SIZES)]).tolist()
+    announce("topk ranking widths", offs[-1], rho, ties)
+    c = Case(offs, rho)
+    g, e = _inputs(c.d, 11, ties=ties)
+    _run_steps(c, "topk", [g, g], e)
+
+
 @pytest.mark.parametrize("kind", ["topk", "randk"])
 def test_bf16_gradient(kind):
     from workloads import to_bf16_bits
