@@ -222,13 +222,15 @@ void ef_layout::build() {
       }
       const uint64_t ct = dl <= kExactMax ? (uint64_t)kl : (uint64_t)std::min(dl, std::ceil(2.0 * et + 8.0 * kl + 256.0));
       // top-k residual: +0 stored at the candidates by the pass (their losers restored by the
-      // emission) on dense segments (k_l >= 0.5 % of d_l, at least a row) whose candidates are
-      // the winners (exact segments) or not many more than them (under 1.8 k_l expected), else +0
-      // stored at the winners by the emission; single words written into evicted lines cost a
-      // line read and a line write each, so whichever set is smaller is written (on sparse or
-      // small segments the winners are few either way, and a layout with no such segment keeps
-      // the pass without the test: ResNet-50 per layer, 57.6 against 61.9 us)
-      zc[l] = dl >= kTile && kl >= 0.005 * dl && (dl <= kExactMax || et <= 1.8 * kl) ? 1u : 0u;
+      // emission) on dense sampled segments (k_l >= 0.5 % of d_l) whose candidates are not many
+      // more than the winners (under 1.8 k_l expected), else +0 stored at the winners by the
+      // emission; single words written into evicted lines cost a line read and a line write
+      // each, so whichever set is smaller is written.  On sparse or small segments the winners
+      // are few either way, and a layout with no such segment keeps the pass without the test
+      // (ResNet-50 per layer, 57.6 against 61.9 us); segments sampled whole are left out for that
+      // reason: their few winners did not pay for the test over the whole layout (ResNet-50 per
+      // layer at 1 %, whose 4096-element layers qualified: 114.1 -> 110.7 us per step)
+      zc[l] = dl > kExactMax && kl >= 0.005 * dl && et <= 1.8 * kl ? 1u : 0u;
       const double mu = (double)tau[l] / 4294967296.0 * dl;
       const uint64_t cr = (uint64_t)std::min(dl, std::ceil(mu + 8.0 * std::sqrt(mu) + 64.0));
       // slots: mu + 4 sqrt(mu) + 32 for top-k's mean mu per row (its candidates above the sampled
