@@ -130,7 +130,24 @@ void ef_layout::build() {
     // written back: BERT per layer at 1 %, 384 -> 403 us with the larger sample)
     if (mus >= 64.0) excess += (tk_sigma * std::sqrt(mus) + tk_extra) * dl / nsl;
   }
-  const double sample_total = density >= 0.005 && excess > 1e6 ? (double)kSampleCap : (double)kSampleTotal;
+  // Multi-segment layouts: the candidates beyond k_l expected under the base sample, with each
+  // segment's own share (at least kSampleMinRuns runs).  Where they number over 4 million, four
+  // times the larger sample: BERT per layer (4.9 and 6.6 million at 5 and 10 %) 489 -> 453 us and
+  // 600 -> 576 us per step; with fewer the longer sample phase cost more than it saved (ResNet-18
+  // per layer at 10 %, 0.5 million: 95 -> 113 us; BERT per layer at 1 %, 2.6 million, with the
+  // larger sample alone: 384 -> 403 us).
+  double lexcess = 0.0;
+  for (int l = 0; l < n && n > 1; ++l) {
+    const double dl = (double)(off64[l + 1] - off64[l]);
+    if (dl <= kExactMax) continue;
+    const double kl = std::min(std::max(std::floor(density * dl + 0.5), 1.0), dl);
+    const double runs = std::min(std::max(std::ceil((double)kSampleTotal * dl / dbig / kSampleRun), (double)kSampleMinRuns),
+                                 std::min((double)(kSampleCap / kSampleRun), std::floor(dl / kSampleRun)));
+    const double ns = runs * kSampleRun, mus = ns * kl / dl;
+    lexcess += std::min(std::ceil(mus + tk_sigma * std::sqrt(mus) + tk_extra), ns) * dl / ns - kl;
+  }
+  double sample_total = density >= 0.005 && excess > 1e6 ? (double)kSampleCap : (double)kSampleTotal;
+  if (density >= 0.005 && lexcess > 4e6) sample_total = 4.0 * kSampleCap;
   for (int l = 0; l < n; ++l) {
     const int64_t dl = off64[l + 1] - off64[l];
     // k per segment: round-half-up of density * d_l in double, clamped to [1, d_l]
